@@ -1,0 +1,200 @@
+"""CPU oracle of the INT8 W8A8 linear -- TEST INFRASTRUCTURE.
+
+Only tests/, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package. It wraps ``liboracle.so`` (built from
+``oracle.c`` by :func:`build`) with NumPy-array functions. It shares no code
+with the GPU library.
+
+bf16 tensors are ``uint16`` arrays of bit patterns. Every function returns new
+arrays and follows the step of the paper's Section 3 recipe named in its
+docstring (see ``oracle.c`` for the arithmetic and the readings it takes).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+CFLAGS = ["-O2", "-fno-fast-math", "-ffp-contract=off", "-fopenmp",
+          "-shared", "-fPIC", "-std=c11", "-Wall", "-Wextra"]
+
+
+def build() -> str:
+    """Compile liboracle.so with gcc (always recompiles)."""
+    tmp = _LIB_PATH + ".tmp"
+    subprocess.run(["gcc", *CFLAGS, "-o", tmp, _SRC, "-lm"], check=True)
+    os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def use_library(path: str | None) -> None:
+    """Point the wrappers at another build of oracle.c (None: the default).
+    Used only by the mutation test, which plants mistakes in copies."""
+    global _lib, _lib_override
+    _lib_override = path
+    _lib = None
+
+
+_lib_override = None
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = _lib_override or _LIB_PATH
+    if path == _LIB_PATH and not os.path.exists(_LIB_PATH):
+        build()
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    I64 = ctypes.c_int64
+    sig = {
+        "oracle_num_threads": ([], ctypes.c_int),
+        "oracle_set_num_threads": ([ctypes.c_int], None),
+        "oracle_bf16_to_float": ([ctypes.c_uint16], ctypes.c_float),
+        "oracle_double_to_bf16": ([ctypes.c_double], ctypes.c_uint16),
+        "oracle_act_absmax": ([P, I64, I64, P], None),
+        "oracle_smooth_factors": ([P, P, I64, I64, ctypes.c_double, P], None),
+        "oracle_prepare_weight": ([P, P, I64, I64, P, P, P], None),
+        "oracle_quant_act": ([P, P, I64, I64, P, P], None),
+        "oracle_gemm_i32": ([P, P, I64, I64, I64, P], None),
+        "oracle_epilogue": ([P, P, P, P, I64, I64, P], None),
+        "oracle_w8a8_linear": ([P, P, P, P, P, I64, I64, I64, P], None),
+        "oracle_bf16_linear": ([P, P, P, I64, I64, I64, P], None),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def _c(a, dtype):
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def num_threads() -> int:
+    return _load().oracle_num_threads()
+
+
+def set_num_threads(n: int) -> None:
+    _load().oracle_set_num_threads(int(n))
+
+
+def bf16_to_float(h: int) -> float:
+    return float(_load().oracle_bf16_to_float(int(h)))
+
+
+def double_to_bf16(d: float) -> int:
+    return int(_load().oracle_double_to_bf16(float(d)))
+
+
+def act_absmax(X, M: int, K: int, s=None) -> np.ndarray:
+    """Calibration statistic s_j = max_t |X_tj| (Section 3, activation scales
+    from a profiling pass), accumulated into ``s`` if given."""
+    X = _c(X, np.uint16)
+    out = np.zeros(K, np.float32) if s is None else np.array(s, np.float32, copy=True)
+    _load().oracle_act_absmax(_p(X), M, K, _p(out))
+    return out
+
+
+def smooth_factors(act_absmax_, W, N: int, K: int, alpha: float = 0.5) -> np.ndarray:
+    """lambda_j = s_j^alpha / max_i |W_ij|^(1-alpha) (Section 3, the
+    smoothing equation), binary64 rounded once to binary32."""
+    s = _c(act_absmax_, np.float32)
+    W = _c(W, np.uint16)
+    lam = np.empty(K, np.float32)
+    _load().oracle_smooth_factors(_p(s), _p(W), N, K, float(alpha), _p(lam))
+    return lam
+
+
+def prepare_weight(W, lam, N: int, K: int):
+    """Offline weight side (Section 3): W*diag(lambda), per-output-row
+    symmetric INT8 with round to nearest. Returns (Wq, w_scale, inv_lambda)."""
+    W = _c(W, np.uint16)
+    lam = _c(lam, np.float32)
+    Wq = np.empty((N, K), np.int8)
+    ws = np.empty(N, np.float32)
+    il = np.empty(K, np.float32)
+    _load().oracle_prepare_weight(_p(W), _p(lam), N, K, _p(Wq), _p(ws), _p(il))
+    return Wq, ws, il
+
+
+def quant_act(X, inv_lam, M: int, K: int):
+    """Runtime activation side (Section 3): X*diag(1/lambda), per-token
+    dynamic symmetric INT8. Returns (Xq, x_scale)."""
+    X = _c(X, np.uint16)
+    il = _c(inv_lam, np.float32)
+    Xq = np.empty((M, K), np.int8)
+    xs = np.empty(M, np.float32)
+    _load().oracle_quant_act(_p(X), _p(il), M, K, _p(Xq), _p(xs))
+    return Xq, xs
+
+
+def gemm_i32(Xq, Wq, M: int, N: int, K: int) -> np.ndarray:
+    """acc = Xq Wq^T with exact int32 accumulation."""
+    Xq = _c(Xq, np.int8)
+    Wq = _c(Wq, np.int8)
+    C = np.empty((M, N), np.int32)
+    _load().oracle_gemm_i32(_p(Xq), _p(Wq), M, N, K, _p(C))
+    return C
+
+
+def epilogue(C, x_scale, w_scale, bias, M: int, N: int) -> np.ndarray:
+    """y = bf16(acc * s_tok * s_ch + bias), one rounding from binary64."""
+    C = _c(C, np.int32)
+    xs = _c(x_scale, np.float32)
+    ws = _c(w_scale, np.float32)
+    b = None if bias is None else _c(bias, np.uint16)
+    Y = np.empty((M, N), np.uint16)
+    _load().oracle_epilogue(_p(C), _p(xs), _p(ws), _p(b), M, N, _p(Y))
+    return Y
+
+
+def w8a8_linear(Xq, x_scale, Wq, w_scale, bias, M: int, N: int, K: int) -> np.ndarray:
+    """The int32 product and the epilogue, fused per row."""
+    Xq = _c(Xq, np.int8)
+    Wq = _c(Wq, np.int8)
+    xs = _c(x_scale, np.float32)
+    ws = _c(w_scale, np.float32)
+    b = None if bias is None else _c(bias, np.uint16)
+    Y = np.empty((M, N), np.uint16)
+    _load().oracle_w8a8_linear(_p(Xq), _p(xs), _p(Wq), _p(ws), _p(b), M, N, K, _p(Y))
+    return Y
+
+
+def bf16_linear(X, W, bias, M: int, N: int, K: int) -> np.ndarray:
+    """Protected layer (Section 3): bf16(X W^T + bias), binary64 sum."""
+    X = _c(X, np.uint16)
+    W = _c(W, np.uint16)
+    b = None if bias is None else _c(bias, np.uint16)
+    Y = np.empty((M, N), np.uint16)
+    _load().oracle_bf16_linear(_p(X), _p(W), _p(b), M, N, K, _p(Y))
+    return Y
+
+
+def recipe(X, W, bias, M: int, N: int, K: int, alpha: float = 0.5, lam=None):
+    """The whole W8A8 recipe on one linear, calibrated on X itself:
+    returns a dict of every intermediate (lambda, inv_lambda, Wq, w_scale,
+    Xq, x_scale, acc, Y)."""
+    if lam is None:
+        lam = smooth_factors(act_absmax(X, M, K), W, N, K, alpha)
+    Wq, ws, il = prepare_weight(W, lam, N, K)
+    Xq, xs = quant_act(X, il, M, K)
+    acc = gemm_i32(Xq, Wq, M, N, K)
+    Y = epilogue(acc, xs, ws, bias, M, N)
+    return {"lambda": lam, "inv_lambda": il, "Wq": Wq, "w_scale": ws,
+            "Xq": Xq, "x_scale": xs, "acc": acc, "Y": Y}

@@ -1,0 +1,301 @@
+/*
+ * oracle.c -- plain, slow CPU reference of the INT8 W8A8 quantized linear.
+ *
+ * TEST INFRASTRUCTURE. Only tests/, __graft_entry__.smoke() and the
+ * cpu_baseline leg of bench.py load this library. The product library
+ * (paper_2606_12280_amd/) never calls it, and the two share no source,
+ * header, helper or table.
+ *
+ * It follows the recipe of Section 3 ("INT8 W8A8" and "Activation-fragility
+ * profiling and protection") step by step, in the paper's order:
+ *
+ *   lambda_j = s_j^alpha / max_i |W_ij|^(1-alpha)      (the smoothing equation)
+ *   weights multiplied by lambda, activations divided by lambda (SmoothQuant)
+ *   weights: symmetric INT8 per output row, round to nearest (Section 2 notes
+ *            that plain round-to-nearest suffices at 8 bits)
+ *   activations: symmetric INT8 per token, scale computed on the fly
+ *   int8 x int8 products summed exactly in int32
+ *   rescale by s_tok * s_ch, add the bias, round once to bf16
+ *   protected layers: bf16 X times bf16 W^T plus bias, no smoothing and no
+ *            activation quantization
+ *
+ * Readings of points the paper leaves open (each one is listed, with its
+ * reason, in the design notes of the repository):
+ *   - every scalar of the quantization is binary32, one IEEE rounding per
+ *     operation, no fused multiply-add; the quantized codes depend on it, so
+ *     the GPU takes the same decisions in the same precision;
+ *   - "divide by lambda" is a multiply by inv_lambda = RN(1/lambda), computed
+ *     once per input channel;
+ *   - scale = absmax/127 and code = clamp(rint(x * RN(127/absmax)), -127, 127)
+ *     with rint = round half to even; -128 is never produced;
+ *   - a row (token or output channel) whose absmax is below 2^-96, including
+ *     an all-zero row, gets scale 0 and all-zero codes, so that 127/absmax
+ *     never overflows;
+ *   - the epilogue and the protected linear are computed in binary64 and
+ *     rounded once to bf16 (round to nearest even);
+ *   - lambda itself is computed in binary64 and rounded once to binary32; a
+ *     channel whose activation or weight statistic is zero keeps lambda = 1.
+ *
+ * Parallelism: rows are independent and each row is computed by one thread in
+ * a fixed order, so results do not depend on the thread count.
+ *
+ * Build: gcc -O2 -fno-fast-math -ffp-contract=off -fopenmp -shared -fPIC
+ */
+#include <float.h>
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORACLE_TINY_ABSMAX 0x1p-96f /* rows below this quantize to zero */
+
+/* ------------------------------------------------------------------ */
+/* bf16 <-> binary32 / binary64                                         */
+/* ------------------------------------------------------------------ */
+
+/* bf16 is the upper half of a binary32 word: widening is exact. */
+static float bf16_to_float(uint16_t h)
+{
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return f;
+}
+
+/* Round a finite binary64 value to the nearest bf16 (ties to even), in a
+ * single rounding: bf16 keeps 8 significant bits and the binary32 exponent
+ * range, with subnormals spaced 2^-133. */
+static uint16_t double_to_bf16(double d)
+{
+    const double bf16_max = 0x1.fep127; /* (2 - 2^-7) * 2^127 */
+    uint32_t u;
+    float f;
+    int e;
+    int ulp_exp;
+    double q;
+    double r;
+
+    if (d == 0.0)
+        return signbit(d) ? 0x8000u : 0x0000u;
+    frexp(fabs(d), &e);   /* |d| = m * 2^e with m in [0.5, 1) */
+    ulp_exp = e - 8;      /* spacing of 8-significant-bit numbers there */
+    if (ulp_exp < -133)
+        ulp_exp = -133;   /* subnormal bf16 spacing */
+    q = nearbyint(ldexp(d, -ulp_exp)); /* exact scaling, ties to even */
+    r = ldexp(q, ulp_exp);
+    if (fabs(r) > bf16_max)
+        return signbit(d) ? 0xff80u : 0x7f80u; /* rounds to infinity */
+    f = (float)r; /* exact: r has at most 8 significant bits */
+    memcpy(&u, &f, sizeof u);
+    return (uint16_t)(u >> 16);
+}
+
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+void oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
+/* Exported so that the tests can pin the conversions on their own. */
+float oracle_bf16_to_float(uint16_t h) { return bf16_to_float(h); }
+uint16_t oracle_double_to_bf16(double d) { return double_to_bf16(d); }
+
+/* ------------------------------------------------------------------ */
+/* Calibration (Section 3: "activation scales come from a profiling     */
+/* pass"): per-input-channel absmax over tokens, and lambda.            */
+/* ------------------------------------------------------------------ */
+
+/* s[k] = max(s[k], max_t |X[t][k]|). X is [M][K] bf16. The caller seeds s
+ * (zeros for a fresh pass); several calls accumulate over batches. */
+void oracle_act_absmax(const uint16_t *X, int64_t M, int64_t K, float *s)
+{
+    int64_t t, k;
+    for (t = 0; t < M; ++t)
+        for (k = 0; k < K; ++k) {
+            float a = fabsf(bf16_to_float(X[t * K + k]));
+            if (a > s[k])
+                s[k] = a;
+        }
+}
+
+/* lambda_j = s_j^alpha / (max_i |W_ij|)^(1 - alpha), W is [N][K] bf16 in the
+ * nn.Linear layout (row i = output channel, column j = input channel). */
+void oracle_smooth_factors(const float *act_absmax, const uint16_t *W,
+                           int64_t N, int64_t K, double alpha, float *lambda)
+{
+    int64_t n, j;
+    for (j = 0; j < K; ++j) {
+        double wmax = 0.0;
+        double s = (double)act_absmax[j];
+        for (n = 0; n < N; ++n) {
+            double a = fabs((double)bf16_to_float(W[n * K + j]));
+            if (a > wmax)
+                wmax = a;
+        }
+        if (s == 0.0 || wmax == 0.0) {
+            lambda[j] = 1.0f;
+            continue;
+        }
+        if (alpha == 0.5)
+            lambda[j] = (float)(sqrt(s) / sqrt(wmax));
+        else
+            lambda[j] = (float)(pow(s, alpha) / pow(wmax, 1.0 - alpha));
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* Smoothing and symmetric per-row INT8 quantization.                  */
+/* ------------------------------------------------------------------ */
+
+/* One row: v_k = float(src_k) * mul_k (the smoothed row, one binary32
+ * rounding), absmax over the row, scale = absmax/127, codes
+ * clamp(rint(v_k * RN(127/absmax)), -127, 127). Two passes over the row, the
+ * smoothed value recomputed in the second (it is the same binary32 number). */
+static void smooth_quantize_row(const uint16_t *src, const float *mul,
+                                int64_t K, int8_t *q, float *scale)
+{
+    int64_t k;
+    float amax = 0.0f;
+    float r;
+    for (k = 0; k < K; ++k) {
+        float a = fabsf(bf16_to_float(src[k]) * mul[k]);
+        if (a > amax)
+            amax = a;
+    }
+    if (amax < ORACLE_TINY_ABSMAX) {
+        *scale = 0.0f;
+        memset(q, 0, (size_t)K);
+        return;
+    }
+    *scale = amax / 127.0f;
+    r = 127.0f / amax;
+    for (k = 0; k < K; ++k) {
+        float v = bf16_to_float(src[k]) * mul[k];
+        float c = rintf(v * r);
+        if (c > 127.0f)
+            c = 127.0f;
+        if (c < -127.0f)
+            c = -127.0f;
+        q[k] = (int8_t)c;
+    }
+}
+
+/* Offline weight preparation: W' = W * diag(lambda) (weights scaled up),
+ * per-output-row INT8. W [N][K] bf16, lambda [K] -> Wq [N][K] int8,
+ * w_scale [N], inv_lambda [K] (the activation-side multiplier). */
+void oracle_prepare_weight(const uint16_t *W, const float *lambda, int64_t N,
+                           int64_t K, int8_t *Wq, float *w_scale,
+                           float *inv_lambda)
+{
+    int64_t n, k;
+    for (k = 0; k < K; ++k)
+        inv_lambda[k] = 1.0f / lambda[k];
+#pragma omp parallel for schedule(static)
+    for (n = 0; n < N; ++n)
+        smooth_quantize_row(W + n * K, lambda, K, Wq + n * K, &w_scale[n]);
+}
+
+/* Runtime activation path: X' = X * diag(inv_lambda) (activations scaled
+ * down), per-token INT8. X [M][K] bf16 -> Xq [M][K] int8, x_scale [M]. */
+void oracle_quant_act(const uint16_t *X, const float *inv_lambda, int64_t M,
+                      int64_t K, int8_t *Xq, float *x_scale)
+{
+    int64_t t;
+#pragma omp parallel for schedule(static)
+    for (t = 0; t < M; ++t)
+        smooth_quantize_row(X + t * K, inv_lambda, K, Xq + t * K, &x_scale[t]);
+}
+
+/* ------------------------------------------------------------------ */
+/* INT8 GEMM and epilogue.                                              */
+/* ------------------------------------------------------------------ */
+
+/* C[t][n] = sum_k Xq[t][k] * Wq[n][k], exact in int32 (|C| <= 127^2 K, which
+ * fits for K <= 133144). */
+void oracle_gemm_i32(const int8_t *Xq, const int8_t *Wq, int64_t M, int64_t N,
+                     int64_t K, int32_t *C)
+{
+    int64_t t, n, k;
+#pragma omp parallel for schedule(static) private(n, k)
+    for (t = 0; t < M; ++t)
+        for (n = 0; n < N; ++n) {
+            int32_t acc = 0;
+            for (k = 0; k < K; ++k)
+                acc += (int32_t)Xq[t * K + k] * (int32_t)Wq[n * K + k];
+            C[t * N + n] = acc;
+        }
+}
+
+/* Y[t][n] = bf16(C[t][n] * (s_tok[t] * s_ch[n]) + bias[n]), in binary64 with
+ * one final rounding. bias may be NULL (treated as zero). */
+void oracle_epilogue(const int32_t *C, const float *x_scale,
+                     const float *w_scale, const uint16_t *bias, int64_t M,
+                     int64_t N, uint16_t *Y)
+{
+    int64_t t, n;
+#pragma omp parallel for schedule(static) private(n)
+    for (t = 0; t < M; ++t)
+        for (n = 0; n < N; ++n) {
+            double b = bias ? (double)bf16_to_float(bias[n]) : 0.0;
+            double y = (double)C[t * N + n] *
+                           ((double)x_scale[t] * (double)w_scale[n]) + b;
+            Y[t * N + n] = double_to_bf16(y);
+        }
+}
+
+/* The W8A8 linear on already-quantized operands: the int32 sum and the
+ * epilogue, row by row (no int32 matrix kept). */
+void oracle_w8a8_linear(const int8_t *Xq, const float *x_scale,
+                        const int8_t *Wq, const float *w_scale,
+                        const uint16_t *bias, int64_t M, int64_t N, int64_t K,
+                        uint16_t *Y)
+{
+    int64_t t, n, k;
+#pragma omp parallel for schedule(static) private(n, k)
+    for (t = 0; t < M; ++t)
+        for (n = 0; n < N; ++n) {
+            int32_t acc = 0;
+            double b = bias ? (double)bf16_to_float(bias[n]) : 0.0;
+            double y;
+            for (k = 0; k < K; ++k)
+                acc += (int32_t)Xq[t * K + k] * (int32_t)Wq[n * K + k];
+            y = (double)acc * ((double)x_scale[t] * (double)w_scale[n]) + b;
+            Y[t * N + n] = double_to_bf16(y);
+        }
+}
+
+/* Protected layer: Y = bf16(X W^T + bias) with X, W bf16. The bf16 products
+ * are exact in binary64; they are summed in binary64 in k order, the bias is
+ * added last and the result is rounded once. bias may be NULL. */
+void oracle_bf16_linear(const uint16_t *X, const uint16_t *W,
+                        const uint16_t *bias, int64_t M, int64_t N, int64_t K,
+                        uint16_t *Y)
+{
+    int64_t t, n, k;
+#pragma omp parallel for schedule(static) private(n, k)
+    for (t = 0; t < M; ++t)
+        for (n = 0; n < N; ++n) {
+            double acc = 0.0;
+            for (k = 0; k < K; ++k)
+                acc += (double)bf16_to_float(X[t * K + k]) *
+                       (double)bf16_to_float(W[n * K + k]);
+            if (bias)
+                acc += (double)bf16_to_float(bias[n]);
+            Y[t * N + n] = double_to_bf16(acc);
+        }
+}

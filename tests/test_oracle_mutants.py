@@ -1,0 +1,100 @@
+"""Plants one mistake at a time in a copy of the CPU oracle and checks that the
+pins in test_oracle_pins.py catch it (CPU only; nothing runs on a GPU).
+
+Each mutant is a plausible slip in following the paper's Section 3 recipe: the
+smoothing direction, the rounding rule, the scale, the SmoothQuant exponent, a
+dropped bias, a wrong index. Clamping at -128 instead of -127 is not listed:
+with scale = absmax/127 and code = rint(x * RN(127/absmax)) the clamp never
+fires (|x * RN(127/absmax)| <= 127 + 2^-17 rounds to 127), so that mutant
+computes the same codes."""
+from __future__ import annotations
+
+import os
+import subprocess
+import tempfile
+
+import pytest
+
+import oracle
+import test_oracle_pins as pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
+
+MUTANTS = {
+    "smoothing_direction": ("inv_lambda[k] = 1.0f / lambda[k];", "inv_lambda[k] = lambda[k];"),
+    "weights_divided": ("smooth_quantize_row(W + n * K, lambda, K,",
+                        "smooth_quantize_row(W + n * K, inv_lambda, K,"),
+    "round_half_away": ("float c = rintf(v * r);", "float c = roundf(v * r);"),
+    "scale_over_128": ("*scale = amax / 127.0f;", "*scale = amax / 128.0f;"),
+    "reciprocal_128": ("r = 127.0f / amax;", "r = 128.0f / amax;"),
+    "absmax_signed": ("float a = fabsf(bf16_to_float(src[k]) * mul[k]);",
+                      "float a = bf16_to_float(src[k]) * mul[k];"),
+    "tiny_row_rule": ("#define ORACLE_TINY_ABSMAX 0x1p-96f", "#define ORACLE_TINY_ABSMAX 0x1p-140f"),
+    "alpha_swapped": ("pow(s, alpha) / pow(wmax, 1.0 - alpha)", "pow(s, 1.0 - alpha) / pow(wmax, alpha)"),
+    "sqrt_inverted": ("(float)(sqrt(s) / sqrt(wmax))", "(float)(sqrt(wmax) / sqrt(s))"),
+    "calib_signed": ("float a = fabsf(bf16_to_float(X[t * K + k]));", "float a = bf16_to_float(X[t * K + k]);"),
+    "gemm_unsigned_x": ("acc += (int32_t)Xq[t * K + k] * (int32_t)Wq[n * K + k];\n            C[t * N + n]",
+                        "acc += (int32_t)(uint8_t)Xq[t * K + k] * (int32_t)Wq[n * K + k];\n            C[t * N + n]"),
+    "gemm_drops_last_k": ("for (k = 0; k < K; ++k)\n                acc += (int32_t)Xq[t * K + k] * (int32_t)Wq[n * K + k];\n            C[t * N + n]",
+                          "for (k = 0; k < K - 1; ++k)\n                acc += (int32_t)Xq[t * K + k] * (int32_t)Wq[n * K + k];\n            C[t * N + n]"),
+    "epilogue_drops_bias": ("double b = bias ? (double)bf16_to_float(bias[n]) : 0.0;\n            double y = (double)C",
+                            "double b = 0.0;\n            double y = (double)C"),
+    "epilogue_scale_index": ("((double)x_scale[t] * (double)w_scale[n]) + b;\n            Y[t * N + n] = double_to_bf16(y);\n        }\n}\n\n/* The W8A8",
+                             "((double)x_scale[t] * (double)w_scale[t % N]) + b;\n            Y[t * N + n] = double_to_bf16(y);\n        }\n}\n\n/* The W8A8"),
+    "bf16_double_rounding": ("q = nearbyint(ldexp(d, -ulp_exp));", "q = nearbyint(ldexp((double)(float)d, -ulp_exp));"),
+    "bf16_subnormal_spacing": ("ulp_exp = -133;", "ulp_exp = -126;"),
+    "protected_drops_bias": ("            if (bias)\n                acc += (double)bf16_to_float(bias[n]);\n", ""),
+}
+
+# every pin, with fixed arguments for the parametrized ones
+PINS = [
+    pins.test_bf16_widening_matches_bit_layout,
+    pins.test_double_to_bf16_matches_exact_rounding,
+    lambda: pins.test_gemm_i32_matches_numpy_int64(17, 9, 128, 2),
+    pins.test_gemm_i32_extreme_magnitudes,
+    pins.test_act_absmax_matches_numpy_and_accumulates,
+    pins.test_smooth_factors_closed_forms,
+    lambda: pins.test_smoothing_balances_channel_ranges(0.25),
+    pins.test_inv_lambda_is_correctly_rounded_reciprocal,
+    pins.test_round_half_even_ties,
+    pins.test_activation_quant_invariants_tiny,
+    pins.test_weight_quant_invariants_tiny,
+    pins.test_quant_special_rows,
+    pins.test_lossless_grid_reduces_to_plain_product,
+    lambda: pins.test_w8a8_error_bound_vs_fp64("tiny"),
+    pins.test_epilogue_against_exact_rationals,
+    pins.test_bf16_linear_small_integers_exact,
+    pins.test_bf16_linear_random_vs_numpy_fp64,
+]
+
+
+def _caught() -> int:
+    n = 0
+    for pin in PINS:
+        try:
+            pin()
+        except AssertionError:
+            n += 1
+    return n
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_planted_mistake(name, tmp_path):
+    before, after = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(before) == 1, "mutation site moved"
+    c_path = tmp_path / "oracle_mut.c"
+    c_path.write_text(src.replace(before, after))
+    so_path = str(tmp_path / "liboracle_mut.so")
+    subprocess.run(["gcc", *oracle.CFLAGS, "-w", "-o", so_path, str(c_path), "-lm"], check=True)
+    oracle.use_library(so_path)
+    try:
+        caught = _caught()
+    finally:
+        oracle.use_library(None)
+    assert caught >= 1, f"no pin catches the '{name}' mutant"
+
+
+def test_unmutated_oracle_passes_every_pin():
+    oracle.use_library(None)
+    assert _caught() == 0

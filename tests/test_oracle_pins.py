@@ -1,0 +1,380 @@
+"""Pins of the CPU oracle against facts fixed outside it (CPU only).
+
+Each test checks the oracle against something other than itself: a library
+routine computing a textbook special case, a closed-form bound, an invariant,
+or brute force on tiny inputs. The recipe is the paper's Section 3 ("INT8
+W8A8"): per-output-row INT8 weights, per-token dynamic INT8 activations,
+SmoothQuant smoothing with lambda_j = s_j^alpha / max_i |W_ij|^(1-alpha), and
+bf16 protection of fragile layers. Each test names the mistake it would catch.
+"""
+from __future__ import annotations
+
+import hashlib
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from bf16ref import bf16_to_f64, round_bf16_exact, ulp_distance
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+QUANT_SLACK = 0.5 + 2.0 ** -14   # |q*s - x'| <= s*(1/2 + fp32 slack)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _built():
+    oracle.build()
+
+
+# --------------------------------------------------------------------------
+# bf16 conversions
+# --------------------------------------------------------------------------
+
+def test_bf16_widening_matches_bit_layout():
+    bits = np.array([0x0000, 0x8000, 0x3F80, 0xBF80, 0x4300, 0x0001, 0x7F7F, 0x3E80],
+                    np.uint16)
+    want = [0.0, -0.0, 1.0, -1.0, 128.0, 2.0 ** -133, float(bf16_to_f64([0x7F7F])[0]), 0.25]
+    got = [oracle.bf16_to_float(int(b)) for b in bits]
+    assert got == want
+
+
+def test_double_to_bf16_matches_exact_rounding():
+    """Ties-to-even, subnormals and overflow against brute-force rational
+    rounding (catches round-half-up, double rounding through binary32,
+    wrong subnormal spacing)."""
+    rng = np.random.default_rng(11)
+    vals = list(rng.standard_normal(300) * 10.0 ** rng.integers(-40, 38, 300))
+    # exact ties: midpoints between neighbouring bf16 values
+    for h in (0x3F80, 0x3F81, 0x4000, 0x0001, 0x0002, 0x7F7E, 0x4B00):
+        lo = Fraction(float(bf16_to_f64([h])[0]))
+        hi = Fraction(float(bf16_to_f64([h + 1])[0]))
+        mid = (lo + hi) / 2
+        vals += [float(mid), -float(mid)]
+    # a value that double-rounds wrongly through binary32: 1 + 2^-8 + 2^-30
+    vals += [1.0 + 2.0 ** -8 + 2.0 ** -30, 1.0 + 2.0 ** -8 - 2.0 ** -30]
+    vals += [3.0e38, 3.3961e38, -3.4e38, 1e-45, 2.0 ** -134, 2.0 ** -134 * 3]
+    for v in vals:
+        assert oracle.double_to_bf16(v) == round_bf16_exact(v), v
+
+
+# --------------------------------------------------------------------------
+# the int32 product
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("M,N,K,seed", [(1, 1, 64, 0), (3, 5, 64, 1), (17, 9, 128, 2),
+                                        (65, 33, 256, 3), (2, 64, 1024, 4)])
+def test_gemm_i32_matches_numpy_int64(M, N, K, seed):
+    """Brute force against NumPy's int64 matmul (catches transposed operands,
+    dropped terms, sign-extension mistakes)."""
+    A = synth.rand_i8([seed, 0], (M, K))
+    B = synth.rand_i8([seed, 1], (N, K))
+    ref = A.astype(np.int64) @ B.astype(np.int64).T
+    got = oracle.gemm_i32(A, B, M, N, K)
+    assert np.array_equal(got.astype(np.int64), ref)
+
+
+def test_gemm_i32_extreme_magnitudes():
+    """All +-127 operands at K = 16384 reach 127^2 K = 2.64e8 without overflow."""
+    K = 16384
+    A = np.full((2, K), 127, np.int8)
+    A[1] = -127
+    B = np.full((3, K), -127, np.int8)
+    B[2, ::2] = 127
+    got = oracle.gemm_i32(A, B, 2, 3, K)
+    ref = A.astype(np.int64) @ B.astype(np.int64).T
+    assert np.array_equal(got, ref)
+    assert abs(int(got[0, 0])) == 127 * 127 * K
+
+
+# --------------------------------------------------------------------------
+# calibration and the smoothing factor
+# --------------------------------------------------------------------------
+
+def test_act_absmax_matches_numpy_and_accumulates():
+    X = synth.rand_bf16(5, (37, 96), 3.0)
+    got = oracle.act_absmax(X, 37, 96)
+    assert np.array_equal(got, np.abs(bf16_to_f64(X)).max(0).astype(np.float32))
+    X2 = synth.rand_bf16(6, (5, 96), 9.0)
+    got2 = oracle.act_absmax(X2, 5, 96, got)
+    ref2 = np.maximum(got, np.abs(bf16_to_f64(X2)).max(0).astype(np.float32))
+    assert np.array_equal(got2, ref2)
+
+
+def _bf16_col(vals):
+    return synth.to_bf16_bits(np.array(vals, np.float32))
+
+
+def test_smooth_factors_closed_forms():
+    """lambda = s^a / m^(1-a) on powers of two (catches a swapped exponent,
+    s and m swapped, or max over the wrong axis of W)."""
+    # K = 4 input channels, N = 2 output rows; column maxima m = [1, 4, 2, 3]
+    W = np.stack([_bf16_col([1.0, -4.0, 0.5, 0.0]), _bf16_col([-0.25, 2.0, -2.0, 3.0])])
+    s = np.array([4.0, 1.0, 2.0, 0.0], np.float32)   # last channel: s = 0
+    lam = oracle.smooth_factors(s, W, 2, 4, 0.5)
+    assert lam.tolist() == [2.0, 0.5, 1.0, 1.0]
+    lam3 = oracle.smooth_factors(np.array([8.0, 1, 1, 1], np.float32), W, 2, 4, 1.0 / 3.0)
+    # 8^(1/3) / 1^(2/3) = 2
+    assert abs(float(lam3[0]) - 2.0) <= 2.0 * 2.0 ** -23
+    # 1^(1/3) / 4^(2/3) = 2^(-4/3)
+    assert abs(float(lam3[1]) - 2.0 ** (-4.0 / 3.0)) <= 2.0 ** -23
+
+
+@pytest.mark.parametrize("alpha", [0.5, 0.25, 0.8])
+def test_smoothing_balances_channel_ranges(alpha):
+    """SmoothQuant's purpose: after X/lambda and W*lambda the per-channel
+    ranges obey (s/lambda) / (m*lambda) = (s m)^(1 - 2 alpha); at alpha = 0.5
+    activation and weight channels end up with equal absmax."""
+    c = synth.tiny_case()
+    M, N, K = c["M"], c["N"], c["K"]
+    s = oracle.act_absmax(c["X"], M, K)
+    lam = oracle.smooth_factors(s, c["W"], N, K, alpha).astype(np.float64)
+    x_rng = np.abs(bf16_to_f64(c["X"]).reshape(M, K)).max(0) / lam
+    w_rng = np.abs(bf16_to_f64(c["W"]).reshape(N, K)).max(0) * lam
+    lhs = np.log(x_rng / w_rng)
+    rhs = (1.0 - 2.0 * alpha) * np.log(x_rng * lam * w_rng / lam)
+    assert np.allclose(lhs, rhs, atol=1e-6)
+
+
+def test_inv_lambda_is_correctly_rounded_reciprocal():
+    """inv_lambda = RN32(1/lambda): double rounding of a binary64 quotient to
+    binary32 is innocuous (53 >= 2*24 + 2), so NumPy gives the exact answer.
+    Also pins the SmoothQuant identity (X diag(1/l))(diag(l) W^T) = X W^T."""
+    rng = np.random.default_rng(3)
+    lam = np.exp(rng.uniform(-6, 6, 512)).astype(np.float32)
+    W = synth.rand_bf16(4, (8, 512), 0.02)
+    _, _, il = oracle.prepare_weight(W, lam, 8, 512)
+    want = (1.0 / lam.astype(np.float64)).astype(np.float32)
+    assert np.array_equal(il, want)
+    X = bf16_to_f64(synth.rand_bf16(5, (16, 512))).reshape(16, 512)
+    Wf = bf16_to_f64(W).reshape(8, 512)
+    lhs = (X * il.astype(np.float64)) @ (Wf * lam.astype(np.float64)).T
+    ref = X @ Wf.T
+    assert np.linalg.norm(lhs - ref) <= 2.0 ** -22 * np.linalg.norm(np.abs(X) @ np.abs(Wf).T)
+
+
+# --------------------------------------------------------------------------
+# per-row quantization
+# --------------------------------------------------------------------------
+
+def test_round_half_even_ties():
+    """With lambda = 1 and a row whose absmax is 127, scale = 1 and the codes
+    are rint(x): NumPy's rint (ties to even) fixes them. Catches round-half-up
+    or round-half-away-from-zero."""
+    row = np.array([127.0, 0.5, 1.5, 2.5, -0.5, -1.5, -2.5, 3.5, 126.5, -126.5,
+                    0.25, 0.75, -0.75, 64.5, 65.5, 0.0], np.float32)
+    K = 64
+    x = np.zeros(K, np.float32)
+    x[: row.size] = row
+    X = synth.to_bf16_bits(x)[None, :]
+    ones = np.ones(K, np.float32)
+    Xq, xs = oracle.quant_act(X, ones, 1, K)
+    assert xs[0] == np.float32(1.0)
+    assert np.array_equal(Xq[0].astype(np.float64), np.rint(x.astype(np.float64)))
+
+
+def _dequant_bound_ok(q, s, exact):
+    err = np.abs(q.astype(np.float64) * s.astype(np.float64)[:, None] - exact)
+    return np.all(err <= s.astype(np.float64)[:, None] * QUANT_SLACK)
+
+
+def test_activation_quant_invariants_tiny():
+    """max|q| = 127 on every nonzero row and |q s - X/lambda| <= s/2 (plus
+    binary32 slack) against X/lambda in binary64 (catches multiplying by
+    lambda instead of dividing, a wrong scale or a per-tensor scale)."""
+    c = synth.tiny_case()
+    M, N, K = c["M"], c["N"], c["K"]
+    r = oracle.recipe(c["X"], c["W"], c["bias"], M, N, K)
+    Xq, xs = r["Xq"], r["x_scale"]
+    assert np.all(np.abs(Xq.astype(np.int32)).max(1) == 127)
+    assert Xq.min() >= -127
+    exact = bf16_to_f64(c["X"]).reshape(M, K) / r["lambda"].astype(np.float64)
+    assert _dequant_bound_ok(Xq, xs, exact)
+    # the scale is absmax/127 of the smoothed row, correctly rounded
+    amax = np.abs((bf16_to_f64(c["X"]).reshape(M, K).astype(np.float32)
+                   * r["inv_lambda"][None, :]).astype(np.float32)).max(1)
+    assert np.array_equal(xs, (amax.astype(np.float64) / 127.0).astype(np.float32))
+
+
+def test_weight_quant_invariants_tiny():
+    """Same for the per-output-row weight codes against W*lambda."""
+    c = synth.tiny_case()
+    M, N, K = c["M"], c["N"], c["K"]
+    r = oracle.recipe(c["X"], c["W"], c["bias"], M, N, K)
+    Wq, ws = r["Wq"], r["w_scale"]
+    assert np.all(np.abs(Wq.astype(np.int32)).max(1) == 127)
+    exact = bf16_to_f64(c["W"]).reshape(N, K) * r["lambda"].astype(np.float64)
+    assert _dequant_bound_ok(Wq, ws, exact)
+
+
+def test_quant_special_rows():
+    """Zero row -> scale 0, codes 0; constant row -> all +-127; a row below
+    2^-96 -> zero (reciprocal would overflow); one nonzero entry -> +-127."""
+    K = 128
+    rows = np.zeros((5, K), np.float32)
+    rows[1, :] = -3.0
+    rows[2, :] = 2.0 ** -100
+    rows[3, 17] = 0.375
+    rows[4, :] = 1.0
+    rows[4, ::3] = -1.0
+    X = synth.to_bf16_bits(rows)
+    Xq, xs = oracle.quant_act(X, np.ones(K, np.float32), 5, K)
+    assert xs[0] == 0 and not Xq[0].any()
+    assert np.all(Xq[1] == -127) and xs[1] == np.float32(3.0 / 127.0)
+    assert xs[2] == 0 and not Xq[2].any()
+    assert Xq[3, 17] == 127 and np.count_nonzero(Xq[3]) == 1
+    assert np.array_equal(np.abs(Xq[4]), np.full(K, 127, np.int8))
+    assert np.all(Xq[4, ::3] == -127)
+
+
+# --------------------------------------------------------------------------
+# the whole recipe
+# --------------------------------------------------------------------------
+
+def _grid_case(rng, M, N, K):
+    """Inputs on the INT8 grid: X_tk = a_t i_tk lambda_k, W_nk = c_n j_nk /
+    lambda_k with powers of two a, c, lambda and integer i, j in [-127, 127],
+    every row holding a +-127. Quantization is then lossless, so the recipe
+    must return bf16(X W^T + b) exactly."""
+    lam = (2.0 ** rng.integers(-2, 3, K)).astype(np.float32)
+    a = 2.0 ** rng.integers(-6, 2, M)
+    cw = 2.0 ** rng.integers(-9, -4, N)
+    i = rng.integers(-127, 128, (M, K))
+    j = rng.integers(-127, 128, (N, K))
+    i[np.arange(M), rng.integers(0, K, M)] = 127
+    j[np.arange(N), rng.integers(0, K, N)] = -127
+    X = a[:, None] * i * lam[None, :]
+    W = cw[:, None] * j / lam[None, :]
+    b = rng.integers(-64, 64, N) * 2.0 ** -8
+    bits = lambda v: synth.to_bf16_bits(np.asarray(v, np.float32))
+    return bits(X), bits(W), bits(b), lam, X, W, b
+
+
+def test_lossless_grid_reduces_to_plain_product():
+    """Special case reducing to an exact matmul: catches the smoothing
+    direction, transposes, scale mistakes and a dropped bias exactly."""
+    rng = np.random.default_rng(21)
+    M, N, K = 9, 7, 128
+    Xb, Wb, bb, lam, X, W, b = _grid_case(rng, M, N, K)
+    assert np.array_equal(bf16_to_f64(Xb).reshape(M, K), X)   # grid is bf16-exact
+    assert np.array_equal(bf16_to_f64(Wb).reshape(N, K), W)
+    r = oracle.recipe(Xb, Wb, bb, M, N, K, lam=lam)
+    exact = X @ W.T + b[None, :]          # every term is a small dyadic: exact
+    want = np.array([[round_bf16_exact(float(v)) for v in row] for row in exact],
+                    np.uint16)
+    assert np.array_equal(r["Y"], want)
+    assert np.array_equal(r["acc"].astype(np.float64) * r["x_scale"][:, None]
+                          * r["w_scale"][None, :], X @ W.T)
+
+
+@pytest.mark.parametrize("which", ["tiny", "gelu_small"])
+def test_w8a8_error_bound_vs_fp64(which):
+    """Closed-form W8A8 error bound against binary64 X W^T + b, elementwise:
+    with x' = q_x s_x + e_x, w' = q_w s_w + e_w and |e| <= c s,
+    |acc s_x s_w - sum x w| <= c s_w sum|q_x s_x| + c s_x sum|q_w s_w| + K c^2 s_x s_w,
+    plus the final bf16 rounding (half an ulp)."""
+    if which == "tiny":
+        c = synth.tiny_case()
+    else:
+        c = synth.linear_case([77], 48, 80, 512, act="gelu")
+    M, N, K = c["M"], c["N"], c["K"]
+    r = oracle.recipe(c["X"], c["W"], c["bias"], M, N, K)
+    X = bf16_to_f64(c["X"]).reshape(M, K)
+    W = bf16_to_f64(c["W"]).reshape(N, K)
+    b = bf16_to_f64(c["bias"])
+    ref = X @ W.T + b[None, :]
+    sx = r["x_scale"].astype(np.float64)[:, None]
+    sw = r["w_scale"].astype(np.float64)[None, :]
+    dqx = np.abs(r["Xq"].astype(np.float64)) * sx
+    dqw = np.abs(r["Wq"].astype(np.float64)) * sw.T
+    cc = QUANT_SLACK
+    bound = cc * sw * dqx.sum(1)[:, None] + cc * sx * dqw.sum(1)[None, :] + K * cc * cc * sx * sw
+    y = bf16_to_f64(r["Y"]).reshape(M, N)
+    total = bound + 2.0 ** -8 * np.abs(y) + 1e-30
+    assert np.all(np.abs(y - ref) <= total)
+    # and the bound is not vacuous: the relative error is small overall
+    assert np.linalg.norm(y - ref) <= 0.05 * np.linalg.norm(ref)
+
+
+def test_epilogue_against_exact_rationals():
+    """bf16(acc * s_x * s_w + b) against exact rational arithmetic with the
+    brute-force rounding (catches a dropped bias, a wrong scale index or
+    rounding through binary32)."""
+    rng = np.random.default_rng(8)
+    M, N = 6, 40
+    C = rng.integers(-2 ** 28, 2 ** 28, (M, N), dtype=np.int64).astype(np.int32)
+    xs = rng.uniform(1e-4, 1e-1, M).astype(np.float32)
+    ws = rng.uniform(1e-5, 1e-2, N).astype(np.float32)
+    b = synth.rand_bf16(9, (N,), 50.0)
+    Y = oracle.epilogue(C, xs, ws, b, M, N)
+    bf = bf16_to_f64(b)
+    for t in range(M):
+        for n in range(N):
+            exact = (Fraction(int(C[t, n])) * Fraction(float(xs[t])) * Fraction(float(ws[n]))
+                     + Fraction(float(bf[n])))
+            assert Y[t, n] == round_bf16_exact(exact), (t, n)
+    Y0 = oracle.epilogue(C, xs, ws, None, M, N)
+    assert Y0[2, 3] == round_bf16_exact(Fraction(int(C[2, 3])) * Fraction(float(xs[2]))
+                                        * Fraction(float(ws[3])))
+
+
+def test_bf16_linear_small_integers_exact():
+    """Protected path on small integers: every partial sum is exact, so the
+    result is bf16 of the integer product (brute-force rounding)."""
+    rng = np.random.default_rng(2)
+    M, N, K = 5, 6, 200
+    X = rng.integers(-8, 9, (M, K)).astype(np.float64)
+    W = rng.integers(-8, 9, (N, K)).astype(np.float64)
+    b = rng.integers(-100, 100, N).astype(np.float64)
+    Y = oracle.bf16_linear(synth.to_bf16_bits(X), synth.to_bf16_bits(W),
+                           synth.to_bf16_bits(b), M, N, K)
+    exact = X @ W.T + b
+    want = np.array([[round_bf16_exact(float(v)) for v in row] for row in exact], np.uint16)
+    assert np.array_equal(Y, want)
+
+
+def test_bf16_linear_random_vs_numpy_fp64():
+    """Random bf16 inputs against BLAS binary64 plus exact rounding: equal up
+    to a binary64 summation-order difference at a bf16 rounding boundary."""
+    M, N, K = 8, 16, 512
+    X = synth.rand_bf16(31, (M, K))
+    W = synth.rand_bf16(32, (N, K), 0.05)
+    b = synth.rand_bf16(33, (N,), 0.1)
+    Y = oracle.bf16_linear(X, W, b, M, N, K)
+    ref = bf16_to_f64(X).reshape(M, K) @ bf16_to_f64(W).reshape(N, K).T + bf16_to_f64(b)
+    want = np.array([[round_bf16_exact(float(v)) for v in row] for row in ref], np.uint16)
+    d = ulp_distance(Y, want)
+    assert d.max() <= 1 and (d == 0).mean() > 0.99
+
+
+def test_oracle_thread_count_invariance():
+    c = synth.linear_case([12], 33, 40, 256)
+    r1 = oracle.recipe(c["X"], c["W"], c["bias"], 33, 40, 256)
+    n = oracle.num_threads()
+    oracle.set_num_threads(1)
+    try:
+        r2 = oracle.recipe(c["X"], c["W"], c["bias"], 33, 40, 256)
+    finally:
+        oracle.set_num_threads(n)
+    for key in r1:
+        assert np.array_equal(r1[key], r2[key]), key
+
+
+def _digest(a) -> str:
+    return hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()
+
+
+def test_tiny_case_digest_is_stable():
+    """Inputs and oracle outputs of the tiny case against the digests stored
+    by tests/golden/make_golden.py (catches a drifting RNG stream or an
+    unintended change to the oracle's arithmetic)."""
+    with open(os.path.join(GOLDEN, "tiny_case_digest.json")) as f:
+        want = json.load(f)
+    c = synth.tiny_case()
+    r = oracle.recipe(c["X"], c["W"], c["bias"], c["M"], c["N"], c["K"])
+    got = {"X": _digest(c["X"]), "W": _digest(c["W"]), "bias": _digest(c["bias"])}
+    got.update({k: _digest(v) for k, v in r.items()})
+    assert got == want["sha256"]

@@ -1,0 +1,154 @@
+/*
+ * w8a8.h -- C ABI of the MI355X (gfx950) INT8 W8A8 quantized linear.
+ *
+ * The library implements the INT8 W8A8 recipe of "Quantizing a Dual-Branch
+ * Flow-Matching Diffusion Transformer for Consumer GPUs" (arXiv 2606.12280),
+ * Section 3, paragraphs "INT8 W8A8" and "Activation-fragility profiling and
+ * protection":
+ *   - weights: per-output-row (per-channel) symmetric INT8, round to nearest;
+ *   - activations: per-token dynamic symmetric INT8;
+ *   - SmoothQuant smoothing with lambda_j = s_j^alpha / max_i |W_ij|^(1-alpha)
+ *     (weights scaled up by lambda, activations down);
+ *   - the most fragile layers kept in bf16 with no activation quantization.
+ *
+ * Conventions shared by every entry point:
+ *   - Matrices are row-major and packed: X [M][K] (M tokens, K input
+ *     channels), W [N][K] (N output channels; the nn.Linear layout),
+ *     Y [M][N]. bf16 values are passed as uint16_t bit patterns.
+ *   - Every pointer is a DEVICE pointer owned by the caller. The library
+ *     allocates nothing, keeps no state between calls and is re-entrant.
+ *   - `stream` is a hipStream_t passed as an opaque pointer (NULL = the null
+ *     stream). Every call only enqueues work on it and returns; inputs must
+ *     stay alive and unmodified until the stream reaches the call.
+ *   - Arguments are validated before any HIP call; on a validation error
+ *     nothing is enqueued. A failed launch returns W8A8_ERR_HIP. Faults in
+ *     the kernels surface at the caller's next synchronization.
+ *   - Sizes: 1 <= M <= 2^22 rows (tokens; also N for the weight-side row
+ *     kernels); GEMM outputs 1 <= N <= 2^20 and M * N <= 2^38;
+ *     64 <= K <= 65536 with K % 64 == 0 (the int32 sum is then exact:
+ *     127^2 * K < 2^31). Ragged M and N need no padding. Matrix pointers
+ *     and lambda / inv_lambda must be 16-byte aligned; scales 4-byte and
+ *     bias 2-byte aligned. Outputs may not overlap inputs.
+ *   - Inputs must be finite. Results are deterministic: the same inputs give
+ *     the same bits on every call.
+ *   - Codes and scales use binary32 arithmetic with one IEEE rounding per
+ *     operation: x' = x * inv_lambda, absmax, scale = absmax / 127,
+ *     code = clamp(rint(x' * RN(127 / absmax)), -127, 127) with rint = round
+ *     half to even. A row whose absmax is below 2^-96 (including an all-zero
+ *     row) gets scale 0 and all-zero codes.
+ */
+#ifndef W8A8_H
+#define W8A8_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum w8a8_status {
+    W8A8_OK = 0,
+    W8A8_ERR_NULL = 1,        /* a required pointer is NULL */
+    W8A8_ERR_SHAPE = 2,       /* a size is out of range */
+    W8A8_ERR_ALIGN = 3,       /* a pointer is not aligned as required */
+    W8A8_ERR_ALIAS = 4,       /* an output overlaps an input or another output */
+    W8A8_ERR_UNSUPPORTED = 5, /* a valid request this build does not handle
+                                 (K not a multiple of 64, K > 65536, alpha
+                                 outside (0, 1)) */
+    W8A8_ERR_HIP = 6          /* the HIP runtime reported an error */
+} w8a8_status;
+
+/* Opaque hipStream_t. */
+typedef void *w8a8_stream;
+
+/* Version of this ABI (increases on any incompatible change). */
+int w8a8_abi_version(void);
+
+/* Static description of a status code; never NULL. */
+const char *w8a8_status_string(int status);
+
+/* Name of the last HIP error seen by a call that returned W8A8_ERR_HIP on the
+ * calling thread ("" if none). */
+const char *w8a8_last_hip_error(void);
+
+/* ---------------------------------------------------------------------- */
+/* Calibration (Section 3: per-channel activation scales come from a      */
+/* profiling pass; the smoothing equation).                               */
+/* ---------------------------------------------------------------------- */
+
+/* Per-input-channel activation absmax, accumulated:
+ *   absmax[k] = max(absmax[k], max_t |X[t][k]|)        for k < K.
+ * X [M][K] bf16; absmax [K] fp32, read and written (seed it with zeros for a
+ * fresh pass; call again per calibration batch). */
+w8a8_status w8a8_act_absmax(const uint16_t *X, int64_t M, int64_t K,
+                            float *absmax, w8a8_stream stream);
+
+/* SmoothQuant factors (Section 3, the smoothing equation):
+ *   lambda[j] = act_absmax[j]^alpha / (max_i |W[i][j]|)^(1 - alpha),
+ * computed in binary64 (sqrt(s)/sqrt(m) when alpha == 0.5, else
+ * pow(s, alpha) / pow(m, 1 - alpha)) and rounded once to binary32. A channel
+ * whose activation absmax or weight-column absmax is 0 gets lambda = 1.
+ * act_absmax [K] fp32, W [N][K] bf16 -> lambda [K] fp32 (also used as the
+ * kernel's scratch for the column absmax). 0 < alpha < 1. */
+w8a8_status w8a8_smooth_factors(const float *act_absmax, const uint16_t *W,
+                                int64_t N, int64_t K, double alpha,
+                                float *lambda, w8a8_stream stream);
+
+/* ---------------------------------------------------------------------- */
+/* The quantized linear (Section 3, "INT8 W8A8").                          */
+/* ---------------------------------------------------------------------- */
+
+/* Offline weight preparation, once per layer:
+ *   inv_lambda[k] = RN(1 / lambda[k]);
+ *   W'[n][k] = W[n][k] * lambda[k];  per output row n: s = absmax/127 and
+ *   Wq[n][k] = clamp(rint(W'[n][k] * RN(127/absmax)), -127, 127).
+ * W [N][K] bf16, lambda [K] fp32 (finite, > 0) -> Wq [N][K] int8,
+ * w_scale [N] fp32, inv_lambda [K] fp32 (consumed by w8a8_quant_act).
+ * Pass lambda = all ones for a layer without smoothing. */
+w8a8_status w8a8_prepare_weight(const uint16_t *W, const float *lambda,
+                                int64_t N, int64_t K, int8_t *Wq,
+                                float *w_scale, float *inv_lambda,
+                                w8a8_stream stream);
+
+/* Runtime activation path, steps (1) smooth and (2) quantize per token:
+ *   X'[t][k] = X[t][k] * inv_lambda[k];  per token t: s = absmax/127 and
+ *   Xq[t][k] = clamp(rint(X'[t][k] * RN(127/absmax)), -127, 127).
+ * X [M][K] bf16, inv_lambda [K] fp32 -> Xq [M][K] int8, x_scale [M] fp32.
+ * One pass over X; the smoothed values never leave registers. */
+w8a8_status w8a8_quant_act(const uint16_t *X, const float *inv_lambda,
+                           int64_t M, int64_t K, int8_t *Xq, float *x_scale,
+                           w8a8_stream stream);
+
+/* Steps (3) INT8 GEMM and (4) fused epilogue:
+ *   acc[t][n] = sum_k Xq[t][k] * Wq[n][k]   (exact int32),
+ *   Y[t][n]   = bf16_rne(float(acc) * (x_scale[t] * w_scale[n]) + bias[n])
+ * with the product and the bias add in binary32 (one fused multiply-add).
+ * Xq [M][K] int8, x_scale [M], Wq [N][K] int8, w_scale [N], bias [N] bf16 or
+ * NULL (no bias) -> Y [M][N] bf16. The int32 accumulators stay in registers. */
+w8a8_status w8a8_linear(const int8_t *Xq, const float *x_scale,
+                        const int8_t *Wq, const float *w_scale,
+                        const uint16_t *bias, int64_t M, int64_t N, int64_t K,
+                        uint16_t *Y, w8a8_stream stream);
+
+/* The same GEMM main loop with the int32 accumulators stored instead of the
+ * epilogue (for verification): C[t][n] = sum_k Xq[t][k] * Wq[n][k].
+ * Xq [M][K] int8, Wq [N][K] int8 -> C [M][N] int32. */
+w8a8_status w8a8_gemm_i32(const int8_t *Xq, const int8_t *Wq, int64_t M,
+                          int64_t N, int64_t K, int32_t *C,
+                          w8a8_stream stream);
+
+/* Protected layer (Section 3: the top-N fragile layers stay in bf16 with no
+ * activation quantization):
+ *   Y[t][n] = bf16_rne(sum_k X[t][k] * W[n][k] + bias[n])
+ * with bf16 products accumulated in binary32 (MFMA). X [M][K] bf16,
+ * W [N][K] bf16 (the original, unsmoothed weights), bias [N] bf16 or NULL
+ * -> Y [M][N] bf16. */
+w8a8_status bf16_linear(const uint16_t *X, const uint16_t *W,
+                        const uint16_t *bias, int64_t M, int64_t N, int64_t K,
+                        uint16_t *Y, w8a8_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* W8A8_H */

@@ -1,0 +1,47 @@
+// Internal launchers of libw8a8 (not part of the ABI). Every launcher assumes
+// its arguments were validated by the entry points in api.hip, enqueues on
+// `stream` and returns the hipError_t of the launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace w8a8 {
+
+// Smoothing + per-row symmetric INT8 quantization of R rows of K bf16
+// values: out[r][k] = clamp(rint((src[r][k] * mul[k]) * RN(127/absmax_r))),
+// scale[r] = absmax_r / 127 (0 and all-zero codes below the tiny threshold).
+hipError_t launch_smooth_quant_rows(const uint16_t *src, const float *mul,
+                                    int64_t R, int64_t K, int8_t *out,
+                                    float *scale, hipStream_t stream);
+
+// inv[k] = RN(1 / lam[k]).
+hipError_t launch_reciprocal(const float *lam, int64_t K, float *inv,
+                             hipStream_t stream);
+
+// colmax[k] = max(colmax[k], max_r |src[r][k]|) over R rows of bf16.
+hipError_t launch_col_absmax(const uint16_t *src, int64_t R, int64_t K,
+                             float *colmax, hipStream_t stream);
+
+// dst[k] = 0 for k < K (a fill kernel, so that the call can be captured).
+hipError_t launch_zero_f32(float *dst, int64_t K, hipStream_t stream);
+
+// lam[k] = s[k]^alpha / lam[k]^(1-alpha) in binary64 (lam holds the weight
+// column absmax on entry); 1 where either statistic is zero.
+hipError_t launch_lambda_from_stats(const float *s, float *lam, int64_t K,
+                                    double alpha, hipStream_t stream);
+
+// C[m][n] = sum_k A[m][k] * B[n][k] with int8 operands; epilogue either
+// stores the int32 sum (Y32 != nullptr) or bf16(acc * xs[m] * ws[n] + b[n]).
+hipError_t launch_gemm_i8(const int8_t *A, const int8_t *B, const float *xs,
+                          const float *ws, const uint16_t *bias, int64_t M,
+                          int64_t N, int64_t K, uint16_t *Y, int32_t *Y32,
+                          hipStream_t stream);
+
+// Y[m][n] = bf16(sum_k A[m][k] * B[n][k] + b[n]) with bf16 operands and
+// binary32 accumulation.
+hipError_t launch_gemm_bf16(const uint16_t *A, const uint16_t *B,
+                            const uint16_t *bias, int64_t M, int64_t N,
+                            int64_t K, uint16_t *Y, hipStream_t stream);
+
+}  // namespace w8a8

@@ -1,0 +1,235 @@
+// Memory-bound kernels of the W8A8 recipe (paper Section 3, "INT8 W8A8"):
+//   - smooth + per-row INT8 quantization (activations per token at run time,
+//     weights per output channel offline);
+//   - the reciprocal of the smoothing factors;
+//   - calibration: per-channel absmax and the smoothing equation
+//     lambda_j = s_j^alpha / max_i |W_ij|^(1-alpha).
+//
+// Row quantization keeps a whole row in registers: a group of G wavefronts
+// owns one row, each lane loads CH chunks of 8 bf16 (one 16-byte load per
+// chunk, consecutive lanes on consecutive chunks, so each wave load is a
+// contiguous 1 KiB), multiplies by the smoothing vector, reduces the absmax
+// across the wave with lane shuffles (and across the G waves through LDS),
+// then writes 8 int8 codes per chunk (8-byte stores, contiguous per wave).
+// X is read from HBM exactly once and the codes written once.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "internal.h"
+
+namespace w8a8 {
+namespace {
+
+constexpr float kTinyAbsmax = 0x1p-96f;  // rows below quantize to zero
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+// One code: clamp(rint(v * r), -127, 127) packed into the low byte.
+__device__ __forceinline__ uint32_t code(float v, float r) {
+    float c = rintf(v * r);
+    c = fminf(fmaxf(c, -127.0f), 127.0f);
+    return static_cast<uint32_t>(static_cast<int32_t>(c)) & 0xffu;
+}
+
+// The 8 smoothed values of one chunk: float(x_e) * mul_e, one binary32
+// rounding each.
+__device__ __forceinline__ void smooth8(const uint4 &x, const float4 &ma, const float4 &mb,
+                                        float (&v)[8]) {
+    v[0] = bf16_lo(x.x) * ma.x;
+    v[1] = bf16_hi(x.x) * ma.y;
+    v[2] = bf16_lo(x.y) * ma.z;
+    v[3] = bf16_hi(x.y) * ma.w;
+    v[4] = bf16_lo(x.z) * mb.x;
+    v[5] = bf16_hi(x.z) * mb.y;
+    v[6] = bf16_lo(x.w) * mb.z;
+    v[7] = bf16_hi(x.w) * mb.w;
+}
+
+// Rows per block = RPB, G waves per row, CH chunks of 8 values per lane. The
+// smoothed values stay in registers between the absmax and the coding pass.
+template <int G, int CH>
+__global__ __launch_bounds__((G >= 4 ? G : 4) * 64) void smooth_quant_rows_kernel(
+    const uint16_t *__restrict__ src, const float *__restrict__ mul, int64_t R,
+    int64_t K, int8_t *__restrict__ out, float *__restrict__ scale) {
+    constexpr int RPB = G >= 4 ? 1 : 4 / G;
+    __shared__ float red[RPB][G];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int sub = wave / G;      // row slot in the block
+    const int gw = wave % G;       // wave index inside the row group
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * RPB + sub;
+    const bool row_ok = row < R;
+    const int64_t nchunk = K >> 3;
+
+    float v[CH][8];
+    float amax = 0.0f;
+    const uint4 *srow = reinterpret_cast<const uint4 *>(src + (row_ok ? row : 0) * K);
+    const float4 *m4 = reinterpret_cast<const float4 *>(mul);
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        const int64_t j = static_cast<int64_t>(c) * (G * 64) + gw * 64 + lane;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[c][e] = 0.0f;
+        if (row_ok && j < nchunk) smooth8(srow[j], m4[2 * j], m4[2 * j + 1], v[c]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(v[c][e]));
+    }
+    amax = wave_max(amax);
+    if constexpr (G > 1) {
+        if (lane == 0) red[sub][gw] = amax;
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < G; ++i) amax = fmaxf(amax, red[sub][i]);
+    }
+    if (!row_ok) return;
+
+    float s = 0.0f;
+    float r = 0.0f;
+    const bool nonzero = amax >= kTinyAbsmax;
+    if (nonzero) {
+        s = amax / 127.0f;
+        r = 127.0f / amax;
+    }
+    if (gw == 0 && lane == 0) scale[row] = s;
+    uint2 *orow = reinterpret_cast<uint2 *>(out + row * K);
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        const int64_t j = static_cast<int64_t>(c) * (G * 64) + gw * 64 + lane;
+        if (j < nchunk) {
+            uint2 q = make_uint2(0u, 0u);
+            if (nonzero) {
+                const float *t = v[c];
+                q.x = code(t[0], r) | code(t[1], r) << 8 | code(t[2], r) << 16 |
+                      code(t[3], r) << 24;
+                q.y = code(t[4], r) | code(t[5], r) << 8 | code(t[6], r) << 16 |
+                      code(t[7], r) << 24;
+            }
+            orow[j] = q;
+        }
+    }
+}
+
+template <int G, int CH>
+hipError_t launch_rows(const uint16_t *src, const float *mul, int64_t R, int64_t K,
+                       int8_t *out, float *scale, hipStream_t stream) {
+    constexpr int RPB = G >= 4 ? 1 : 4 / G;
+    constexpr int threads = (G >= 4 ? G : 4) * 64;
+    const int64_t blocks = (R + RPB - 1) / RPB;
+    hipLaunchKernelGGL((smooth_quant_rows_kernel<G, CH>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(threads), 0, stream, src, mul, R, K, out, scale);
+    return hipGetLastError();
+}
+
+__global__ void reciprocal_kernel(const float *__restrict__ lam, int64_t K,
+                                  float *__restrict__ inv) {
+    const int64_t k = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (k < K) inv[k] = 1.0f / lam[k];
+}
+
+__global__ void zero_kernel(float *__restrict__ dst, int64_t K) {
+    const int64_t k = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (k < K) dst[k] = 0.0f;
+}
+
+// Column absmax: a thread owns 8 consecutive columns and a strip of `strip`
+// rows; partial maxima merge with an integer atomic max (the bit patterns of
+// non-negative floats order like the floats).
+constexpr int64_t kColRows = 64;      // rows per strip, at least
+constexpr int64_t kColStrips = 32768; // strips (grid height), at most
+
+__global__ __launch_bounds__(256) void col_absmax_kernel(const uint16_t *__restrict__ src,
+                                                          int64_t R, int64_t K, int64_t strip,
+                                                          float *__restrict__ colmax) {
+    const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;  // chunk of 8
+    if (j * 8 >= K) return;
+    const int64_t r0 = static_cast<int64_t>(blockIdx.y) * strip;
+    const int64_t r1 = r0 + strip < R ? r0 + strip : R;
+    float m[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int64_t r = r0; r < r1; ++r) {
+        const uint4 x = reinterpret_cast<const uint4 *>(src + r * K)[j];
+        m[0] = fmaxf(m[0], fabsf(bf16_lo(x.x)));
+        m[1] = fmaxf(m[1], fabsf(bf16_hi(x.x)));
+        m[2] = fmaxf(m[2], fabsf(bf16_lo(x.y)));
+        m[3] = fmaxf(m[3], fabsf(bf16_hi(x.y)));
+        m[4] = fmaxf(m[4], fabsf(bf16_lo(x.z)));
+        m[5] = fmaxf(m[5], fabsf(bf16_hi(x.z)));
+        m[6] = fmaxf(m[6], fabsf(bf16_lo(x.w)));
+        m[7] = fmaxf(m[7], fabsf(bf16_hi(x.w)));
+    }
+    unsigned int *dst = reinterpret_cast<unsigned int *>(colmax) + j * 8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) atomicMax(dst + e, __float_as_uint(m[e]));
+}
+
+__global__ void lambda_kernel(const float *__restrict__ s, float *__restrict__ lam, int64_t K,
+                              double alpha) {
+    const int64_t k = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (k >= K) return;
+    const double sk = static_cast<double>(s[k]);
+    const double wk = static_cast<double>(lam[k]);  // weight column absmax
+    float out = 1.0f;
+    if (sk != 0.0 && wk != 0.0) {
+        if (alpha == 0.5)
+            out = static_cast<float>(sqrt(sk) / sqrt(wk));
+        else
+            out = static_cast<float>(pow(sk, alpha) / pow(wk, 1.0 - alpha));
+    }
+    lam[k] = out;
+}
+
+unsigned blocks_for(int64_t n, int threads) {
+    return static_cast<unsigned>((n + threads - 1) / threads);
+}
+
+}  // namespace
+
+hipError_t launch_smooth_quant_rows(const uint16_t *src, const float *mul, int64_t R,
+                                    int64_t K, int8_t *out, float *scale,
+                                    hipStream_t stream) {
+    // Row coverage is 512 * G * CH values; pick the smallest that holds K.
+    if (K <= 512) return launch_rows<1, 1>(src, mul, R, K, out, scale, stream);
+    if (K <= 1024) return launch_rows<1, 2>(src, mul, R, K, out, scale, stream);
+    if (K <= 2048) return launch_rows<1, 4>(src, mul, R, K, out, scale, stream);
+    if (K <= 4096) return launch_rows<1, 8>(src, mul, R, K, out, scale, stream);
+    if (K <= 8192) return launch_rows<2, 8>(src, mul, R, K, out, scale, stream);
+    if (K <= 16384) return launch_rows<4, 8>(src, mul, R, K, out, scale, stream);
+    if (K <= 32768) return launch_rows<8, 8>(src, mul, R, K, out, scale, stream);
+    return launch_rows<16, 8>(src, mul, R, K, out, scale, stream);  // K <= 65536
+}
+
+hipError_t launch_reciprocal(const float *lam, int64_t K, float *inv, hipStream_t stream) {
+    hipLaunchKernelGGL(reciprocal_kernel, dim3(blocks_for(K, 256)), dim3(256), 0, stream, lam,
+                       K, inv);
+    return hipGetLastError();
+}
+
+hipError_t launch_zero_f32(float *dst, int64_t K, hipStream_t stream) {
+    hipLaunchKernelGGL(zero_kernel, dim3(blocks_for(K, 256)), dim3(256), 0, stream, dst, K);
+    return hipGetLastError();
+}
+
+hipError_t launch_col_absmax(const uint16_t *src, int64_t R, int64_t K, float *colmax,
+                             hipStream_t stream) {
+    int64_t strip = (R + kColStrips - 1) / kColStrips;
+    if (strip < kColRows) strip = kColRows;
+    const dim3 grid(blocks_for(K / 8, 256), static_cast<unsigned>((R + strip - 1) / strip));
+    hipLaunchKernelGGL(col_absmax_kernel, grid, dim3(256), 0, stream, src, R, K, strip, colmax);
+    return hipGetLastError();
+}
+
+hipError_t launch_lambda_from_stats(const float *s, float *lam, int64_t K, double alpha,
+                                    hipStream_t stream) {
+    hipLaunchKernelGGL(lambda_kernel, dim3(blocks_for(K, 256)), dim3(256), 0, stream, s, lam, K,
+                       alpha);
+    return hipGetLastError();
+}
+
+}  // namespace w8a8

@@ -1,0 +1,171 @@
+"""Torch-tensor binding of the C ABI (include/w8a8.h), same names.
+
+Argument marshalling only: each function checks dtypes, devices and
+contiguity, allocates missing outputs with torch (device memory is all torch
+provides here), passes raw device pointers and torch's current HIP stream to
+the library, and raises W8A8Error on a non-zero status. Every arithmetic step
+runs in the library's HIP kernels. bf16 tensors are torch.bfloat16."""
+from __future__ import annotations
+
+import torch
+
+from ._lib import check, load
+
+__all__ = [
+    "w8a8_act_absmax", "w8a8_smooth_factors", "w8a8_prepare_weight", "w8a8_quant_act",
+    "w8a8_linear", "w8a8_gemm_i32", "bf16_linear",
+]
+
+
+def _stream(device: torch.device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _need(t: torch.Tensor, name: str, dtype: torch.dtype, ndim: int, device=None) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions, got shape {tuple(t.shape)}")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a GPU, got {t.device}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _out(t, shape, dtype, device, name):
+    if t is None:
+        return torch.empty(shape, dtype=dtype, device=device)
+    _need(t, name, dtype, len(shape), device)
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return t
+
+
+def w8a8_act_absmax(X: torch.Tensor, absmax: torch.Tensor) -> torch.Tensor:
+    """absmax[k] = max(absmax[k], max_t |X[t, k]|), in place (calibration)."""
+    _need(X, "X", torch.bfloat16, 2)
+    M, K = X.shape
+    _need(absmax, "absmax", torch.float32, 1, X.device)
+    if absmax.numel() != K:
+        raise ValueError("absmax must have K entries")
+    lib = load()
+    with torch.cuda.device(X.device):
+        check("w8a8_act_absmax",
+              lib.w8a8_act_absmax(_ptr(X), M, K, _ptr(absmax), _stream(X.device)))
+    return absmax
+
+
+def w8a8_smooth_factors(act_absmax: torch.Tensor, W: torch.Tensor, alpha: float = 0.5,
+                        out: torch.Tensor | None = None) -> torch.Tensor:
+    """lambda_j = s_j^alpha / max_i |W_ij|^(1 - alpha) -> fp32 [K]."""
+    _need(W, "W", torch.bfloat16, 2)
+    N, K = W.shape
+    _need(act_absmax, "act_absmax", torch.float32, 1, W.device)
+    lam = _out(out, (K,), torch.float32, W.device, "out")
+    lib = load()
+    with torch.cuda.device(W.device):
+        check("w8a8_smooth_factors",
+              lib.w8a8_smooth_factors(_ptr(act_absmax), _ptr(W), N, K, float(alpha), _ptr(lam),
+                                      _stream(W.device)))
+    return lam
+
+
+def w8a8_prepare_weight(W: torch.Tensor, lam: torch.Tensor, Wq=None, w_scale=None,
+                        inv_lambda=None):
+    """Offline weight side -> (Wq int8 [N, K], w_scale fp32 [N], inv_lambda fp32 [K])."""
+    _need(W, "W", torch.bfloat16, 2)
+    N, K = W.shape
+    _need(lam, "lambda", torch.float32, 1, W.device)
+    dev = W.device
+    Wq = _out(Wq, (N, K), torch.int8, dev, "Wq")
+    w_scale = _out(w_scale, (N,), torch.float32, dev, "w_scale")
+    inv_lambda = _out(inv_lambda, (K,), torch.float32, dev, "inv_lambda")
+    lib = load()
+    with torch.cuda.device(dev):
+        check("w8a8_prepare_weight",
+              lib.w8a8_prepare_weight(_ptr(W), _ptr(lam), N, K, _ptr(Wq), _ptr(w_scale),
+                                      _ptr(inv_lambda), _stream(dev)))
+    return Wq, w_scale, inv_lambda
+
+
+def w8a8_quant_act(X: torch.Tensor, inv_lambda: torch.Tensor, Xq=None, x_scale=None):
+    """Smooth + per-token quantize -> (Xq int8 [M, K], x_scale fp32 [M])."""
+    _need(X, "X", torch.bfloat16, 2)
+    M, K = X.shape
+    _need(inv_lambda, "inv_lambda", torch.float32, 1, X.device)
+    dev = X.device
+    Xq = _out(Xq, (M, K), torch.int8, dev, "Xq")
+    x_scale = _out(x_scale, (M,), torch.float32, dev, "x_scale")
+    lib = load()
+    with torch.cuda.device(dev):
+        check("w8a8_quant_act",
+              lib.w8a8_quant_act(_ptr(X), _ptr(inv_lambda), M, K, _ptr(Xq), _ptr(x_scale),
+                                 _stream(dev)))
+    return Xq, x_scale
+
+
+def w8a8_linear(Xq: torch.Tensor, x_scale: torch.Tensor, Wq: torch.Tensor,
+                w_scale: torch.Tensor, bias: torch.Tensor | None = None,
+                out: torch.Tensor | None = None) -> torch.Tensor:
+    """INT8 GEMM + fused dequant/bias epilogue -> Y bf16 [M, N]."""
+    _need(Xq, "Xq", torch.int8, 2)
+    _need(Wq, "Wq", torch.int8, 2, Xq.device)
+    M, K = Xq.shape
+    N = Wq.shape[0]
+    if Wq.shape[1] != K:
+        raise ValueError("Xq and Wq must share K")
+    _need(x_scale, "x_scale", torch.float32, 1, Xq.device)
+    _need(w_scale, "w_scale", torch.float32, 1, Xq.device)
+    if bias is not None:
+        _need(bias, "bias", torch.bfloat16, 1, Xq.device)
+    Y = _out(out, (M, N), torch.bfloat16, Xq.device, "out")
+    lib = load()
+    with torch.cuda.device(Xq.device):
+        check("w8a8_linear",
+              lib.w8a8_linear(_ptr(Xq), _ptr(x_scale), _ptr(Wq), _ptr(w_scale), _ptr(bias),
+                              M, N, K, _ptr(Y), _stream(Xq.device)))
+    return Y
+
+
+def w8a8_gemm_i32(Xq: torch.Tensor, Wq: torch.Tensor, out: torch.Tensor | None = None):
+    """The same GEMM storing the int32 accumulators -> C int32 [M, N]."""
+    _need(Xq, "Xq", torch.int8, 2)
+    _need(Wq, "Wq", torch.int8, 2, Xq.device)
+    M, K = Xq.shape
+    N = Wq.shape[0]
+    if Wq.shape[1] != K:
+        raise ValueError("Xq and Wq must share K")
+    C = _out(out, (M, N), torch.int32, Xq.device, "out")
+    lib = load()
+    with torch.cuda.device(Xq.device):
+        check("w8a8_gemm_i32",
+              lib.w8a8_gemm_i32(_ptr(Xq), _ptr(Wq), M, N, K, _ptr(C), _stream(Xq.device)))
+    return C
+
+
+def bf16_linear(X: torch.Tensor, W: torch.Tensor, bias: torch.Tensor | None = None,
+                out: torch.Tensor | None = None) -> torch.Tensor:
+    """Protected layer: bf16 X W^T + bias with fp32 accumulation -> Y bf16 [M, N]."""
+    _need(X, "X", torch.bfloat16, 2)
+    _need(W, "W", torch.bfloat16, 2, X.device)
+    M, K = X.shape
+    N = W.shape[0]
+    if W.shape[1] != K:
+        raise ValueError("X and W must share K")
+    if bias is not None:
+        _need(bias, "bias", torch.bfloat16, 1, X.device)
+    Y = _out(out, (M, N), torch.bfloat16, X.device, "out")
+    lib = load()
+    with torch.cuda.device(X.device):
+        check("bf16_linear",
+              lib.bf16_linear(_ptr(X), _ptr(W), _ptr(bias), M, N, K, _ptr(Y), _stream(X.device)))
+    return Y

@@ -1,0 +1,136 @@
+"""The C ABI without a GPU: the library loads, exports every function that
+include/w8a8.h declares, and rejects bad arguments with the documented status
+before touching HIP (the fake device addresses below are never dereferenced).
+Also the host-side routing rule of the protected layers."""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+import paper_2606_12280_amd as pkg
+from paper_2606_12280_amd import _lib, layer, ops
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "w8a8.h")
+
+OK, NULL, SHAPE, ALIGN, ALIAS, UNSUP = 0, 1, 2, 3, 4, 5
+A = 0x7F0000000000          # fake, 256-byte aligned device addresses
+B = 0x7F0100000000
+C = 0x7F0200000000
+D = 0x7F0300000000
+E = 0x7F0400000000
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return re.findall(r"^[A-Za-z_][\w \*]*?\b(\w+)\s*\(", text, flags=re.M)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return pkg.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(_lib.SIGNATURES), "binding and header disagree"
+
+
+def test_version_and_status_strings(lib):
+    assert lib.w8a8_abi_version() == 1
+    for s in range(7):
+        assert lib.w8a8_status_string(s)
+    assert lib.w8a8_status_string(99) == b"unknown status"
+    assert lib.w8a8_last_hip_error() == b""
+
+
+def test_quant_act_validation(lib):
+    f = lib.w8a8_quant_act
+    assert f(None, B, 4, 64, C, D, None) == NULL
+    assert f(A, B, 0, 64, C, D, None) == SHAPE
+    assert f(A, B, (1 << 22) + 1, 64, C, D, None) == SHAPE
+    assert f(A, B, 4, 0, C, D, None) == SHAPE
+    assert f(A, B, 4, 100, C, D, None) == UNSUP
+    assert f(A, B, 4, 65536 + 64, C, D, None) == UNSUP
+    assert f(A + 8, B, 4, 64, C, D, None) == ALIGN
+    assert f(A, B + 4, 4, 64, C, D, None) == ALIGN
+    assert f(A, B, 4, 64, C + 1, D, None) == ALIGN
+    assert f(A, B, 4, 64, A, D, None) == ALIAS               # Xq over X
+    assert f(A, B, 4, 64, C, C + 64, None) == ALIAS          # x_scale inside Xq
+
+
+def test_prepare_weight_validation(lib):
+    f = lib.w8a8_prepare_weight
+    assert f(A, B, 8, 64, C, D, None, None) == NULL
+    assert f(A, B, -1, 64, C, D, E, None) == SHAPE
+    assert f(A, B, 8, 64, C, D, B, None) == ALIAS            # inv_lambda over lambda
+    assert f(A, B + 8, 8, 64, C, D, E, None) == ALIGN
+
+
+def test_linear_validation(lib):
+    f = lib.w8a8_linear
+    assert f(A, B, C, D, None, 4, 8, 64, None, None) == NULL
+    assert f(A, B, C, D, None, 4, (1 << 20) + 1, 64, E, None) == SHAPE
+    assert f(A, B, C, D, None, 1 << 22, 1 << 20, 64, E, None) == SHAPE   # M*N > 2^38
+    assert f(A, B, C, D, None, 4, 8, 96, E, None) == UNSUP
+    assert f(A, B, C, D, E + 1, 4, 8, 64, E + 4096, None) == ALIGN       # odd bias
+    assert f(A, B, C, D, None, 4, 8, 64, C, None) == ALIAS               # Y over Wq
+    assert f(A, B, C, D, E, 4, 8, 64, E, None) == ALIAS                  # Y over bias
+    g = lib.w8a8_gemm_i32
+    assert g(A, B, 4, 8, 64, None, None) == NULL
+    assert g(A, B, 4, 8, 64, A + 16, None) == ALIAS
+    h = lib.bf16_linear
+    assert h(A, None, None, 4, 8, 64, C, None) == NULL
+    assert h(A, B, None, 4, 8, 64, A, None) == ALIAS
+    assert h(A, B, None, 4, 8, 0, C, None) == SHAPE
+
+
+def test_calibration_validation(lib):
+    f = lib.w8a8_smooth_factors
+    assert f(A, B, 8, 64, 0.5, None, None) == NULL
+    assert f(A, B, 8, 64, 0.0, C, None) == UNSUP
+    assert f(A, B, 8, 64, 1.0, C, None) == UNSUP
+    assert f(A, B, 8, 64, float("nan"), C, None) == UNSUP
+    assert f(A, B, 8, 64, 0.5, A, None) == ALIAS
+    g = lib.w8a8_act_absmax
+    assert g(A, 8, 64, None, None) == NULL
+    assert g(A, 8, 64, A + 64, None) == ALIAS
+    assert g(A + 2, 8, 64, C, None) == ALIGN
+
+
+def test_binding_rejects_host_tensors():
+    X = torch.zeros(4, 64, dtype=torch.bfloat16)
+    il = torch.ones(64)
+    with pytest.raises(ValueError, match="GPU"):
+        ops.w8a8_quant_act(X, il)
+    with pytest.raises(TypeError):
+        ops.w8a8_quant_act(X.float(), il)
+
+
+def test_binding_fails_loudly_without_library(monkeypatch):
+    monkeypatch.setattr(_lib, "_lib", None)
+    monkeypatch.setattr(_lib, "LIB_PATH", "/nonexistent/libw8a8.so")
+    with pytest.raises(RuntimeError, match="no CPU fallback"):
+        _lib.load()
+
+
+def test_status_error_carries_name():
+    err = _lib.W8A8Error("w8a8_linear", 4, "overlap")
+    assert "W8A8_ERR_ALIAS" in str(err) and err.status == 4
+
+
+def test_protection_rule_first_17_down_projections():
+    flags = layer.protected_layers(211, 17)
+    idx = [i for i, f in enumerate(flags) if f]
+    assert len(idx) == 17
+    assert all(i % 4 == 3 for i in idx)
+    assert idx == [4 * j + 3 for j in range(17)]
+    assert sum(1 for i in range(211) if i % 4 == 3) == 52

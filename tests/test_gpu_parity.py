@@ -1,0 +1,308 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle on
+the same seeded inputs.
+
+Bit-exact: inv_lambda, Wq, w_scale, Xq, x_scale, the int32 accumulators and
+the calibration absmax. Within the stated tolerance: the W8A8 bf16 output
+(<= 2 bf16 ulp, binary32 floor under cancellation), lambda (<= 1 binary32
+ulp) and the protected bf16 output (binary64 reference with the binary32
+summation bound). Full-size workloads are checked on whole tensors for the
+quantization and on sampled token rows for the GEMMs."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from parity import (check_bf16_output, check_w8a8_output, dev, dev_bf16, host,
+                    host_bits)
+
+pytestmark = pytest.mark.gpu
+
+from paper_2606_12280_amd import ops  # noqa: E402
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _setup():
+    oracle.build()
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    yield
+    torch.cuda.synchronize()
+
+
+def _quant_case(X, lam, M, K):
+    """GPU and oracle quantization of X with smoothing lam; returns both."""
+    il_ref = (1.0 / lam.astype(np.float64)).astype(np.float32)
+    Xq_ref, xs_ref = oracle.quant_act(X, il_ref, M, K)
+    Xq, xs = ops.w8a8_quant_act(dev_bf16(X.reshape(M, K)), dev(il_ref))
+    return host(Xq), host(xs), Xq_ref, xs_ref
+
+
+# --------------------------------------------------------------------------
+# quantization kernels
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("M,K", [(1, 64), (5, 192), (64, 256), (33, 512), (7, 1088),
+                                 (19, 2048), (64, 4096), (3, 4160), (9, 8192),
+                                 (4, 12352), (3, 16384), (2, 32768), (1, 65536)])
+def test_quant_act_bit_exact(M, K):
+    c = synth.linear_case([100, M, K], M, 8, K, act="gelu")
+    rng = np.random.default_rng([101, K])
+    lam = np.exp(rng.uniform(-2, 2, K)).astype(np.float32)
+    Xq, xs, Xq_ref, xs_ref = _quant_case(c["X"], lam, M, K)
+    assert np.array_equal(xs, xs_ref)
+    assert np.array_equal(Xq, Xq_ref)
+
+
+def test_quant_act_special_rows():
+    """Zero, tiny (below 2^-96), constant, one-hot and tie rows."""
+    K = 256
+    rows = np.zeros((6, K), np.float32)
+    rows[1, :] = -3.0
+    rows[2, :] = 2.0 ** -100
+    rows[3, 17] = 0.375
+    rows[4, :16] = [127.0, 0.5, 1.5, 2.5, -0.5, -1.5, -2.5, 3.5, 126.5, -126.5,
+                    0.25, 0.75, -0.75, 64.5, 65.5, 0.0]
+    rows[5, :] = np.linspace(-1e-20, 1e-20, K)
+    X = synth.to_bf16_bits(rows)
+    Xq, xs, Xq_ref, xs_ref = _quant_case(X, np.ones(K, np.float32), 6, K)
+    assert np.array_equal(xs, xs_ref) and np.array_equal(Xq, Xq_ref)
+    assert xs[0] == 0 and xs[2] == 0 and not Xq[0].any() and not Xq[2].any()
+
+
+@pytest.mark.parametrize("N,K", [(512, 256), (100, 4096), (33, 16384), (7, 1024)])
+def test_prepare_weight_bit_exact(N, K):
+    c = synth.linear_case([102, N, K], 4, N, K)
+    rng = np.random.default_rng([103, K])
+    lam = np.exp(rng.uniform(-3, 3, K)).astype(np.float32)
+    Wq_ref, ws_ref, il_ref = oracle.prepare_weight(c["W"], lam, N, K)
+    Wq, ws, il = ops.w8a8_prepare_weight(dev_bf16(c["W"]), dev(lam))
+    assert np.array_equal(host(il), il_ref)
+    assert np.array_equal(host(ws), ws_ref)
+    assert np.array_equal(host(Wq), Wq_ref)
+
+
+@pytest.mark.parametrize("M,K", [(64, 256), (4608, 4096), (1000, 16384), (3, 64)])
+def test_act_absmax_bit_exact_and_accumulates(M, K):
+    X1 = synth.rand_bf16([104, M, K], (M, K), 2.0)
+    X2 = synth.rand_bf16([105, M, K], (7, K), 5.0)
+    ref = oracle.act_absmax(X2, 7, K, oracle.act_absmax(X1, M, K))
+    s = torch.zeros(K, dtype=torch.float32, device="cuda")
+    ops.w8a8_act_absmax(dev_bf16(X1), s)
+    ops.w8a8_act_absmax(dev_bf16(X2), s)
+    assert np.array_equal(host(s), ref)
+
+
+@pytest.mark.parametrize("alpha", [0.5, 0.3])
+def test_smooth_factors(alpha):
+    c = synth.tiny_case()
+    M, N, K = c["M"], c["N"], c["K"]
+    s_ref = oracle.act_absmax(c["X"], M, K)
+    s_ref[5] = 0.0                              # lambda = 1 rule
+    lam_ref = oracle.smooth_factors(s_ref, c["W"], N, K, alpha)
+    lam = host(ops.w8a8_smooth_factors(dev(s_ref), dev_bf16(c["W"]), alpha))
+    assert lam[5] == 1.0
+    ulps = np.abs(lam.view(np.int32).astype(np.int64) - lam_ref.view(np.int32).astype(np.int64))
+    assert ulps.max() <= 1
+    if alpha == 0.5:
+        assert np.array_equal(lam, lam_ref)     # sqrt and divide are correctly rounded
+
+
+# --------------------------------------------------------------------------
+# GEMMs on small and ragged shapes (full outputs)
+# --------------------------------------------------------------------------
+
+GEMM_SHAPES = [(1, 1, 64), (64, 512, 256), (257, 129, 192), (300, 520, 1088),
+               (513, 384, 4160), (31, 1000, 64), (256, 128, 128), (200, 4096, 512)]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+def test_gemm_i32_bit_exact(M, N, K):
+    A = synth.rand_i8([106, M, K], (M, K))
+    B = synth.rand_i8([107, N, K], (N, K))
+    ref = oracle.gemm_i32(A, B, M, N, K)
+    C = host(ops.w8a8_gemm_i32(dev(A), dev(B)))
+    assert np.array_equal(C, ref)
+
+
+def test_gemm_i32_extremes():
+    """All +-127 codes at K = 16384: |acc| = 127^2 K, the largest sum."""
+    M, N, K = 64, 96, 16384
+    A = np.full((M, K), 127, np.int8)
+    A[1::2] = -127
+    B = np.full((N, K), -127, np.int8)
+    B[::3, ::2] = 127
+    C = host(ops.w8a8_gemm_i32(dev(A), dev(B)))
+    assert np.array_equal(C, oracle.gemm_i32(A, B, M, N, K))
+    assert abs(int(C[0, 1])) == 127 * 127 * K
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES + [(64, 512, 256)])
+@pytest.mark.parametrize("with_bias", [True, False])
+def test_w8a8_linear_recipe(M, N, K, with_bias):
+    """Whole recipe through the library: prepare, quantize, linear; every
+    intermediate bit-exact and Y within tolerance of the oracle."""
+    c = synth.linear_case([108, M, N, K], M, N, K, bias=with_bias)
+    lam = oracle.smooth_factors(oracle.act_absmax(c["X"], M, K), c["W"], N, K, 0.5)
+    r = oracle.recipe(c["X"], c["W"], c["bias"], M, N, K, lam=lam)
+    Wq, ws, il = ops.w8a8_prepare_weight(dev_bf16(c["W"]), dev(lam))
+    Xq, xs = ops.w8a8_quant_act(dev_bf16(c["X"]), il)
+    bias = dev_bf16(c["bias"]) if with_bias else None
+    Y = ops.w8a8_linear(Xq, xs, Wq, ws, bias)
+    C = ops.w8a8_gemm_i32(Xq, Wq)
+    assert np.array_equal(host(Wq), r["Wq"]) and np.array_equal(host(ws), r["w_scale"])
+    assert np.array_equal(host(Xq), r["Xq"]) and np.array_equal(host(xs), r["x_scale"])
+    assert np.array_equal(host(C), r["acc"])
+    check_w8a8_output(host_bits(Y), r["Y"], r["acc"], r["x_scale"], r["w_scale"], c["bias"])
+
+
+def test_w8a8_linear_tiny_case_and_determinism():
+    c = synth.tiny_case()
+    M, N, K = c["M"], c["N"], c["K"]
+    r = oracle.recipe(c["X"], c["W"], c["bias"], M, N, K)
+    Wq, ws, il = ops.w8a8_prepare_weight(dev_bf16(c["W"]), dev(r["lambda"]))
+    Xq, xs = ops.w8a8_quant_act(dev_bf16(c["X"]), il)
+    Y1 = host_bits(ops.w8a8_linear(Xq, xs, Wq, ws, dev_bf16(c["bias"])))
+    Y2 = host_bits(ops.w8a8_linear(Xq, xs, Wq, ws, dev_bf16(c["bias"])))
+    assert np.array_equal(Y1, Y2)
+    mx, eq = check_w8a8_output(Y1, r["Y"], r["acc"], r["x_scale"], r["w_scale"], c["bias"])
+    assert eq > 0.9
+
+
+def test_outputs_stay_inside_their_bounds():
+    """Guard bands around ragged outputs: no store lands outside Y or C."""
+    M, N, K = 257, 129, 192
+    A = synth.rand_i8([109], (M, K))
+    B = synth.rand_i8([110], (N, K))
+    pad = 4096
+    Cbuf = torch.full((M * N + 2 * pad,), 0x5A5A5A5A, dtype=torch.int32, device="cuda")
+    C = Cbuf[pad:pad + M * N].view(M, N)
+    ops.w8a8_gemm_i32(dev(A), dev(B), out=C)
+    Cb = host(Cbuf)
+    assert np.all(Cb[:pad] == 0x5A5A5A5A) and np.all(Cb[pad + M * N:] == 0x5A5A5A5A)
+    Ybuf = torch.full((M * N + 2 * pad,), 0x1234, dtype=torch.int16, device="cuda")
+    Y = Ybuf[pad:pad + M * N].view(torch.bfloat16).view(M, N)
+    xs = dev(np.ones(M, np.float32))
+    ws = dev(np.ones(N, np.float32))
+    ops.w8a8_linear(dev(A), xs, dev(B), ws, None, out=Y)
+    ops.bf16_linear(dev_bf16(synth.rand_bf16(1, (M, K))), dev_bf16(synth.rand_bf16(2, (N, K))),
+                    None, out=Y)
+    Yb = host(Ybuf)
+    assert np.all(Yb[:pad] == 0x1234) and np.all(Yb[pad + M * N:] == 0x1234)
+
+
+def test_nondefault_stream():
+    M, N, K = 130, 260, 320
+    A = synth.rand_i8([111], (M, K))
+    B = synth.rand_i8([112], (N, K))
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        C = ops.w8a8_gemm_i32(dev(A), dev(B))
+    s.synchronize()
+    assert np.array_equal(host(C), oracle.gemm_i32(A, B, M, N, K))
+
+
+# --------------------------------------------------------------------------
+# protected bf16 path
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("M,N,K", [(64, 512, 256), (257, 129, 192), (100, 300, 4160),
+                                   (33, 64, 16384)])
+def test_bf16_linear_small_integers_exact(M, N, K):
+    """Integer inputs keep every binary32 partial sum exact, so the result
+    must equal the oracle's bit for bit (catches any dropped or repeated
+    K block)."""
+    rng = np.random.default_rng([113, M, N, K])
+    X = synth.to_bf16_bits(rng.integers(-8, 9, (M, K)).astype(np.float32))
+    W = synth.to_bf16_bits(rng.integers(-8, 9, (N, K)).astype(np.float32))
+    b = synth.to_bf16_bits(rng.integers(-64, 64, N).astype(np.float32))
+    Y = host_bits(ops.bf16_linear(dev_bf16(X), dev_bf16(W), dev_bf16(b)))
+    assert np.array_equal(Y, oracle.bf16_linear(X, W, b, M, N, K))
+
+
+@pytest.mark.parametrize("M,N,K", [(64, 512, 256), (300, 520, 1088), (65, 128, 16384)])
+def test_bf16_linear_random(M, N, K):
+    c = synth.linear_case([114, M, N, K], M, N, K, act="gelu")
+    Y = host_bits(ops.bf16_linear(dev_bf16(c["X"]), dev_bf16(c["W"]), dev_bf16(c["bias"])))
+    check_bf16_output(Y, c["X"].reshape(M, K), c["W"].reshape(N, K), c["bias"])
+    ref = oracle.bf16_linear(c["X"], c["W"], c["bias"], M, N, K)
+    from bf16ref import ulp_distance
+    assert (ulp_distance(Y, ref) <= 1).mean() > 0.999
+
+
+# --------------------------------------------------------------------------
+# full-size DiT workloads: whole tensors for quantization, sampled rows for
+# the GEMMs (the launch configuration the benchmark times)
+# --------------------------------------------------------------------------
+
+SAMPLE_ROWS = 24
+
+
+def _full_size_check(c, protected_too=False):
+    M, N, K = c["M"], c["N"], c["K"]
+    lam = oracle.smooth_factors(oracle.act_absmax(c["X"], M, K), c["W"], N, K, 0.5)
+    Wq_ref, ws_ref, il_ref = oracle.prepare_weight(c["W"], lam, N, K)
+    Xq_ref, xs_ref = oracle.quant_act(c["X"], il_ref, M, K)
+    Xd, Wd = dev_bf16(c["X"].reshape(M, K)), dev_bf16(c["W"].reshape(N, K))
+    bd = dev_bf16(c["bias"])
+    s = torch.zeros(K, dtype=torch.float32, device="cuda")
+    ops.w8a8_act_absmax(Xd, s)
+    lam_gpu = ops.w8a8_smooth_factors(s, Wd, 0.5)
+    assert np.array_equal(host(lam_gpu), lam)
+    Wq, ws, il = ops.w8a8_prepare_weight(Wd, dev(lam))
+    Xq, xs = ops.w8a8_quant_act(Xd, il)
+    assert np.array_equal(host(il), il_ref)
+    assert np.array_equal(host(ws), ws_ref) and np.array_equal(host(Wq), Wq_ref)
+    assert np.array_equal(host(xs), xs_ref) and np.array_equal(host(Xq), Xq_ref)
+    Y = ops.w8a8_linear(Xq, xs, Wq, ws, bd)
+    C = ops.w8a8_gemm_i32(Xq, Wq)
+    rng = np.random.default_rng([115, M, N, K])
+    rows = np.sort(np.concatenate([[0, M - 1], rng.choice(M, SAMPLE_ROWS - 2, replace=False)]))
+    acc_ref = oracle.gemm_i32(Xq_ref[rows], Wq_ref, len(rows), N, K)
+    Y_ref = oracle.epilogue(acc_ref, xs_ref[rows], ws_ref, c["bias"], len(rows), N)
+    assert np.array_equal(host(C)[rows], acc_ref)
+    check_w8a8_output(host_bits(Y)[rows], Y_ref, acc_ref, xs_ref[rows], ws_ref, c["bias"])
+    # run-to-run determinism of the whole output at this size
+    Y2 = ops.w8a8_linear(Xq, xs, Wq, ws, bd)
+    assert torch.equal(Y.view(torch.int16), Y2.view(torch.int16))
+    if protected_too:
+        Yb = host_bits(ops.bf16_linear(Xd, Wd, bd))
+        check_bf16_output(Yb[rows], c["X"].reshape(M, K)[rows], c["W"].reshape(N, K), c["bias"])
+
+
+def test_full_size_ffn_up():
+    """4608 x 4096 -> 16384 (one branch's FFN up-projection)."""
+    _full_size_check(synth.ffn_up_case())
+
+
+def test_full_size_ffn_down_both_paths():
+    """4608 x 16384 -> 4096 with post-GELU heavy-tailed activations, W8A8 and
+    the protected bf16 path."""
+    _full_size_check(synth.ffn_down_case(), protected_too=True)
+
+
+@pytest.mark.parametrize("branch", [0, 1])
+def test_full_size_dit_block(branch):
+    """The four linears of one DiT block for one CFG branch; the FFN down
+    is routed to the protected path."""
+    from paper_2606_12280_amd import layer as L
+    for li in range(4):
+        c = synth.block_case(branch, li)
+        M, N, K = c["M"], c["N"], c["K"]
+        lam = oracle.smooth_factors(oracle.act_absmax(c["X"], M, K), c["W"], N, K, 0.5)
+        protected = c["name"] == "ffn_down"
+        Xd, Wd = dev_bf16(c["X"].reshape(M, K)), dev_bf16(c["W"].reshape(N, K))
+        lay = L.prepare_linear(Wd, dev_bf16(c["bias"]), dev(lam), protected)
+        Y = host_bits(L.route(lay, Xd))
+        rows = np.random.default_rng([116, branch, li]).choice(M, 8, replace=False)
+        if protected:
+            check_bf16_output(Y[rows], c["X"].reshape(M, K)[rows], c["W"].reshape(N, K),
+                              c["bias"])
+        else:
+            Wq_ref, ws_ref, il_ref = oracle.prepare_weight(c["W"], lam, N, K)
+            Xs = c["X"].reshape(M, K)[rows]
+            Xq_ref, xs_ref = oracle.quant_act(Xs, il_ref, len(rows), K)
+            acc = oracle.gemm_i32(Xq_ref, Wq_ref, len(rows), N, K)
+            Y_ref = oracle.epilogue(acc, xs_ref, ws_ref, c["bias"], len(rows), N)
+            check_w8a8_output(Y[rows], Y_ref, acc, xs_ref, ws_ref, c["bias"])

@@ -1,0 +1,426 @@
+"""Benchmark of the W8A8 linear on one MI355X.
+
+One step is one pass of the hot path over one batch of synthetic input. The
+layer goes through the protection router: a W8A8 layer runs smoothing +
+per-token quantization (w8a8_quant_act) and then the INT8 GEMM with its fused
+epilogue (w8a8_linear). A protected layer runs bf16_linear. Weights are
+prepared (quantized) once, outside the timed region, as in deployment.
+
+Default workload: the DiT FFN up-projection of one branch, X [4608 x 4096] ->
+Y [4608 x 16384]. Other workloads (--workload): ffn_down (W8A8 and protected
+paths), dit_block (the four linears of a block, both CFG branches), backbone
+(211 linears x 2 branches, 17 protected per branch).
+
+Prints one JSON line. ``value`` is the step's throughput in TOPS
+(2 M N K per step divided by the step time). ``roofline`` covers the dominant
+kernel (the INT8 GEMM). ``cpu_baseline`` is the CPU oracle timed on a bounded
+sample of the same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+from paper_2606_12280_amd import layer as L  # noqa: E402
+from paper_2606_12280_amd import ops  # noqa: E402
+
+METRIC = "W8A8 linear TOPS (% INT8 MFMA peak) + act-quant GB/s at DiT FFN shapes"
+PEAK_INT8_TOPS = 5000.0    # MI355X dense INT8 MFMA
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
+GEMM_SOURCES = ["paper_2606_12280_amd/csrc/gemm.hip"]
+QUANT_SOURCES = ["paper_2606_12280_amd/csrc/quant.hip"]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def sources_sha(paths) -> str:
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def to_dev_bf16(bits: np.ndarray, dev) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
+
+
+# --------------------------------------------------------------------------
+# workloads: lists of (prepared layer, input pool)
+# --------------------------------------------------------------------------
+
+class Linear:
+    def __init__(self, name, lay: L.PreparedLinear, xs: list[torch.Tensor]):
+        self.name = name
+        self.lay = lay
+        self.xs = xs
+        self.M = xs[0].shape[0]
+        self.Y = torch.empty(self.M, lay.N, dtype=torch.bfloat16, device=xs[0].device)
+
+    @property
+    def ops(self) -> int:
+        return 2 * self.M * self.lay.N * self.lay.K
+
+
+def calibrated_layer(X: torch.Tensor, W: torch.Tensor, bias, protected: bool):
+    """lambda from the activation absmax of X (calibration on the layer's
+    own input) and the weight column absmax, alpha = 0.5; then prepare."""
+    if protected:
+        return L.prepare_linear(W, bias, None, True)
+    s = torch.zeros(W.shape[1], dtype=torch.float32, device=W.device)
+    ops.w8a8_act_absmax(X, s)
+    lam = ops.w8a8_smooth_factors(s, W, 0.5)
+    return L.prepare_linear(W, bias, lam, False)
+
+
+def host_case_linear(name, case, dev, pool: int, protected: bool, seed_base) -> Linear:
+    """A layer from the seeded host generator (the documented case) plus
+    pool - 1 further inputs of the same distribution for rotation."""
+    M, N, K = case["M"], case["N"], case["K"]
+    X0 = to_dev_bf16(case["X"].reshape(M, K), dev)
+    W = to_dev_bf16(case["W"].reshape(N, K), dev)
+    b = to_dev_bf16(case["bias"], dev)
+    lay = calibrated_layer(X0, W, b, protected)
+    if not protected:
+        del W
+    xs = [X0]
+    act = "gelu" if K == 16384 else "outlier"
+    for i in range(1, pool):
+        rng = np.random.default_rng([seed_base, 1000 + i])
+        if act == "gelu":
+            x = synth.gelu_lognormal_activations(rng, M, K)
+        else:
+            x = synth.outlier_activations(rng, M, K, int(round(0.01 * K)), 20.0)
+        xs.append(to_dev_bf16(synth.to_bf16_bits(x), dev))
+    return Linear(name, lay, xs)
+
+
+def device_linear(name, M, N, K, dev, gen: torch.Generator, protected: bool, x_pool) -> Linear:
+    """A layer with device-generated N(0, 0.02) weights (the large sweeps;
+    timing only), sharing an input pool with the layers of its shape."""
+    W = (torch.randn(N, K, device=dev, generator=gen) * 0.02).bfloat16()
+    b = (torch.randn(N, device=dev, generator=gen) * 0.01).bfloat16()
+    lay = calibrated_layer(x_pool[0], W, b, protected)
+    return Linear(name, lay, x_pool)
+
+
+def device_inputs(M, K, dev, gen, n, gelu: bool):
+    out = []
+    for _ in range(n):
+        if gelu:
+            z = torch.randn(M, K, device=dev, generator=gen) * 1.5
+            c = torch.exp(torch.randn(K, device=dev, generator=gen) * 1.5)
+            out.append((torch.nn.functional.gelu(z) * c).bfloat16())
+        else:
+            x = torch.randn(M, K, device=dev, generator=gen)
+            idx = torch.randperm(K, device=dev, generator=gen)[: int(round(0.01 * K))]
+            x[:, idx] *= 20.0
+            out.append(x.bfloat16())
+    return out
+
+
+def build_workload(name: str, dev, pool: int):
+    if name == "ffn_up":
+        return [host_case_linear("ffn_up", synth.ffn_up_case(), dev, pool, False, 2)]
+    if name == "ffn_down":
+        c = synth.ffn_down_case()
+        return [host_case_linear("ffn_down_w8a8", c, dev, pool, False, 3),
+                host_case_linear("ffn_down_bf16", c, dev, pool, True, 3)]
+    gen = torch.Generator(device=dev)
+    if name == "dit_block":
+        out = []
+        for br in range(2):
+            for li in range(4):
+                c = synth.block_case(br, li)
+                out.append(host_case_linear(f"b{br}_{c['name']}", c, dev, 1,
+                                            c["name"] == "ffn_down", 40 + 10 * br + li))
+        return out
+    if name == "backbone":
+        gen.manual_seed(5)
+        M = synth.TOKENS
+        pools = {}
+        for sname, N, K in synth.BLOCK_SHAPES:
+            pools[sname] = device_inputs(M, K, dev, gen, 2, sname == "ffn_down")
+        flags = L.protected_layers(211, 17)
+        out = []
+        for br in range(2):
+            for i in range(211):
+                sname, N, K = synth.BLOCK_SHAPES[i % 4]
+                out.append(device_linear(f"b{br}_{i}_{sname}", M, N, K, dev, gen, flags[i],
+                                         pools[sname]))
+        return out
+    raise SystemExit(f"unknown workload {name}")
+
+
+# --------------------------------------------------------------------------
+# timing
+# --------------------------------------------------------------------------
+
+def run_step(layers, it: int, ws: L.Workspace, events=None):
+    """One pass over every layer. If events is given, records
+    (start, after-quant, end) per layer."""
+    for li, lin in enumerate(layers):
+        X = lin.xs[it % len(lin.xs)]
+        if lin.lay.protected:
+            if events is not None:
+                events[li][0].record()
+                events[li][1].record()
+            ops.bf16_linear(X, lin.lay.W, lin.lay.bias, out=lin.Y)
+        else:
+            Xq, xs = ws.get(lin.M, lin.lay.K)
+            if events is not None:
+                events[li][0].record()
+            ops.w8a8_quant_act(X, lin.lay.inv_lambda, Xq=Xq, x_scale=xs)
+            if events is not None:
+                events[li][1].record()
+            ops.w8a8_linear(Xq, xs, lin.lay.Wq, lin.lay.w_scale, lin.lay.bias, out=lin.Y)
+        if events is not None:
+            events[li][2].record()
+
+
+def measure(layers, steps: int, warmup: int, dev, per_kernel: bool):
+    ws = L.Workspace(dev)
+    for i in range(warmup):
+        run_step(layers, i, ws)
+    torch.cuda.synchronize()
+    ev = None
+    if per_kernel:
+        ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in layers]
+              for _ in range(steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record()
+    for s in range(steps):
+        run_step(layers, warmup + s, ws, ev[s] if ev else None)
+    t1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t0.elapsed_time(t1)
+    quant_us = np.zeros(len(layers))
+    gemm_us = np.zeros(len(layers))
+    if ev:
+        for s in range(steps):
+            for li in range(len(layers)):
+                a, b, c = ev[s][li]
+                quant_us[li] += a.elapsed_time(b) * 1e3
+                gemm_us[li] += b.elapsed_time(c) * 1e3
+        quant_us /= steps
+        gemm_us /= steps
+    return total_ms / steps, wall / steps * 1e3, quant_us, gemm_us
+
+
+def quant_isolated(lin: Linear, dev, reps: int = 50):
+    """Quant kernel alone, inputs rotating over buffers larger than the
+    256 MB Infinity Cache so that X is read from HBM."""
+    M, K = lin.M, lin.lay.K
+    nbuf = max(2, int(np.ceil(600e6 / (2 * M * K))))
+    xs = [lin.xs[i % len(lin.xs)].clone() for i in range(nbuf)]
+    qs = [torch.empty(M, K, dtype=torch.int8, device=dev) for _ in range(nbuf)]
+    sc = torch.empty(M, dtype=torch.float32, device=dev)
+    for i in range(nbuf):
+        ops.w8a8_quant_act(xs[i], lin.lay.inv_lambda, Xq=qs[i], x_scale=sc)
+    torch.cuda.synchronize()
+    e = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+         for _ in range(reps)]
+    for r in range(reps):
+        i = r % nbuf
+        e[r][0].record()
+        ops.w8a8_quant_act(xs[i], lin.lay.inv_lambda, Xq=qs[i], x_scale=sc)
+        e[r][1].record()
+    torch.cuda.synchronize()
+    us = np.array([a.elapsed_time(b) * 1e3 for a, b in e])
+    del xs, qs
+    return float(np.median(us)), float(np.percentile(us, 10)), float(np.percentile(us, 90))
+
+
+def quant_bytes(M, K) -> int:
+    """Algorithmic bytes of one quant launch: read X (bf16) and inv_lambda,
+    write Xq (int8) and x_scale."""
+    return 2 * M * K + M * K + 4 * M + 4 * K
+
+
+# --------------------------------------------------------------------------
+# CPU oracle baseline
+# --------------------------------------------------------------------------
+
+def cpu_baseline(workload: str, target_s: float = 10.0):
+    """The oracle (quant + int32 GEMM + epilogue) on a bounded sample of
+    token rows of the workload's first W8A8 linear, on this host's cores."""
+    import oracle
+
+    oracle.build()
+    if workload == "ffn_down":
+        c = synth.ffn_down_case()
+    else:
+        c = synth.ffn_up_case()
+    M, N, K = c["M"], c["N"], c["K"]
+    lam = oracle.smooth_factors(oracle.act_absmax(c["X"], M, K), c["W"], N, K, 0.5)
+    Wq, ws, il = oracle.prepare_weight(c["W"], lam, N, K)   # offline, not timed
+    X = c["X"].reshape(M, K)
+
+    def run(rows):
+        t = time.perf_counter()
+        Xq, xs = oracle.quant_act(X[:rows], il, rows, K)
+        oracle.w8a8_linear(Xq, xs, Wq, ws, c["bias"], rows, N, K)
+        return time.perf_counter() - t
+
+    probe = 16
+    dt = run(probe)
+    rows = int(min(M, max(probe, probe * target_s / max(dt, 1e-6))))
+    rows = max(probe, rows // 16 * 16)
+    dt = run(rows)
+    tops = 2.0 * rows * N * K / dt / 1e12
+    return {"value": round(tops, 6), "unit": "TOPS", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"{rows} of {M} token rows of the {M}x{K}->{N} linear: smoothing + "
+                      f"per-token quant + int32 GEMM + bf16 epilogue (weights prepared "
+                      f"outside the timing), {dt:.1f} s"}
+
+
+# --------------------------------------------------------------------------
+# roofline traffic from committed counters
+# --------------------------------------------------------------------------
+
+def counter_traffic(workload: str):
+    """HBM bytes per GEMM launch from the rocprofv3 counter summary in
+    profiles/, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"gemm_{workload}_counters.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("kernel_source_sha256") != sources_sha(GEMM_SOURCES):
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+# --------------------------------------------------------------------------
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="ffn_up",
+                    choices=["ffn_up", "ffn_down", "dit_block", "backbone"])
+    ap.add_argument("--pool", type=int, default=4, help="distinct inputs rotated over steps")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the W8A8 linear shards by CFG branch or token rows with no exchange; "
+              "run --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    props = torch.cuda.get_device_properties(dev)
+    log(f"device {props.name} {getattr(props, 'gcnArchName', '')} CUs {props.multi_processor_count}")
+
+    t_build = time.perf_counter()
+    layers = build_workload(args.workload, dev, args.pool)
+    torch.cuda.synchronize()
+    log(f"workload {args.workload}: {len(layers)} linears prepared in "
+        f"{time.perf_counter() - t_build:.1f} s")
+
+    # per-kernel durations inside the timed steps (events between kernels)
+    step_ms_ev, _, quant_us, gemm_us = measure(layers, args.steps, args.warmup, dev, True)
+    # the step time proper, without per-kernel events
+    step_ms, wall_ms, _, _ = measure(layers, args.steps, args.warmup, dev, False)
+    total_ops = sum(lin.ops for lin in layers)
+    value = total_ops / (step_ms * 1e-3) / 1e12
+
+    w8 = [i for i, lin in enumerate(layers) if not lin.lay.protected]
+    prot = [i for i, lin in enumerate(layers) if lin.lay.protected]
+    dom = max(w8, key=lambda i: gemm_us[i]) if w8 else None
+    kernels = {}
+    for shape_key in sorted({(layers[i].M, layers[i].lay.N, layers[i].lay.K) for i in w8}):
+        idx = [i for i in w8 if (layers[i].M, layers[i].lay.N, layers[i].lay.K) == shape_key]
+        M, N, K = shape_key
+        g = float(np.mean(gemm_us[idx]))
+        q = float(np.mean(quant_us[idx]))
+        kernels[f"w8a8_linear_{M}x{K}x{N}"] = {
+            "us": round(g, 2), "TOPS": round(2 * M * N * K / g / 1e6, 1),
+            "frac_int8_peak": round(2 * M * N * K / g / 1e6 / PEAK_INT8_TOPS, 4), "count": len(idx)}
+        kernels[f"w8a8_quant_act_{M}x{K}_in_step"] = {
+            "us": round(q, 2), "GB_s": round(quant_bytes(M, K) / q / 1e3, 1),
+            "frac_hbm": round(quant_bytes(M, K) / q / 1e3 / PEAK_HBM_GBS, 4)}
+    for shape_key in sorted({(layers[i].M, layers[i].lay.N, layers[i].lay.K) for i in prot}):
+        idx = [i for i in prot if (layers[i].M, layers[i].lay.N, layers[i].lay.K) == shape_key]
+        M, N, K = shape_key
+        g = float(np.mean(gemm_us[idx]))
+        kernels[f"bf16_linear_{M}x{K}x{N}"] = {
+            "us": round(g, 2), "TFLOPS": round(2 * M * N * K / g / 1e6, 1),
+            "frac_bf16_peak": round(2 * M * N * K / g / 1e6 / PEAK_BF16_TFLOPS, 4),
+            "count": len(idx)}
+    # the quant kernel alone with HBM-resident (not cache-resident) inputs
+    seen = set()
+    for i in w8:
+        lin = layers[i]
+        if lin.lay.K in seen:
+            continue
+        seen.add(lin.lay.K)
+        med, p10, p90 = quant_isolated(lin, dev)
+        by = quant_bytes(lin.M, lin.lay.K)
+        kernels[f"w8a8_quant_act_{lin.M}x{lin.lay.K}_hbm"] = {
+            "us": round(med, 2), "us_p10": round(p10, 2), "us_p90": round(p90, 2),
+            "GB_s": round(by / med / 1e3, 1), "frac_hbm": round(by / med / 1e3 / PEAK_HBM_GBS, 4),
+            "bytes": by}
+
+    roofline = None
+    if dom is not None:
+        lin = layers[dom]
+        ach = lin.ops / (gemm_us[dom] * 1e-6) / 1e12
+        roofline = {"bound": "mfma", "kernel": "w8a8_linear (INT8 MFMA GEMM + fused epilogue)",
+                    "achieved": round(ach, 1), "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
+                    "frac": round(ach / PEAK_INT8_TOPS, 4),
+                    "traffic": counter_traffic(args.workload),
+                    "ops_per_launch": lin.ops, "avg_launch_us": round(float(gemm_us[dom]), 2)}
+
+    cpu = None
+    if not args.no_cpu_baseline and args.workload in ("ffn_up", "ffn_down"):
+        log("timing the CPU oracle on a bounded sample ...")
+        cpu = cpu_baseline(args.workload, args.cpu_seconds)
+
+    M0 = layers[0].M
+    cfg = {"workload": {"ffn_up": "DiT FFN up-projection 4608x4096->16384, one branch",
+                        "ffn_down": "DiT FFN down-projection 4608x16384->4096, W8A8 and protected bf16",
+                        "dit_block": "one DiT block (qkv, attn_out, ffn_up, ffn_down protected), both CFG branches",
+                        "backbone": "211 linears x 2 branches, 17 protected per branch"}[args.workload],
+           "tokens": M0, "linears": len(layers), "protected": len(prot),
+           "input_pool": args.pool if args.workload in ("ffn_up", "ffn_down") else None,
+           "smoothquant_alpha": 0.5}
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TOPS", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int8",
+        "data": "synthetic", "config": cfg, "roofline": roofline, "cpu_baseline": cpu,
+        "kernels": kernels, "ms_per_step_with_kernel_events": round(step_ms_ev, 4),
+        "host_wall_ms_per_step": round(wall_ms, 4),
+        "device": {"name": props.name, "arch": getattr(props, "gcnArchName", ""),
+                   "cus": props.multi_processor_count},
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

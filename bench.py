@@ -192,11 +192,18 @@ def run_step(layers, it: int, ws: L.Workspace, events=None):
             events[li][2].record()
 
 
-def measure(layers, steps: int, warmup: int, dev, per_kernel: bool):
+def measure(layers, steps: int, warmup: int, dev, per_kernel: bool, warm_ms: float = 200.0):
     ws = L.Workspace(dev)
     for i in range(warmup):
         run_step(layers, i, ws)
     torch.cuda.synchronize()
+    # keep the GPU busy long enough for its clocks to settle before timing
+    t_end = time.perf_counter() + warm_ms * 1e-3
+    i = warmup
+    while time.perf_counter() < t_end:
+        run_step(layers, i, ws)
+        torch.cuda.synchronize()
+        i += 1
     ev = None
     if per_kernel:
         ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in layers]
@@ -310,6 +317,96 @@ def counter_traffic(workload: str):
     return d.get("hbm_bytes_per_launch")
 
 
+# The counter passes. HBM traffic of the GEMM comes from two rocprofv3
+# counter runs over the same short launch sequence (--counter-run): one with
+# FETCH_SIZE, one with WRITE_SIZE (KiB per dispatch). Both counters are
+# calibrated against a plain streaming kernel (y = -x over COPY_BYTES, larger
+# than the 256 MB last-level cache, so it reads and writes COPY_BYTES of HBM
+# each); --counters-from turns the two CSVs into the summary that
+# counter_traffic() reads.
+COPY_BYTES = 512 << 20
+
+
+def counter_run(layers, dev, reps: int = 3):
+    lin = max((x for x in layers if not x.lay.protected), key=lambda x: x.ops)
+    ws = L.Workspace(dev)
+    Xq, xs = ws.get(lin.M, lin.lay.K)
+    ops.w8a8_quant_act(lin.xs[0], lin.lay.inv_lambda, Xq=Xq, x_scale=xs)
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        ops.w8a8_linear(Xq, xs, lin.lay.Wq, lin.lay.w_scale, lin.lay.bias, out=lin.Y)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+    log(f"counter run: {reps} x w8a8_linear {lin.M}x{lin.lay.K}->{lin.lay.N}, "
+        f"{reps} x neg over {COPY_BYTES} bytes")
+    return lin
+
+
+def _counter_means(run_dir: str, counter: str):
+    """Mean counter value per dispatch for the GEMM and the calibration
+    kernel, from a rocprofv3 counter_collection.csv under run_dir."""
+    import csv
+    import glob
+
+    files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {run_dir}")
+    per = {}
+    with open(files[0]) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            kind = "gemm" if "gemm" in name else ("copy" if "neg" in name else None)
+            if kind is None:
+                continue
+            key = (kind, r.get("Dispatch_Id", r.get("Correlation_Id")))
+            per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+    out = {}
+    for kind in ("gemm", "copy"):
+        vals = [v for (k, _), v in per.items() if k == kind]
+        if not vals:
+            raise SystemExit(f"no {kind} dispatch with {counter} in {files[0]}")
+        out[kind] = float(np.mean(vals))
+    return out
+
+
+def counters_from(fetch_dir: str, write_dir: str, workload: str, lin_shape):
+    M, N, K = lin_shape
+    fe = _counter_means(fetch_dir, "FETCH_SIZE")
+    wr = _counter_means(write_dir, "WRITE_SIZE")
+    f_fetch = COPY_BYTES / (fe["copy"] * 1024.0)
+    f_write = COPY_BYTES / (wr["copy"] * 1024.0)
+    traffic = fe["gemm"] * 1024.0 * f_fetch + wr["gemm"] * 1024.0 * f_write
+    d = {
+        "kernel_source_sha256": sources_sha(GEMM_SOURCES),
+        "workload": f"w8a8_linear {M}x{K}->{N}",
+        "fetch_kib_per_launch": round(fe["gemm"], 1),
+        "write_kib_per_launch": round(wr["gemm"], 1),
+        "calibration": {"kernel": "y = -x (float32)", "bytes_read": COPY_BYTES,
+                        "bytes_written": COPY_BYTES,
+                        "fetch_kib": round(fe["copy"], 1), "write_kib": round(wr["copy"], 1),
+                        "fetch_factor": round(f_fetch, 4), "write_factor": round(f_write, 4)},
+        "hbm_bytes_per_launch": int(round(traffic)),
+        "algorithmic_bytes_per_launch": M * K + N * K + 2 * M * N + 4 * M + 4 * N + 2 * N,
+        "commands": [
+            f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {fetch_dir} -o run -- "
+            f"python -u bench.py --workload {workload} --counter-run",
+            f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {write_dir} -o run -- "
+            f"python -u bench.py --workload {workload} --counter-run",
+            f"python bench.py --workload {workload} --counters-from {fetch_dir} {write_dir}",
+        ],
+    }
+    path = os.path.join(ROOT, "profiles", f"gemm_{workload}_counters.json")
+    with open(path, "w") as f:
+        json.dump(d, f, indent=1)
+        f.write("\n")
+    print(json.dumps(d))
+
+
 # --------------------------------------------------------------------------
 
 def main():
@@ -322,12 +419,21 @@ def main():
     ap.add_argument("--pool", type=int, default=4, help="distinct inputs rotated over steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--counter-run", action="store_true",
+                    help="only the short launch sequence the counter passes profile")
+    ap.add_argument("--counters-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 counter runs into profiles/ (no GPU)")
     args = ap.parse_args()
 
+    if args.counters_from:
+        shapes = {"ffn_up": (synth.TOKENS, 16384, 4096), "ffn_down": (synth.TOKENS, 4096, 16384)}
+        counters_from(*args.counters_from, args.workload, shapes[args.workload])
+        return
+
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the W8A8 linear shards by CFG branch or token rows with no exchange; "
-              "run --gpus 1)", file=sys.stderr)
+        print("bench.py measures one GPU only and has no multi-GPU path "
+              "(the W8A8 linear shards by CFG branch or token rows with no exchange "
+              "between GPUs); run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -341,6 +447,9 @@ def main():
     torch.cuda.synchronize()
     log(f"workload {args.workload}: {len(layers)} linears prepared in "
         f"{time.perf_counter() - t_build:.1f} s")
+    if args.counter_run:
+        counter_run(layers, dev)
+        return
 
     # per-kernel durations inside the timed steps (events between kernels)
     step_ms_ev, _, quant_us, gemm_us = measure(layers, args.steps, args.warmup, dev, True)

@@ -5,29 +5,39 @@
 //
 // Both operands are K-contiguous ("NT": X [M][K], W [N][K]), the natural
 // layout for MFMA, where each lane feeds 16 contiguous bytes of one row per
-// instruction. The kernel works on 16-byte chunks along K, so one skeleton
+// instruction. The kernels work on 16-byte chunks along K, so one skeleton
 // serves both element types: v_mfma_i32_32x32x32_i8 consumes 32 int8 of a row
 // and v_mfma_f32_32x32x16_bf16 16 bf16, i.e. two chunks either way.
 //
-// One workgroup computes a BM x BN tile of Y with WAVES_M x WAVES_N waves.
+// A workgroup computes a BM x BN tile of Y.
 //
 //   global -> LDS: direct-to-LDS buffer loads (buffer_load_dwordx4 ... lds),
 //     no VGPR staging. Each wave instruction fills 1 KiB of LDS; the global
 //     address of every lane is chosen so that the 16-byte chunks land
-//     XOR-swizzled (chunk c of row r at chunk c ^ ((r >> SWZ) & (CPR-1))),
-//     which keeps the fragment reads free of bank conflicts. The loads are
-//     range-checked: rows past M/N and the K tail read as zero.
-//   pipeline: a ring of STAGES K-tiles in LDS; STAGES-1 tiles are in flight
-//     while one is multiplied. Waits are explicit (s_waitcnt vmcnt(n) on the
-//     wave's own loads, then s_barrier for the other waves'), so prefetches
-//     stay in flight across iterations. MFMA fragments are double-buffered
-//     in registers: the next step's LDS reads overlap the current MFMAs, also
-//     across the tile boundary.
+//     XOR-swizzled (chunk c of row r at chunk c ^ ((r >> SWZ) & (CPR-1))).
+//     The LDS has 64 banks and serves a 16-byte read for 16 lanes per cycle,
+//     i.e. 256 bytes = 256/BK rows, so SWZ = log2(256/BK) makes the fragment
+//     reads conflict-free. Loads are range-checked: rows past M/N read as 0.
+//   pipeline: a ring of STAGES K tiles in LDS. Waits are explicit
+//     (s_waitcnt vmcnt(n) on a wave's own loads, then s_barrier without a
+//     memory fence, which would drain every prefetch).
 //   MFMA: the W tile feeds the instruction's first operand and the X tile
 //     its second, so C = W X^T and lane l holds token m = l % 32 of a 32x32
 //     block with 4 consecutive output channels per accumulator quad.
+//     Fragments are double-buffered in registers: the next step's LDS reads
+//     overlap the current MFMAs, also across tile boundaries.
 //   epilogue: y = float(acc) * (x_scale[m] * w_scale[n]) + bias[n] with one
 //     fma, four channels packed into 8 bytes of bf16 per store.
+//
+// Two kernels share this skeleton:
+//   gemm_kernel     every wave loads and multiplies (used when the K tile is
+//                   64 bytes, i.e. K not a multiple of 128 bytes);
+//   gemm_ws_kernel  warp-specialized: NPROD producer waves only issue the
+//                   tile loads, the WAVES_M x WAVES_N consumer waves only read
+//                   fragments and run MFMAs. With one wave doing both, the
+//                   in-order issue stalls the MFMA stream whenever the load
+//                   path pushes back; split across waves that share a SIMD,
+//                   loads and MFMAs proceed side by side.
 //
 // Launch order is XCD-aware: workgroups are dispatched round-robin over the
 // 8 XCDs, so block id b runs on XCD b % 8. Each XCD is given a contiguous
@@ -46,7 +56,6 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef float v16f __attribute__((ext_vector_type(16)));
-typedef float v4f __attribute__((ext_vector_type(4)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef unsigned int v2u __attribute__((ext_vector_type(2)));
 
@@ -64,8 +73,6 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
     return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));  // v_cvt_pk_bf16_f32 (RNE)
 }
 
-__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
-
 // s_waitcnt with only vmcnt constrained (gfx9 encoding: vmcnt[3:0] in bits
 // 3:0 and vmcnt[5:4] in bits 15:14; expcnt and lgkmcnt left at their maxima).
 template <int N>
@@ -74,10 +81,29 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0f70);
 }
 
-// Workgroup barrier without a memory fence: a fence would drain every
-// outstanding global load, i.e. the prefetch pipeline. Ordering of LDS
-// accesses around it is by the explicit waits; the empty asm statements keep
-// the compiler from moving memory operations across.
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xc07f); }
+
+// Device-only builtins are wrapped in __device__ functions: used directly in
+// a __global__ template body they make the host-side instantiation fail,
+// which silently drops the kernel's host stub.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, int8_t *lds, uint32_t off) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LDS_AS void *)lds, 16, off, 0, 0, 0);
+}
+// A no-op that mentions an AGPR. A kernel limited to 256 registers per wave
+// that never names an AGPR gets its MFMAs in the VGPR form (accumulators in
+// VGPRs), which measured ~20% slower here than the AGPR form: the MFMA's
+// accumulator traffic then competes with the fragment reads for VGPR ports.
+__device__ __forceinline__ void prefer_agpr_mfma() { asm volatile("" ::"a"(0)); }
+__device__ __forceinline__ void keep_args(const void *a, const void *b, const void *c,
+                                          const void *d) {
+    asm volatile("" ::"s"(a), "s"(b), "s"(c), "s"(d));
+}
+
+// Workgroup barrier without a memory fence. Ordering of LDS accesses around
+// it is by the explicit waits; the empty asm statements keep the compiler
+// from moving memory operations across.
 __device__ __forceinline__ void barrier() {
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
@@ -117,63 +143,22 @@ __device__ __forceinline__ void map_tile(int pid, int tiles_m, int tiles_n, int 
     tn = in / gm;
 }
 
-template <class Op, int BM, int BN, int BK, int WAVES_M, int WAVES_N, int STAGES, int SWZ,
-          int GROUP_M, int EPI, bool N_VEC, bool HAS_BIAS>
-__global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_kernel(
-    const int8_t *__restrict__ X, const int8_t *__restrict__ W, const float *__restrict__ xs,
-    const float *__restrict__ ws, const uint16_t *__restrict__ bias, int M, int N, int Kb,
-    void *__restrict__ Yout, int tiles_m, int tiles_n) {
-    constexpr int NW = WAVES_M * WAVES_N;
-    constexpr int WTM = BM / WAVES_M;   // tokens per wave
-    constexpr int WTN = BN / WAVES_N;   // channels per wave
-    constexpr int TJ = WTM / 32;        // 32-token blocks per wave
-    constexpr int TI = WTN / 32;        // 32-channel blocks per wave
-    constexpr int CPR = BK / 16;        // 16-byte chunks per tile row
-    constexpr int ROWS_PER_KB = 1024 / BK;
-    constexpr int LA = BM * BK / 1024 / NW;  // 1 KiB DMA blocks per wave, X tile
-    constexpr int LB = BN * BK / 1024 / NW;  // ... W tile
-    constexpr int LOADS = LA + LB;
-    constexpr int KSTEPS = BK / 32;
-    constexpr int STAGE = (BM + BN) * BK;
-    static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be whole 32x32 blocks");
-    static_assert(LA * NW * 1024 == BM * BK && LB * NW * 1024 == BN * BK, "DMA split");
-    static_assert(CPR == 4 || CPR == 8, "K tile of 64 or 128 bytes");
-    static_assert(STAGES >= 2 && LOADS * (STAGES - 2) < 64, "vmcnt range");
-    static_assert(KSTEPS % 2 == 0, "fragment buffer 0 starts every tile");
-    static_assert(STAGES * STAGE <= 160 * 1024, "LDS");
+// Epilogue of one wave: its TJ x 32 tokens starting at row mbase of the tile
+// and its TI x 32 channels starting at channel nbase. In block (i, j),
+// accumulator element r of lane l holds channel 32 i + 8 (r / 4) + 4 (l / 32)
+// + r % 4 and token 32 j + l % 32: each quad r = 4g..4g+3 is 4 consecutive
+// channels. The operands are loaded once, before the main loop.
+template <int TI, int TJ, int EPI, bool N_VEC, bool HAS_BIAS>
+struct Epi {
+    float xs_[TJ];
+    float ws_[TI][4][4];
+    uint32_t b_[TI][4][2];  // bf16 pairs, converted when stored
 
-    __shared__ __attribute__((aligned(1024))) int8_t smem[STAGES * STAGE];
-
-    // Materialize the epilogue's pointer arguments now: a scalar load of a
-    // kernel argument left pending into the main loop would make every LDS
-    // wait there a full lgkmcnt(0) (scalar loads complete out of order).
-    asm volatile("" ::"s"(xs), "s"(ws), "s"(bias), "s"(Yout));
-
-    int tm, tn;
-    map_tile<GROUP_M>(blockIdx.x, tiles_m, tiles_n, tm, tn);
-    const int m0 = tm * BM;
-    const int n0 = tn * BN;
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int wm = wave / WAVES_N;
-    const int wn = wave % WAVES_N;
-
-    const int rows_x = min(BM, M - m0);
-    const int rows_w = min(BN, N - n0);
-
-    // Epilogue operands of this lane, loaded up front (before the tile loads,
-    // so that the in-order vmcnt accounting below is unaffected): x_scale of
-    // its TJ tokens, w_scale and bias of its TI x 4 x 4 channels. Channel
-    // quad g of block i is n = n0 + wn*WTN + 32 i + 8 g + 4 (l / 32) + e.
-    const int frow = lane & 31;
-    const int fhalf = lane >> 5;
-    float ep_xs[TJ];
-    float ep_ws[TI][4][4];
-    uint32_t ep_b[TI][4][2];  // bf16 pairs, converted in the epilogue
-    {
+    __device__ __forceinline__ void load(const float *xs, const float *ws, const uint16_t *bias,
+                                         int m0, int rows_x, int mbase, int nbase, int N, int frow,
+                                         int fhalf) {
         // Range-checked loads (zero past M / N, or for a missing bias): no
-        // branch, and nothing consumes them before the epilogue, so the
-        // compiler waits for them only there.
+        // branch, and nothing consumes them before the epilogue.
         const __amdgpu_buffer_rsrc_t rxs =
             make_rsrc(EPI == kDequantBf16 ? xs + m0 : nullptr,
                       EPI == kDequantBf16 ? static_cast<uint32_t>(rows_x) * 4u : 0u);
@@ -183,15 +168,15 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_kernel(
             make_rsrc(bias, HAS_BIAS ? static_cast<uint32_t>(N) * 2u : 0u);
 #pragma unroll
         for (int j = 0; j < TJ; ++j) {
-            const uint32_t ml = wm * WTM + 32 * j + frow;
-            ep_xs[j] = __builtin_bit_cast(float,
-                                          __builtin_amdgcn_raw_buffer_load_b32(rxs, ml * 4u, 0, 0));
+            const uint32_t ml = mbase + 32 * j + frow;
+            xs_[j] = __builtin_bit_cast(float,
+                                        __builtin_amdgcn_raw_buffer_load_b32(rxs, ml * 4u, 0, 0));
         }
 #pragma unroll
         for (int i = 0; i < TI; ++i)
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                const uint32_t n = n0 + wn * WTN + 32 * i + 8 * g + 4 * fhalf;
+                const uint32_t n = nbase + 32 * i + 8 * g + 4 * fhalf;
                 if constexpr (N_VEC) {
                     // N % 4 == 0 (and w_scale / bias aligned): the 4 channels are all
                     // inside or all outside; outside, a valid address is read and
@@ -202,29 +187,29 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_kernel(
                     const uint32_t nc = ok ? n : 0u;
                     if constexpr (EPI == kDequantBf16) {
                         const float4 w4 = *reinterpret_cast<const float4 *>(ws + nc);
-                        ep_ws[i][g][0] = ok ? w4.x : 0.0f;
-                        ep_ws[i][g][1] = ok ? w4.y : 0.0f;
-                        ep_ws[i][g][2] = ok ? w4.z : 0.0f;
-                        ep_ws[i][g][3] = ok ? w4.w : 0.0f;
+                        ws_[i][g][0] = ok ? w4.x : 0.0f;
+                        ws_[i][g][1] = ok ? w4.y : 0.0f;
+                        ws_[i][g][2] = ok ? w4.z : 0.0f;
+                        ws_[i][g][3] = ok ? w4.w : 0.0f;
                     } else {
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) ep_ws[i][g][e] = 0.0f;
+                        for (int e = 0; e < 4; ++e) ws_[i][g][e] = 0.0f;
                     }
-                    ep_b[i][g][0] = 0u;
-                    ep_b[i][g][1] = 0u;
+                    b_[i][g][0] = 0u;
+                    b_[i][g][1] = 0u;
                     if constexpr (HAS_BIAS) {
                         const uint2 b2 = *reinterpret_cast<const uint2 *>(bias + nc);
-                        ep_b[i][g][0] = ok ? b2.x : 0u;
-                        ep_b[i][g][1] = ok ? b2.y : 0u;
+                        b_[i][g][0] = ok ? b2.x : 0u;
+                        b_[i][g][1] = ok ? b2.y : 0u;
                     }
                 } else {
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
-                        ep_ws[i][g][e] = __builtin_bit_cast(
+                        ws_[i][g][e] = __builtin_bit_cast(
                             float, __builtin_amdgcn_raw_buffer_load_b32(rws, (n + e) * 4u, 0, 0));
 #pragma unroll
                     for (int h = 0; h < 2; ++h)
-                        ep_b[i][g][h] =
+                        b_[i][g][h] =
                             __builtin_amdgcn_raw_buffer_load_b16(rbs, (n + 2 * h) * 2u, 0, 0) |
                             static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(
                                 rbs, (n + 2 * h + 1) * 2u, 0, 0))
@@ -232,123 +217,258 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_kernel(
                 }
             }
     }
-    // These loads must stay older than every tile load: the vmcnt waits of
-    // the pipeline below count only tile loads as younger. (They are global
-    // loads and the tile loads write LDS, so nothing else orders them.)
-    __builtin_amdgcn_sched_barrier(0);
+
+    // The same operands from the LDS copy written by fill_lds() (tile-local
+    // indices: token mbase.., channel nbase..).
+    __device__ __forceinline__ void load_lds(const float *xs_l, const float *ws_l,
+                                             const uint16_t *b_l, int mbase, int nbase, int frow,
+                                             int fhalf) {
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) xs_[j] = xs_l[mbase + 32 * j + frow];
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int n = nbase + 32 * i + 8 * g + 4 * fhalf;
+                const float4 w4 = *reinterpret_cast<const float4 *>(ws_l + n);
+                ws_[i][g][0] = w4.x;
+                ws_[i][g][1] = w4.y;
+                ws_[i][g][2] = w4.z;
+                ws_[i][g][3] = w4.w;
+                const uint2 b2 = *reinterpret_cast<const uint2 *>(b_l + n);
+                b_[i][g][0] = b2.x;
+                b_[i][g][1] = b2.y;
+            }
+    }
+
+    // Writes a tile's operands to LDS (one wave): x_scale of BM tokens,
+    // w_scale and bias of BN channels, zero past M / N or without a bias.
+    template <int BM, int BN>
+    __device__ static void fill_lds(float *xs_l, float *ws_l, uint16_t *b_l, const float *xs,
+                                    const float *ws, const uint16_t *bias, int m0, int rows_x,
+                                    int n0, int rows_w, int lane) {
+#pragma unroll
+        for (int t = lane; t < BM; t += 64)
+            xs_l[t] = (EPI == kDequantBf16 && t < rows_x) ? xs[m0 + t] : 0.0f;
+#pragma unroll
+        for (int t = lane; t < BN; t += 64) {
+            ws_l[t] = (EPI == kDequantBf16 && t < rows_w) ? ws[n0 + t] : 0.0f;
+            b_l[t] = (HAS_BIAS && t < rows_w) ? bias[n0 + t] : static_cast<uint16_t>(0);
+        }
+    }
+
+    template <class Acc>
+    __device__ __forceinline__ void store(const Acc (&acc)[TI][TJ], void *Yout, int m0,
+                                          int rows_x, int mbase, int nbase, int N, int frow,
+                                          int fhalf) const {
+        constexpr uint32_t kYBytes = EPI == kStoreI32 ? 4u : 2u;
+        const __amdgpu_buffer_rsrc_t ry =
+            make_rsrc(static_cast<int8_t *>(Yout) + static_cast<int64_t>(m0) * N * kYBytes,
+                      static_cast<uint32_t>(rows_x) * N * kYBytes);
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) {
+            const uint32_t row_off = static_cast<uint32_t>(mbase + 32 * j + frow) * N;
+#pragma unroll
+            for (int i = 0; i < TI; ++i) {
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int n = nbase + 32 * i + 8 * g + 4 * fhalf;
+                    if constexpr (EPI == kStoreI32) {
+                        if (N_VEC && n + 3 < N) {
+                            const v4i v = {acc[i][j][4 * g], acc[i][j][4 * g + 1],
+                                           acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+                            __builtin_amdgcn_raw_buffer_store_b128(v, ry, (row_off + n) * 4u, 0, 0);
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                const uint32_t off =
+                                    n + e < N ? (row_off + n + e) * 4u : kOutOfRange;
+                                __builtin_amdgcn_raw_buffer_store_b32(acc[i][j][4 * g + e], ry, off,
+                                                                      0, 0);
+                            }
+                        }
+                    } else {
+                        uint32_t h[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const float a = static_cast<float>(acc[i][j][4 * g + e]);
+                            const uint32_t bw = b_[i][g][e >> 1];
+                            const float b =
+                                __uint_as_float((e & 1) ? (bw & 0xffff0000u) : (bw << 16));
+                            float y;
+                            if constexpr (EPI == kDequantBf16)
+                                y = __builtin_fmaf(a, xs_[j] * ws_[i][g][e], b);
+                            else
+                                y = a + b;
+                            h[e] = f32_to_bf16_bits(y);
+                        }
+                        if (N_VEC && n + 3 < N) {
+                            const v2u v = {h[0] | h[1] << 16, h[2] | h[3] << 16};
+                            __builtin_amdgcn_raw_buffer_store_b64(v, ry, (row_off + n) * 2u, 0, 0);
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                const uint32_t off =
+                                    n + e < N ? (row_off + n + e) * 2u : kOutOfRange;
+                                __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(h[e]),
+                                                                      ry, off, 0, 0);
+                            }
+                        }
+                    }
+                }
+            }
+        }
+    }
+};
+
+// MFMA side of one wave: fragment reads from an LDS slot and the MFMAs of a
+// WTN x WTM wave tile (TI channel blocks, TJ token blocks). Lane l reads row
+// l % 32 of a 32-row block, chunk 2 s + l / 32 of the K tile; the swizzle key
+// depends on l only.
+template <class Op, int BM, int BK, int TI, int TJ, int SWZ>
+struct Mma {
+    static constexpr int CPR = BK / 16;
+    typename Op::Acc acc[TI][TJ];
+    v4i wf[2][TI];
+    v4i xf[2][TJ];
+    int x_base, w_base, fhalf, fkey;
+
+    __device__ __forceinline__ void init(int lane, int mbase, int nbase) {
+        const int frow = lane & 31;
+        fhalf = lane >> 5;
+        fkey = (frow >> SWZ) & (CPR - 1);
+        x_base = (mbase + frow) * BK;
+        w_base = BM * BK + (nbase + frow) * BK;
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+            for (int j = 0; j < TJ; ++j) acc[i][j] = typename Op::Acc{};
+    }
+    __device__ __forceinline__ void load(const int8_t *slot, int s, int buf) {
+        const int chunk = (2 * s + fhalf) ^ fkey;
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+            wf[buf][i] = *reinterpret_cast<const v4i *>(slot + w_base + i * 32 * BK + chunk * 16);
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+            xf[buf][j] = *reinterpret_cast<const v4i *>(slot + x_base + j * 32 * BK + chunk * 16);
+    }
+    __device__ __forceinline__ void step(int buf) {
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+            for (int j = 0; j < TJ; ++j) acc[i][j] = Op::mma(wf[buf][i], xf[buf][j], acc[i][j]);
+    }
+    // One K tile whose data is in `slot`. Steps 0..KSTEPS-2 read the next
+    // step's fragments, then run the current MFMAs. Before the last step
+    // comes `boundary()` (the tile hand-over, see the kernels) unless this is
+    // the last tile; it ends by reading the next tile's first fragments.
+    // Scheduling barriers keep each group of reads ahead of the MFMAs it
+    // overlaps (the compiler would otherwise sink the reads to their uses).
+    template <bool LAST, class Boundary>
+    __device__ __forceinline__ void tile(const int8_t *slot, Boundary &&boundary) {
+        constexpr int KSTEPS = BK / 32;
+        static_assert(KSTEPS % 2 == 0, "fragment buffer 0 starts every tile");
+#pragma unroll
+        for (int s = 0; s + 1 < KSTEPS; ++s) {
+            load(slot, s + 1, (s + 1) & 1);
+            sched_fence();
+            step(s & 1);
+            sched_fence();
+        }
+        if constexpr (!LAST) {
+            boundary();
+            sched_fence();
+        }
+        step((KSTEPS - 1) & 1);
+        sched_fence();
+    }
+};
+
+// Lane l of 1 KiB DMA block `blk` of a BK-wide tile writes LDS bytes
+// [blk*1024 + 16 l, +16) = row blk*(1024/BK) + l / CPR, physical chunk
+// l % CPR, which holds logical chunk (l % CPR) ^ swizzle(row). Returns the
+// lane's source offset within the panel at K tile 0.
+template <int BK, int SWZ>
+__device__ __forceinline__ uint32_t dma_offset(int blk, int lane, int Kb) {
+    constexpr int CPR = BK / 16;
+    const int row = blk * (1024 / BK) + lane / CPR;
+    const int chunk = (lane % CPR) ^ ((row >> SWZ) & (CPR - 1));
+    return static_cast<uint32_t>(row) * Kb + chunk * 16;
+}
+
+// --------------------------------------------------------------------------
+// gemm_kernel: every wave loads and multiplies.
+// --------------------------------------------------------------------------
+template <class Op, int BM, int BN, int BK, int WAVES_M, int WAVES_N, int STAGES, int SWZ,
+          int GROUP_M, int EPI, bool N_VEC, bool HAS_BIAS>
+__global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_kernel(
+    const int8_t *__restrict__ X, const int8_t *__restrict__ W, const float *__restrict__ xs,
+    const float *__restrict__ ws, const uint16_t *__restrict__ bias, int M, int N, int Kb,
+    void *__restrict__ Yout, int tiles_m, int tiles_n) {
+    constexpr int NW = WAVES_M * WAVES_N;
+    constexpr int WTM = BM / WAVES_M;  // tokens per wave
+    constexpr int WTN = BN / WAVES_N;  // channels per wave
+    constexpr int TJ = WTM / 32;
+    constexpr int TI = WTN / 32;
+    constexpr int LA = BM * BK / 1024 / NW;  // 1 KiB DMA blocks per wave, X tile
+    constexpr int LB = BN * BK / 1024 / NW;  // ... W tile
+    constexpr int LOADS = LA + LB;
+    constexpr int STAGE = (BM + BN) * BK;
+    static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be whole 32x32 blocks");
+    static_assert(LA * NW * 1024 == BM * BK && LB * NW * 1024 == BN * BK, "DMA split");
+    static_assert(BK == 64 || BK == 128, "K tile of 64 or 128 bytes");
+    static_assert(STAGES >= 2 && LOADS * (STAGES - 2) < 64, "vmcnt range");
+    static_assert(STAGES * STAGE <= 160 * 1024, "LDS");
+
+    __shared__ __attribute__((aligned(1024))) int8_t smem[STAGES * STAGE];
+
+    // Materialize the epilogue's pointer arguments now: a scalar load of a
+    // kernel argument left pending into the main loop would make every LDS
+    // wait there a full lgkmcnt(0) (scalar loads complete out of order).
+    keep_args(xs, ws, bias, Yout);
+
+    int tm, tn;
+    map_tile<GROUP_M>(blockIdx.x, tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * BM;
+    const int n0 = tn * BN;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int mbase = (wave / WAVES_N) * WTM;
+    const int nbase = (wave % WAVES_N) * WTN;
+    const int rows_x = min(BM, M - m0);
+    const int rows_w = min(BN, N - n0);
+
+    // Epilogue operands first, and kept older than every tile load: the vmcnt
+    // waits below count only tile loads as younger. (They are global loads
+    // and the tile loads write LDS, so nothing else orders them.)
+    Epi<TI, TJ, EPI, N_VEC, HAS_BIAS> epi;
+    epi.load(xs, ws, bias, m0, rows_x, mbase, n0 + nbase, N, lane & 31, lane >> 5);
+    sched_fence();
 
     const __amdgpu_buffer_rsrc_t rx =
         make_rsrc(X + static_cast<int64_t>(m0) * Kb, static_cast<uint32_t>(rows_x) * Kb);
     const __amdgpu_buffer_rsrc_t rw =
         make_rsrc(W + static_cast<int64_t>(n0) * Kb, static_cast<uint32_t>(rows_w) * Kb);
-
-    // DMA source offsets. Lane l of the wave's i-th block writes LDS bytes
-    // [blk*1024 + 16 l, +16) = row (blk*ROWS_PER_KB + l / CPR), physical
-    // chunk l % CPR, which holds logical chunk (l % CPR) ^ swizzle(row).
-    const int dma_row = lane / CPR;
-    const int dma_phys = lane % CPR;
     uint32_t off_x[LA], off_w[LB];
-    int chunk_x[LA], chunk_w[LB];
 #pragma unroll
-    for (int i = 0; i < LA; ++i) {
-        const int row = (wave + i * NW) * ROWS_PER_KB + dma_row;
-        chunk_x[i] = dma_phys ^ ((row >> SWZ) & (CPR - 1));
-        off_x[i] = static_cast<uint32_t>(row) * Kb + chunk_x[i] * 16;
-    }
+    for (int i = 0; i < LA; ++i) off_x[i] = dma_offset<BK, SWZ>(wave + i * NW, lane, Kb);
 #pragma unroll
-    for (int i = 0; i < LB; ++i) {
-        const int row = (wave + i * NW) * ROWS_PER_KB + dma_row;
-        chunk_w[i] = dma_phys ^ ((row >> SWZ) & (CPR - 1));
-        off_w[i] = static_cast<uint32_t>(row) * Kb + chunk_w[i] * 16;
-    }
+    for (int i = 0; i < LB; ++i) off_w[i] = dma_offset<BK, SWZ>(wave + i * NW, lane, Kb);
 
-    const int KT = (Kb + BK - 1) / BK;
+    const int KT = Kb / BK;  // the launcher guarantees BK divides Kb
     auto issue = [&](int kt) {
         int8_t *slot = smem + (kt % STAGES) * STAGE;
         const int kb = kt * BK;
 #pragma unroll
-        for (int i = 0; i < LA; ++i) {
-            const uint32_t off = kb + chunk_x[i] * 16 < Kb ? off_x[i] + kb : kOutOfRange;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rx, (LDS_AS void *)(slot + (wave + i * NW) * 1024), 16, off, 0, 0, 0);
-        }
+        for (int i = 0; i < LA; ++i) dma16(rx, slot + (wave + i * NW) * 1024, off_x[i] + kb);
 #pragma unroll
-        for (int i = 0; i < LB; ++i) {
-            const uint32_t off = kb + chunk_w[i] * 16 < Kb ? off_w[i] + kb : kOutOfRange;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rw, (LDS_AS void *)(slot + BM * BK + (wave + i * NW) * 1024), 16, off, 0, 0, 0);
-        }
+        for (int i = 0; i < LB; ++i)
+            dma16(rw, slot + BM * BK + (wave + i * NW) * 1024, off_w[i] + kb);
     };
 
-    // Fragment reads: lane reads row (l % 32) of a 32-row block, chunk
-    // 2 s + l / 32 of the K tile; the swizzle key depends on l only.
-    const int fkey = (frow >> SWZ) & (CPR - 1);
-    const int x_base = (wm * WTM + frow) * BK;
-    const int w_base = BM * BK + (wn * WTN + frow) * BK;
-
-    typename Op::Acc acc[TI][TJ];
-#pragma unroll
-    for (int i = 0; i < TI; ++i)
-#pragma unroll
-        for (int j = 0; j < TJ; ++j) acc[i][j] = typename Op::Acc{};
-
-    // Fragments of one MFMA step, double-buffered: the next step's are read
-    // from LDS while the current step's MFMAs run.
-    v4i wf[2][TI];
-    v4i xf[2][TJ];
-    auto load_frags = [&](const int8_t *slot, int s, v4i(&wb)[TI], v4i(&xb)[TJ]) {
-        const int chunk = (2 * s + fhalf) ^ fkey;
-#pragma unroll
-        for (int i = 0; i < TI; ++i)
-            wb[i] = *reinterpret_cast<const v4i *>(slot + w_base + i * 32 * BK + chunk * 16);
-#pragma unroll
-        for (int j = 0; j < TJ; ++j)
-            xb[j] = *reinterpret_cast<const v4i *>(slot + x_base + j * 32 * BK + chunk * 16);
-    };
-
-    auto mfma_step = [&](int cur) {
-#pragma unroll
-        for (int i = 0; i < TI; ++i)
-#pragma unroll
-            for (int j = 0; j < TJ; ++j) acc[i][j] = Op::mma(wf[cur][i], xf[cur][j], acc[i][j]);
-    };
-
-    // One K tile. Steps 0..KSTEPS-2 read the next step's fragments, then run
-    // the current MFMAs. Before the last step comes the tile boundary: every
-    // read of tile kt has completed (the last ones were issued a whole MFMA
-    // step ago); once this wave's loads of tile kt+1 are in and all waves
-    // meet, slot kt is refilled with tile kt+STAGES (ISSUE) and tile kt+1's
-    // first fragments are read. Scheduling barriers keep each group of reads
-    // ahead of the MFMAs it overlaps (the compiler would otherwise sink the
-    // reads to their uses), and the loops below are branch-free so that the
-    // compiler's own waits stay exact (lgkmcnt(n) on the older reads only).
-    auto tile = [&](int kt, auto issue_tag, auto vm_tag, auto last_tag) {
-        constexpr bool ISSUE = decltype(issue_tag)::value;
-        constexpr int VM = decltype(vm_tag)::value;
-        constexpr bool LAST = decltype(last_tag)::value;
-        const int8_t *slot = smem + (kt % STAGES) * STAGE;
-#pragma unroll
-        for (int s = 0; s + 1 < KSTEPS; ++s) {
-            load_frags(slot, s + 1, wf[(s + 1) & 1], xf[(s + 1) & 1]);
-            __builtin_amdgcn_sched_barrier(0);
-            mfma_step(s & 1);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        if constexpr (!LAST) {
-            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
-            wait_vmcnt<VM>();
-            barrier();
-            if constexpr (ISSUE) issue(kt + STAGES);
-            load_frags(smem + ((kt + 1) % STAGES) * STAGE, 0, wf[0], xf[0]);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        mfma_step((KSTEPS - 1) & 1);
-        __builtin_amdgcn_sched_barrier(0);
-    };
-    using T = std::true_type;
-    using F = std::false_type;
-    using VM_STEADY = std::integral_constant<int, LOADS * (STAGES - 2)>;
-    using VM_ALL = std::integral_constant<int, 0>;
+    Mma<Op, BM, BK, TI, TJ, SWZ> mma;
+    mma.init(lane, mbase, nbase);
 
     // Prologue: tiles 0..STAGES-2 in flight; once tile 0 has landed the last
     // slot is issued too and the first fragments are read.
@@ -361,125 +481,286 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_kernel(
         wait_vmcnt<0>();
     barrier();
     if (STAGES - 1 < KT) issue(STAGES - 1);
-    load_frags(smem, 0, wf[0], xf[0]);
+    mma.load(smem, 0, 0);
 
+    // Tile boundary kt -> kt+1: every read of tile kt has completed (the last
+    // ones were issued a whole MFMA step ago); once this wave's loads of tile
+    // kt+1 are in and all waves meet, slot kt is refilled with tile
+    // kt+STAGES and tile kt+1's first fragments are read. The three loops are
+    // branch-free so that the compiler's own waits stay exact.
     int kt = 0;
-    for (; kt + STAGES < KT; ++kt) tile(kt, T{}, VM_STEADY{}, F{});   // refill as we go
-    for (; kt + 1 < KT; ++kt) tile(kt, F{}, VM_ALL{}, F{});           // drain the ring
-    tile(kt, F{}, VM_ALL{}, T{});                                     // last tile
+    for (; kt + STAGES < KT; ++kt)  // refill as we go
+        mma.template tile<false>(smem + (kt % STAGES) * STAGE, [&] {
+            wait_lgkmcnt0();
+            wait_vmcnt<LOADS * (STAGES - 2)>();
+            barrier();
+            issue(kt + STAGES);
+            mma.load(smem + ((kt + 1) % STAGES) * STAGE, 0, 0);
+        });
+    for (; kt + 1 < KT; ++kt)  // drain the ring
+        mma.template tile<false>(smem + (kt % STAGES) * STAGE, [&] {
+            wait_lgkmcnt0();
+            wait_vmcnt<0>();
+            barrier();
+            mma.load(smem + ((kt + 1) % STAGES) * STAGE, 0, 0);
+        });
+    mma.template tile<true>(smem + (kt % STAGES) * STAGE, [] {});
 
-    // Epilogue. In block (i, j), accumulator element r of lane l holds
-    // channel 32 i + 8 (r / 4) + 4 (l / 32) + r % 4 and token 32 j + l % 32
-    // of the wave tile: each quad r = 4g..4g+3 is 4 consecutive channels.
-    constexpr uint32_t kYBytes = EPI == kStoreI32 ? 4u : 2u;
-    const __amdgpu_buffer_rsrc_t ry =
-        make_rsrc(static_cast<int8_t *>(Yout) + static_cast<int64_t>(m0) * N * kYBytes,
-                  static_cast<uint32_t>(rows_x) * N * kYBytes);
+    epi.store(mma.acc, Yout, m0, rows_x, mbase, n0 + nbase, N, lane & 31, lane >> 5);
+}
+
+// --------------------------------------------------------------------------
+// gemm_ws_kernel: NPROD producer waves issue the tile loads, WAVES_M x
+// WAVES_N consumer waves multiply. One barrier per K tile hands slots over:
+//   barrier #0: tile 0 has landed;
+//   between barrier #kt and #kt+1: consumers multiply tile kt; producers
+//     refill slot kt-1 (free: every consumer read of it completed before
+//     barrier #kt) with tile kt+STAGES-1, then wait for tile kt+1.
+// The launcher guarantees BK divides K (no K tail).
+// --------------------------------------------------------------------------
+template <class Op, int BM, int BN, int BK, int WAVES_M, int WAVES_N, int NPROD, int STAGES,
+          int SWZ, int GROUP_M, int EPI, bool N_VEC, bool HAS_BIAS>
+__global__ __launch_bounds__((WAVES_M * WAVES_N + NPROD) * 64) void gemm_ws_kernel(
+    const int8_t *__restrict__ X, const int8_t *__restrict__ W, const float *__restrict__ xs,
+    const float *__restrict__ ws, const uint16_t *__restrict__ bias, int M, int N, int Kb,
+    void *__restrict__ Yout, int tiles_m, int tiles_n) {
+    constexpr int NC = WAVES_M * WAVES_N;
+    constexpr int WTM = BM / WAVES_M;
+    constexpr int WTN = BN / WAVES_N;
+    constexpr int TJ = WTM / 32;
+    constexpr int TI = WTN / 32;
+    constexpr int NBX = BM * BK / 1024;      // 1 KiB DMA blocks per stage, X tile
+    constexpr int NBW = BN * BK / 1024;      // ... W tile
+    constexpr int LP = (NBX + NBW) / NPROD;  // blocks per producer wave
+    constexpr int STAGE = (BM + BN) * BK;
+    static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be whole 32x32 blocks");
+    static_assert(LP * NPROD == NBX + NBW, "DMA split");
+    static_assert(BK == 64 || BK == 128, "K tile of 64 or 128 bytes");
+    static_assert(STAGES >= 2 && LP * (STAGES - 2) < 64, "vmcnt range");
+    static_assert(STAGES * STAGE + 4 * BM + 6 * BN <= 160 * 1024, "LDS");
+
+    // LDS: the ring, then the tile's epilogue operands (x_scale [BM],
+    // w_scale [BN], bias [BN]).
+    constexpr int EP_BYTES = 4 * BM + 4 * BN + 2 * BN;
+    __shared__ __attribute__((aligned(1024))) int8_t smem[STAGES * STAGE + EP_BYTES];
+    float *ep_xs = reinterpret_cast<float *>(smem + STAGES * STAGE);
+    float *ep_ws = ep_xs + BM;
+    uint16_t *ep_b = reinterpret_cast<uint16_t *>(ep_ws + BN);
+    using EpiT = Epi<TI, TJ, EPI, N_VEC, HAS_BIAS>;
+    keep_args(xs, ws, bias, Yout);
+
+    int tm, tn;
+    map_tile<GROUP_M>(blockIdx.x, tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * BM;
+    const int n0 = tn * BN;
+    const int lane = threadIdx.x & 63;
+    const int wave = wave_id();
+    const int rows_x = min(BM, M - m0);
+    const int rows_w = min(BN, N - n0);
+    const int KT = Kb / BK;
+
+    if (wave >= NC) {
+        // ---------------- producer ----------------
+        const int p = wave - NC;
+        const __amdgpu_buffer_rsrc_t rx =
+            make_rsrc(X + static_cast<int64_t>(m0) * Kb, static_cast<uint32_t>(rows_x) * Kb);
+        const __amdgpu_buffer_rsrc_t rw =
+            make_rsrc(W + static_cast<int64_t>(n0) * Kb, static_cast<uint32_t>(rows_w) * Kb);
+        uint32_t off[LP];
 #pragma unroll
-    for (int j = 0; j < TJ; ++j) {
-        const int ml = wm * WTM + 32 * j + frow;  // token within the tile
-        const uint32_t row_off = static_cast<uint32_t>(ml) * N;
-#pragma unroll
-        for (int i = 0; i < TI; ++i) {
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int n = n0 + wn * WTN + 32 * i + 8 * g + 4 * fhalf;
-                if constexpr (EPI == kStoreI32) {
-                    if (N_VEC && n + 3 < N) {
-                        const v4i v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
-                                       acc[i][j][4 * g + 3]};
-                        __builtin_amdgcn_raw_buffer_store_b128(v, ry, (row_off + n) * 4u, 0, 0);
-                    } else {
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const uint32_t off = n + e < N ? (row_off + n + e) * 4u : kOutOfRange;
-                            __builtin_amdgcn_raw_buffer_store_b32(acc[i][j][4 * g + e], ry, off, 0,
-                                                                  0);
-                        }
-                    }
-                } else {
-                    uint32_t h[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float a = static_cast<float>(acc[i][j][4 * g + e]);
-                        float y;
-                        const uint32_t bw = ep_b[i][g][e >> 1];
-                        const float b = __uint_as_float((e & 1) ? (bw & 0xffff0000u) : (bw << 16));
-                        if constexpr (EPI == kDequantBf16)
-                            y = __builtin_fmaf(a, ep_xs[j] * ep_ws[i][g][e], b);
-                        else
-                            y = a + b;
-                        h[e] = f32_to_bf16_bits(y);
-                    }
-                    if (N_VEC && n + 3 < N) {
-                        const v2u v = {h[0] | h[1] << 16, h[2] | h[3] << 16};
-                        __builtin_amdgcn_raw_buffer_store_b64(v, ry, (row_off + n) * 2u, 0, 0);
-                    } else {
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const uint32_t off = n + e < N ? (row_off + n + e) * 2u : kOutOfRange;
-                            __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(h[e]), ry,
-                                                                  off, 0, 0);
-                        }
-                    }
-                }
-            }
+        for (int i = 0; i < LP; ++i) {
+            const int b = p * LP + i;
+            off[i] = dma_offset<BK, SWZ>(b < NBX ? b : b - NBX, lane, Kb);
         }
+        auto issue = [&](int t) {
+            int8_t *slot = smem + (t % STAGES) * STAGE;
+            const int kb = t * BK;
+#pragma unroll
+            for (int i = 0; i < LP; ++i) {
+                const int b = p * LP + i;  // X blocks first, then W blocks
+                dma16(b < NBX ? rx : rw, slot + b * 1024, off[i] + kb);
+            }
+        };
+#pragma unroll
+        for (int t = 0; t < STAGES - 1; ++t)
+            if (t < KT) issue(t);
+        if (STAGES - 1 <= KT)
+            wait_vmcnt<LP * (STAGES - 2)>();
+        else
+            wait_vmcnt<0>();
+        barrier();  // #0
+        int kt = 0;
+        for (; kt + STAGES - 1 < KT; ++kt) {
+            issue(kt + STAGES - 1);
+            wait_vmcnt<LP * (STAGES - 2)>();  // tile kt+1 has landed
+            barrier();                        // #kt+1
+        }
+        // Every tile load is issued: the first producer now stages the
+        // epilogue operands in LDS (their latency overlaps the last tiles).
+        if (EPI != kStoreI32 && p == 0) {
+            EpiT::template fill_lds<BM, BN>(ep_xs, ep_ws, ep_b, xs, ws, bias, m0, rows_x, n0,
+                                            rows_w, lane);
+            wait_lgkmcnt0();
+        }
+        for (; kt + 1 < KT; ++kt) {
+            wait_vmcnt<0>();
+            barrier();
+        }
+        barrier();  // final: the epilogue operands are in LDS
+        return;
     }
+
+    // ---------------- consumer ----------------
+    prefer_agpr_mfma();
+    const int mbase = (wave / WAVES_N) * WTM;
+    const int nbase = (wave % WAVES_N) * WTN;
+    Mma<Op, BM, BK, TI, TJ, SWZ> mma;
+    mma.init(lane, mbase, nbase);
+    barrier();  // #0
+    mma.load(smem, 0, 0);
+    int kt = 0;
+    for (; kt + 1 < KT; ++kt)
+        mma.template tile<false>(smem + (kt % STAGES) * STAGE, [&] {
+            wait_lgkmcnt0();  // every read of slot kt has completed
+            barrier();        // #kt+1: tile kt+1 has landed
+            mma.load(smem + ((kt + 1) % STAGES) * STAGE, 0, 0);
+        });
+    mma.template tile<true>(smem + (kt % STAGES) * STAGE, [] {});
+    barrier();  // final: the epilogue operands are in LDS
+
+    EpiT epi;
+    if (EPI != kStoreI32) epi.load_lds(ep_xs, ep_ws, ep_b, mbase, nbase, lane & 31, lane >> 5);
+    epi.store(mma.acc, Yout, m0, rows_x, mbase, n0 + nbase, N, lane & 31, lane >> 5);
+}
+
+// --------------------------------------------------------------------------
+// launchers
+// --------------------------------------------------------------------------
+
+struct GemmArgs {
+    const int8_t *X;
+    const int8_t *W;
+    const float *xs;
+    const float *ws;
+    const uint16_t *bias;
+    int M, N, Kb;
+    void *Y;
+    hipStream_t stream;
+};
+
+// The four instances of one configuration: vector epilogue operands (N % 4
+// == 0 with aligned w_scale / bias) or not, with or without a bias.
+template <template <bool, bool> class K>
+hipError_t dispatch(const GemmArgs &a, int EPI_is_i32, int BM, int BN, int threads) {
+    int tiles_m = (a.M + BM - 1) / BM;
+    int tiles_n = (a.N + BN - 1) / BN;
+    const dim3 grid(static_cast<unsigned>(static_cast<int64_t>(tiles_m) * tiles_n));
+    const bool has_bias = !EPI_is_i32 && a.bias != nullptr;
+    const bool n_vec = a.N % 4 == 0 && (reinterpret_cast<uintptr_t>(a.ws) & 15) == 0 &&
+                       (reinterpret_cast<uintptr_t>(a.bias) & 7) == 0;
+    const void *fn = n_vec ? (has_bias ? K<true, true>::fn() : K<true, false>::fn())
+                           : (has_bias ? K<false, true>::fn() : K<false, false>::fn());
+    const int8_t *X = a.X;
+    const int8_t *W = a.W;
+    const float *xs = a.xs;
+    const float *ws = a.ws;
+    const uint16_t *bias = a.bias;
+    int M = a.M, N = a.N, Kb = a.Kb;
+    void *Y = a.Y;
+    void *args[] = {&X, &W, &xs, &ws, &bias, &M, &N, &Kb, &Y, &tiles_m, &tiles_n};
+    return hipLaunchKernel(fn, grid, dim3(threads), args, 0, a.stream);
 }
 
 template <class Op, int BM, int BN, int BK, int WAVES_M, int WAVES_N, int STAGES, int SWZ,
           int GROUP_M, int EPI>
-hipError_t launch(const int8_t *X, const int8_t *W, const float *xs, const float *ws,
-                  const uint16_t *bias, int64_t M, int64_t N, int64_t Kb, void *Y,
-                  hipStream_t stream) {
-    const int tiles_m = static_cast<int>((M + BM - 1) / BM);
-    const int tiles_n = static_cast<int>((N + BN - 1) / BN);
-    const dim3 grid(static_cast<unsigned>(static_cast<int64_t>(tiles_m) * tiles_n));
-    const dim3 block(WAVES_M * WAVES_N * 64);
-    const bool has_bias = EPI != kStoreI32 && bias != nullptr;
-    const bool n_vec = N % 4 == 0 && (reinterpret_cast<uintptr_t>(ws) & 15) == 0 &&
-                       (reinterpret_cast<uintptr_t>(bias) & 7) == 0;
-    const int iM = static_cast<int>(M), iN = static_cast<int>(N), iK = static_cast<int>(Kb);
-#define W8A8_LAUNCH(NV, HB)                                                                     \
-    hipLaunchKernelGGL(                                                                          \
-        (gemm_kernel<Op, BM, BN, BK, WAVES_M, WAVES_N, STAGES, SWZ, GROUP_M, EPI, NV, HB>), grid, \
-        block, 0, stream, X, W, xs, ws, bias, iM, iN, iK, Y, tiles_m, tiles_n)
-    if (n_vec && has_bias)
-        W8A8_LAUNCH(true, true);
-    else if (n_vec)
-        W8A8_LAUNCH(true, false);
-    else if (has_bias)
-        W8A8_LAUNCH(false, true);
-    else
-        W8A8_LAUNCH(false, false);
-#undef W8A8_LAUNCH
-    return hipGetLastError();
+struct Uniform {
+    template <bool NV, bool HB>
+    struct K {
+        static const void *fn() {
+            return reinterpret_cast<const void *>(
+                &gemm_kernel<Op, BM, BN, BK, WAVES_M, WAVES_N, STAGES, SWZ, GROUP_M, EPI, NV, HB>);
+        }
+    };
+    static hipError_t launch(const GemmArgs &a) {
+        if (a.Kb % BK != 0) return hipErrorInvalidValue;
+        return dispatch<K>(a, EPI == kStoreI32, BM, BN, WAVES_M * WAVES_N * 64);
+    }
+};
+
+template <class Op, int BM, int BN, int BK, int WAVES_M, int WAVES_N, int NPROD, int STAGES,
+          int SWZ, int GROUP_M, int EPI>
+struct Specialized {
+    template <bool NV, bool HB>
+    struct K {
+        static const void *fn() {
+            return reinterpret_cast<const void *>(
+                &gemm_ws_kernel<Op, BM, BN, BK, WAVES_M, WAVES_N, NPROD, STAGES, SWZ, GROUP_M, EPI,
+                                NV, HB>);
+        }
+    };
+    static hipError_t launch(const GemmArgs &a) {
+        if (a.Kb % BK != 0) return hipErrorInvalidValue;
+        return dispatch<K>(a, EPI == kStoreI32, BM, BN, (WAVES_M * WAVES_N + NPROD) * 64);
+    }
+};
+
+// Fraction of the slots of ceil(tiles / 256) full rounds of the 256 CUs
+// (one workgroup per CU) that the tiles of an M x N output fill.
+double round_fill(int M, int N, int BM, int BN) {
+    const int64_t tiles = static_cast<int64_t>((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+    const int64_t rounds = (tiles + 255) / 256;
+    return static_cast<double>(tiles) / static_cast<double>(rounds * 256);
 }
 
-// 192 x 256 tiles (tokens x channels), four waves of 192 x 64, 4-stage ring of
-// 64-byte K tiles, chunk swizzle key (row >> 2) & 3 (conflict-free for the
-// 64-bank LDS, which serves a 16-byte read for 16 lanes per cycle), groups of
-// 4 tile rows. At M = 4608 the DiT FFN up-projection is 24 x 64 tiles: six
-// full rounds of the 256 CUs.
-#define W8A8_GEMM_CFG 192, 256, 64, 1, 4, 4, 2, 4
+// Default configurations.
+//  - K a multiple of 128 bytes (every DiT shape): warp-specialized, 4
+//    consumer waves and 4 producer waves, 3-slot ring of 128-byte K tiles
+//    (full 128-byte cache lines per row), swizzle key (row >> 1) & 7, groups
+//    of 4 tile rows; 256 x 128 tiles (tokens x channels, consumer waves of
+//    128 x 64) unless 192 x 128 tiles (waves of 96 x 64) fill the rounds of
+//    the 256 CUs better (at M = 4608: the N = 4096 projections, 3 full
+//    rounds instead of 2.25).
+//  - otherwise: every wave loads, 192 x 256 tiles, 4 waves of 192 x 64,
+//    4-slot ring of 64-byte K tiles (BK = 64 divides K), key (row >> 2) & 3.
+template <class Op, int EPI>
+hipError_t launch_default(const GemmArgs &a) {
+    if (a.Kb % 128 == 0) {
+        if (round_fill(a.M, a.N, 192, 128) > round_fill(a.M, a.N, 256, 128) + 1e-9)
+            return Specialized<Op, 192, 128, 128, 2, 2, 4, 3, 1, 4, EPI>::launch(a);
+        return Specialized<Op, 256, 128, 128, 2, 2, 4, 3, 1, 4, EPI>::launch(a);
+    }
+    return Uniform<Op, 192, 256, 64, 1, 4, 4, 2, 4, EPI>::launch(a);
+}
 
 }  // namespace
 
 hipError_t launch_gemm_i8(const int8_t *A, const int8_t *B, const float *xs, const float *ws,
                           const uint16_t *bias, int64_t M, int64_t N, int64_t K, uint16_t *Y,
                           int32_t *Y32, hipStream_t stream) {
-    if (Y32 != nullptr)
-        return launch<I8Op, W8A8_GEMM_CFG, kStoreI32>(A, B, nullptr, nullptr, nullptr, M, N, K,
-                                                      Y32, stream);
-    return launch<I8Op, W8A8_GEMM_CFG, kDequantBf16>(A, B, xs, ws, bias, M, N, K, Y, stream);
+    GemmArgs a{A, B, xs, ws, bias, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K),
+               Y32 != nullptr ? static_cast<void *>(Y32) : static_cast<void *>(Y), stream};
+    if (Y32 != nullptr) {
+        a.xs = nullptr;
+        a.ws = nullptr;
+        a.bias = nullptr;
+        return launch_default<I8Op, kStoreI32>(a);
+    }
+    return launch_default<I8Op, kDequantBf16>(a);
 }
 
 hipError_t launch_gemm_bf16(const uint16_t *A, const uint16_t *B, const uint16_t *bias,
                             int64_t M, int64_t N, int64_t K, uint16_t *Y, hipStream_t stream) {
-    return launch<Bf16Op, W8A8_GEMM_CFG, kBiasBf16>(
-        reinterpret_cast<const int8_t *>(A), reinterpret_cast<const int8_t *>(B), nullptr, nullptr,
-        bias, M, N, 2 * K, Y, stream);
+    GemmArgs a{reinterpret_cast<const int8_t *>(A),
+               reinterpret_cast<const int8_t *>(B),
+               nullptr,
+               nullptr,
+               bias,
+               static_cast<int>(M),
+               static_cast<int>(N),
+               static_cast<int>(2 * K),
+               Y,
+               stream};
+    return launch_default<Bf16Op, kBiasBf16>(a);
 }
 
 }  // namespace w8a8

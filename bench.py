@@ -232,28 +232,34 @@ def measure(layers, steps: int, warmup: int, dev, per_kernel: bool, warm_ms: flo
     return total_ms / steps, wall / steps * 1e3, quant_us, gemm_us
 
 
-def quant_isolated(lin: Linear, dev, reps: int = 50):
+def quant_isolated(lin: Linear, dev, reps: int = 60, rounds: int = 5):
     """Quant kernel alone, inputs rotating over buffers larger than the
-    256 MB Infinity Cache so that X is read from HBM."""
+    256 MB Infinity Cache so that X is read from HBM. Each round times `reps`
+    back-to-back launches between one pair of events; an event pair around
+    every launch would add several microseconds to a ~10 us kernel. Returns
+    the median, min and max per-launch time over the rounds."""
     M, K = lin.M, lin.lay.K
-    nbuf = max(2, int(np.ceil(600e6 / (2 * M * K))))
+    nbuf = max(3, int(np.ceil(700e6 / (3 * M * K))))
     xs = [lin.xs[i % len(lin.xs)].clone() for i in range(nbuf)]
     qs = [torch.empty(M, K, dtype=torch.int8, device=dev) for _ in range(nbuf)]
     sc = torch.empty(M, dtype=torch.float32, device=dev)
     for i in range(nbuf):
         ops.w8a8_quant_act(xs[i], lin.lay.inv_lambda, Xq=qs[i], x_scale=sc)
     torch.cuda.synchronize()
-    e = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-         for _ in range(reps)]
-    for r in range(reps):
-        i = r % nbuf
-        e[r][0].record()
-        ops.w8a8_quant_act(xs[i], lin.lay.inv_lambda, Xq=qs[i], x_scale=sc)
-        e[r][1].record()
-    torch.cuda.synchronize()
-    us = np.array([a.elapsed_time(b) * 1e3 for a, b in e])
+    per = []
+    for _ in range(rounds):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for r in range(reps):
+            i = r % nbuf
+            ops.w8a8_quant_act(xs[i], lin.lay.inv_lambda, Xq=qs[i], x_scale=sc)
+        b.record()
+        torch.cuda.synchronize()
+        per.append(a.elapsed_time(b) * 1e3 / reps)
     del xs, qs
-    return float(np.median(us)), float(np.percentile(us, 10)), float(np.percentile(us, 90))
+    per = np.array(per)
+    return float(np.median(per)), float(per.min()), float(per.max())
 
 
 def quant_bytes(M, K) -> int:
@@ -488,10 +494,10 @@ def main():
         if lin.lay.K in seen:
             continue
         seen.add(lin.lay.K)
-        med, p10, p90 = quant_isolated(lin, dev)
+        med, lo, hi = quant_isolated(lin, dev)
         by = quant_bytes(lin.M, lin.lay.K)
         kernels[f"w8a8_quant_act_{lin.M}x{lin.lay.K}_hbm"] = {
-            "us": round(med, 2), "us_p10": round(p10, 2), "us_p90": round(p90, 2),
+            "us": round(med, 2), "us_min": round(lo, 2), "us_max": round(hi, 2),
             "GB_s": round(by / med / 1e3, 1), "frac_hbm": round(by / med / 1e3 / PEAK_HBM_GBS, 4),
             "bytes": by}
 

@@ -5,13 +5,18 @@
 //   - calibration: per-channel absmax and the smoothing equation
 //     lambda_j = s_j^alpha / max_i |W_ij|^(1-alpha).
 //
-// Row quantization keeps a whole row in registers: a group of G wavefronts
-// owns one row, each lane loads CH chunks of 8 bf16 (one 16-byte load per
-// chunk, consecutive lanes on consecutive chunks, so each wave load is a
-// contiguous 1 KiB), multiplies by the smoothing vector, reduces the absmax
-// across the wave with lane shuffles (and across the G waves through LDS),
-// then writes 8 int8 codes per chunk (8-byte stores, contiguous per wave).
-// X is read from HBM exactly once and the codes written once.
+// Row quantization: a group of G wavefronts owns one row. Each lane owns CH
+// chunks of 8 columns (consecutive lanes on consecutive 16-byte chunks, so
+// every wave load is one contiguous 1 KiB) and keeps the matching 8 smoothing
+// multipliers of each chunk in registers for all the rows it visits. A group
+// walks RPW rows, loading the next row while it reduces and writes the
+// current one:
+//   absmax over the row (lane shuffles, then across the G waves in LDS),
+//   scale, then 8 codes per chunk as one 8-byte store.
+// The smoothed value float(x) * mul is recomputed for the coding pass rather
+// than held, which halves the registers a row needs; it is the same binary32
+// product both times. X is read exactly once and the codes written once,
+// both with nontemporal hints (streamed through the caches, not kept).
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -53,78 +58,129 @@ __device__ __forceinline__ void smooth8(const uint4 &x, const float4 &ma, const 
     v[7] = bf16_hi(x.w) * mb.w;
 }
 
-// Rows per block = RPB, G waves per row, CH chunks of 8 values per lane. The
-// smoothed values stay in registers between the absmax and the coding pass.
-template <int G, int CH>
-__global__ __launch_bounds__((G >= 4 ? G : 4) * 64) void smooth_quant_rows_kernel(
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint4 load_stream(const uint4 *p) {
+    const v4u v = __builtin_nontemporal_load(reinterpret_cast<const v4u *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ void store_stream(uint2 *p, uint32_t lo, uint32_t hi) {
+    const v2u v = {lo, hi};
+    __builtin_nontemporal_store(v, reinterpret_cast<v2u *>(p));
+}
+
+__device__ __forceinline__ float absmax8(const uint4 &x, const float4 &ma, const float4 &mb,
+                                         float a) {
+    float v[8];
+    smooth8(x, ma, mb, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) a = fmaxf(a, fabsf(v[e]));
+    return a;
+}
+
+// WPB waves per block hold WPB / G row groups. Every wave runs exactly RPW
+// iterations, so the LDS barrier is uniform; rows past R are masked. Group g
+// of the grid visits rows g, g + groups, g + 2 groups, ...
+template <int G, int CH, int RPW, int WPB>
+__global__ __launch_bounds__(WPB * 64) void smooth_quant_rows_kernel(
     const uint16_t *__restrict__ src, const float *__restrict__ mul, int64_t R,
     int64_t K, int8_t *__restrict__ out, float *__restrict__ scale) {
-    constexpr int RPB = G >= 4 ? 1 : 4 / G;
-    __shared__ float red[RPB][G];
+    constexpr int SLOTS = WPB / G;
+    static_assert(SLOTS * G == WPB, "G must divide WPB");
+    __shared__ float red[2][SLOTS][G];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int sub = wave / G;      // row slot in the block
-    const int gw = wave % G;       // wave index inside the row group
-    const int64_t row = static_cast<int64_t>(blockIdx.x) * RPB + sub;
-    const bool row_ok = row < R;
+    const int sub = wave / G;
+    const int gw = wave % G;
     const int64_t nchunk = K >> 3;
+    const int64_t group = static_cast<int64_t>(blockIdx.x) * SLOTS + sub;
+    const int64_t groups = static_cast<int64_t>(gridDim.x) * SLOTS;
 
-    float v[CH][8];
-    float amax = 0.0f;
-    const uint4 *srow = reinterpret_cast<const uint4 *>(src + (row_ok ? row : 0) * K);
+    int64_t col[CH];
+    bool live[CH];
+    float4 ma[CH], mb[CH];
     const float4 *m4 = reinterpret_cast<const float4 *>(mul);
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
-        const int64_t j = static_cast<int64_t>(c) * (G * 64) + gw * 64 + lane;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[c][e] = 0.0f;
-        if (row_ok && j < nchunk) smooth8(srow[j], m4[2 * j], m4[2 * j + 1], v[c]);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(v[c][e]));
+        col[c] = static_cast<int64_t>(c) * (G * 64) + gw * 64 + lane;
+        live[c] = col[c] < nchunk;
+        ma[c] = live[c] ? m4[2 * col[c]] : make_float4(0.f, 0.f, 0.f, 0.f);
+        mb[c] = live[c] ? m4[2 * col[c] + 1] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
-    amax = wave_max(amax);
-    if constexpr (G > 1) {
-        if (lane == 0) red[sub][gw] = amax;
-        __syncthreads();
-#pragma unroll
-        for (int i = 0; i < G; ++i) amax = fmaxf(amax, red[sub][i]);
-    }
-    if (!row_ok) return;
 
-    float s = 0.0f;
-    float r = 0.0f;
-    const bool nonzero = amax >= kTinyAbsmax;
-    if (nonzero) {
-        s = amax / 127.0f;
-        r = 127.0f / amax;
-    }
-    if (gw == 0 && lane == 0) scale[row] = s;
-    uint2 *orow = reinterpret_cast<uint2 *>(out + row * K);
+    uint4 x[CH];
+    {
+        const bool ok = group < R;
+        const uint4 *srow = reinterpret_cast<const uint4 *>(src + (ok ? group : 0) * K);
 #pragma unroll
-    for (int c = 0; c < CH; ++c) {
-        const int64_t j = static_cast<int64_t>(c) * (G * 64) + gw * 64 + lane;
-        if (j < nchunk) {
-            uint2 q = make_uint2(0u, 0u);
+        for (int c = 0; c < CH; ++c)
+            x[c] = (ok && live[c]) ? load_stream(srow + col[c]) : make_uint4(0u, 0u, 0u, 0u);
+    }
+    for (int it = 0; it < RPW; ++it) {
+        const int64_t row = group + it * groups;
+        uint4 xn[CH];
+        if (it + 1 < RPW) {
+            const int64_t nrow = row + groups;
+            const bool ok = nrow < R;
+            const uint4 *srow = reinterpret_cast<const uint4 *>(src + (ok ? nrow : 0) * K);
+#pragma unroll
+            for (int c = 0; c < CH; ++c)
+                xn[c] = (ok && live[c]) ? load_stream(srow + col[c]) : make_uint4(0u, 0u, 0u, 0u);
+        }
+        float amax = 0.0f;
+#pragma unroll
+        for (int c = 0; c < CH; ++c) amax = absmax8(x[c], ma[c], mb[c], amax);
+        amax = wave_max(amax);
+        if constexpr (G > 1) {
+            if (lane == 0) red[it & 1][sub][gw] = amax;
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < G; ++i) amax = fmaxf(amax, red[it & 1][sub][i]);
+        }
+        if (row < R) {
+            float sc = 0.0f;
+            float r = 0.0f;
+            const bool nonzero = amax >= kTinyAbsmax;
             if (nonzero) {
-                const float *t = v[c];
-                q.x = code(t[0], r) | code(t[1], r) << 8 | code(t[2], r) << 16 |
-                      code(t[3], r) << 24;
-                q.y = code(t[4], r) | code(t[5], r) << 8 | code(t[6], r) << 16 |
-                      code(t[7], r) << 24;
+                sc = amax / 127.0f;
+                r = 127.0f / amax;
             }
-            orow[j] = q;
+            if (gw == 0 && lane == 0) scale[row] = sc;
+            uint2 *orow = reinterpret_cast<uint2 *>(out + row * K);
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                if (!live[c]) continue;
+                uint32_t lo = 0u;
+                uint32_t hi = 0u;
+                if (nonzero) {
+                    float t[8];
+                    smooth8(x[c], ma[c], mb[c], t);
+                    lo = code(t[0], r) | code(t[1], r) << 8 | code(t[2], r) << 16 |
+                         code(t[3], r) << 24;
+                    hi = code(t[4], r) | code(t[5], r) << 8 | code(t[6], r) << 16 |
+                         code(t[7], r) << 24;
+                }
+                store_stream(orow + col[c], lo, hi);
+            }
+        }
+        if (it + 1 < RPW) {
+#pragma unroll
+            for (int c = 0; c < CH; ++c) x[c] = xn[c];
         }
     }
 }
 
-template <int G, int CH>
+template <int G, int CH, int RPW, int WPB>
 hipError_t launch_rows(const uint16_t *src, const float *mul, int64_t R, int64_t K,
                        int8_t *out, float *scale, hipStream_t stream) {
-    constexpr int RPB = G >= 4 ? 1 : 4 / G;
-    constexpr int threads = (G >= 4 ? G : 4) * 64;
-    const int64_t blocks = (R + RPB - 1) / RPB;
-    hipLaunchKernelGGL((smooth_quant_rows_kernel<G, CH>), dim3(static_cast<unsigned>(blocks)),
-                       dim3(threads), 0, stream, src, mul, R, K, out, scale);
+    constexpr int SLOTS = WPB / G;
+    const int64_t groups = (R + RPW - 1) / RPW;
+    const int64_t blocks = (groups + SLOTS - 1) / SLOTS;
+    hipLaunchKernelGGL((smooth_quant_rows_kernel<G, CH, RPW, WPB>),
+                       dim3(static_cast<unsigned>(blocks)), dim3(WPB * 64), 0, stream, src, mul,
+                       R, K, out, scale);
     return hipGetLastError();
 }
 
@@ -194,15 +250,18 @@ unsigned blocks_for(int64_t n, int threads) {
 hipError_t launch_smooth_quant_rows(const uint16_t *src, const float *mul, int64_t R,
                                     int64_t K, int8_t *out, float *scale,
                                     hipStream_t stream) {
-    // Row coverage is 512 * G * CH values; pick the smallest that holds K.
-    if (K <= 512) return launch_rows<1, 1>(src, mul, R, K, out, scale, stream);
-    if (K <= 1024) return launch_rows<1, 2>(src, mul, R, K, out, scale, stream);
-    if (K <= 2048) return launch_rows<1, 4>(src, mul, R, K, out, scale, stream);
-    if (K <= 4096) return launch_rows<1, 8>(src, mul, R, K, out, scale, stream);
-    if (K <= 8192) return launch_rows<2, 8>(src, mul, R, K, out, scale, stream);
-    if (K <= 16384) return launch_rows<4, 8>(src, mul, R, K, out, scale, stream);
-    if (K <= 32768) return launch_rows<8, 8>(src, mul, R, K, out, scale, stream);
-    return launch_rows<16, 8>(src, mul, R, K, out, scale, stream);  // K <= 65536
+    // A group covers 512 * G * CH columns; take the smallest that holds K.
+    // Up to K = 32768 a group has at most 8 waves and walks two rows (the
+    // second one prefetched); the K = 65536 group of 16 waves has no register
+    // room for a prefetched row and walks one.
+    if (K <= 512) return launch_rows<1, 1, 2, 4>(src, mul, R, K, out, scale, stream);
+    if (K <= 1024) return launch_rows<2, 1, 2, 4>(src, mul, R, K, out, scale, stream);
+    if (K <= 2048) return launch_rows<4, 1, 2, 4>(src, mul, R, K, out, scale, stream);
+    if (K <= 4096) return launch_rows<4, 2, 2, 4>(src, mul, R, K, out, scale, stream);
+    if (K <= 8192) return launch_rows<8, 2, 2, 8>(src, mul, R, K, out, scale, stream);
+    if (K <= 16384) return launch_rows<8, 4, 2, 8>(src, mul, R, K, out, scale, stream);
+    if (K <= 32768) return launch_rows<8, 8, 2, 8>(src, mul, R, K, out, scale, stream);
+    return launch_rows<16, 8, 1, 16>(src, mul, R, K, out, scale, stream);  // K <= 65536
 }
 
 hipError_t launch_reciprocal(const float *lam, int64_t K, float *inv, hipStream_t stream) {

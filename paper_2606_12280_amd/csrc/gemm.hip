@@ -91,6 +91,20 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, int8_t *lds, uint32_t off) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LDS_AS void *)lds, 16, off, 0, 0, 0);
 }
+// Instruction-group ordering for the scheduler (sched_group_barrier masks:
+// 0x008 MFMA, 0x100 LDS read, 0x020 global/buffer read). One MFMA, then one
+// LDS read while any remain, then one buffer load while any remain, repeated:
+// the fragment reads and tile loads of a K step are spread over its MFMAs.
+template <int I, int NM, int NR, int ND>
+__device__ __forceinline__ void interleave_from() {
+    if constexpr (I < NM) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if constexpr (I < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        if constexpr (I < ND) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        interleave_from<I + 1, NM, NR, ND>();
+    }
+}
+
 // A no-op that mentions an AGPR. A kernel limited to 256 registers per wave
 // that never names an AGPR gets its MFMAs in the VGPR form (accumulators in
 // VGPRs), which measured ~20% slower here than the AGPR form: the MFMA's
@@ -319,6 +333,75 @@ struct Epi {
             }
         }
     }
+
+    // The bf16 epilogues through LDS. The per-lane layout of the accumulators
+    // puts the 32 lanes of an 8-byte store on 32 different output rows (64
+    // cache lines per store instruction). Instead the wave writes its
+    // 32 TJ x 32 TI tile of bf16 into `stage` (its own region, rows padded
+    // by 16 bytes against bank conflicts), then stores whole rows: 16 bytes
+    // per lane, 8 lanes per 128-byte row, 8 rows per instruction. Nothing
+    // else uses `stage`, so no barrier is needed between the two passes.
+    static constexpr int kRowStride = 64 * TI + 16;
+    static constexpr int kStageBytes = 32 * TJ * kRowStride;
+
+    template <class Acc>
+    __device__ __forceinline__ void store_rows(const Acc (&acc)[TI][TJ], int8_t *stage,
+                                               void *Yout, int m0, int rows_x, int mbase,
+                                               int nbase, int N, int frow, int fhalf,
+                                               int lane) const {
+        static_assert(EPI != kStoreI32, "row stores are for the bf16 epilogues");
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+#pragma unroll
+            for (int i = 0; i < TI; ++i)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    uint32_t h[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float a = static_cast<float>(acc[i][j][4 * g + e]);
+                        const uint32_t bw = b_[i][g][e >> 1];
+                        const float b = __uint_as_float((e & 1) ? (bw & 0xffff0000u) : (bw << 16));
+                        float y;
+                        if constexpr (EPI == kDequantBf16)
+                            y = __builtin_fmaf(a, xs_[j] * ws_[i][g][e], b);
+                        else
+                            y = a + b;
+                        h[e] = f32_to_bf16_bits(y);
+                    }
+                    const int t = 32 * j + frow;
+                    const int c = 32 * i + 8 * g + 4 * fhalf;
+                    *reinterpret_cast<v2u *>(stage + t * kRowStride + c * 2) =
+                        v2u{h[0] | h[1] << 16, h[2] | h[3] << 16};
+                }
+        constexpr int CPR = 64 * TI / 16;  // 16-byte chunks per row
+        constexpr int ROUNDS = 32 * TJ * CPR / 64;
+        static_assert(32 * TJ * CPR % 64 == 0, "whole store rounds");
+        const __amdgpu_buffer_rsrc_t ry =
+            make_rsrc(static_cast<int8_t *>(Yout) + static_cast<int64_t>(m0) * N * 2,
+                      static_cast<uint32_t>(rows_x) * N * 2u);
+        const bool vec8 = (N & 7) == 0;
+#pragma unroll
+        for (int r = 0; r < ROUNDS; ++r) {
+            const int id = r * 64 + lane;
+            const int row = id / CPR;
+            const int c = id % CPR;
+            const v4i v = *reinterpret_cast<const v4i *>(stage + row * kRowStride + c * 16);
+            const int n = nbase + 8 * c;
+            const uint32_t base = static_cast<uint32_t>(mbase + row) * N;
+            if (vec8 && n + 8 <= N) {
+                __builtin_amdgcn_raw_buffer_store_b128(v, ry, (base + n) * 2u, 0, 0);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t off = n + e < N ? (base + n + e) * 2u : kOutOfRange;
+                    __builtin_amdgcn_raw_buffer_store_b16(
+                        static_cast<uint16_t>(static_cast<uint32_t>(v[e >> 1]) >> (16 * (e & 1))),
+                        ry, off, 0, 0);
+                }
+            }
+        }
+    }
 };
 
 // MFMA side of one wave: fragment reads from an LDS slot and the MFMAs of a
@@ -331,14 +414,15 @@ struct Mma {
     typename Op::Acc acc[TI][TJ];
     v4i wf[2][TI];
     v4i xf[2][TJ];
-    int x_base, w_base, fhalf, fkey;
+    int x_base, w_base, w_row, fhalf, fkey;
 
     __device__ __forceinline__ void init(int lane, int mbase, int nbase) {
         const int frow = lane & 31;
         fhalf = lane >> 5;
         fkey = (frow >> SWZ) & (CPR - 1);
         x_base = (mbase + frow) * BK;
-        w_base = BM * BK + (nbase + frow) * BK;
+        w_row = (nbase + frow) * BK;
+        w_base = BM * BK + w_row;
 #pragma unroll
         for (int i = 0; i < TI; ++i)
 #pragma unroll
@@ -352,6 +436,17 @@ struct Mma {
 #pragma unroll
         for (int j = 0; j < TJ; ++j)
             xf[buf][j] = *reinterpret_cast<const v4i *>(slot + x_base + j * 32 * BK + chunk * 16);
+    }
+    // The same from separate X and W slots.
+    __device__ __forceinline__ void load2(const int8_t *xslot, const int8_t *wslot, int s,
+                                          int buf) {
+        const int chunk = (2 * s + fhalf) ^ fkey;
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+            wf[buf][i] = *reinterpret_cast<const v4i *>(wslot + w_row + i * 32 * BK + chunk * 16);
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+            xf[buf][j] = *reinterpret_cast<const v4i *>(xslot + x_base + j * 32 * BK + chunk * 16);
     }
     __device__ __forceinline__ void step(int buf) {
 #pragma unroll
@@ -381,6 +476,32 @@ struct Mma {
             sched_fence();
         }
         step((KSTEPS - 1) & 1);
+        sched_fence();
+    }
+    // One K tile for gemm_2s_kernel, from separate X and W slots.
+    // `boundary()` comes before the last MFMA step (as in tile()); right after
+    // it the slots this tile came from are free, and LOADS loads of the tile
+    // after next (`issue(i)`) go out while the last MFMAs run.
+    template <bool LAST, int LOADS, class Boundary, class Issue>
+    __device__ __forceinline__ void tile_2s(const int8_t *xslot, const int8_t *wslot,
+                                            Boundary &&boundary, Issue &&issue) {
+        constexpr int KSTEPS = BK / 32;
+        static_assert(KSTEPS % 2 == 0, "fragment buffer 0 starts every tile");
+#pragma unroll
+        for (int s = 0; s + 1 < KSTEPS; ++s) {
+            load2(xslot, wslot, s + 1, (s + 1) & 1);
+            step(s & 1);
+            interleave_from<0, TI * TJ, TI + TJ, 0>();
+            sched_fence();
+        }
+        if constexpr (!LAST) {
+            boundary();
+#pragma unroll
+            for (int i = 0; i < LOADS; ++i) issue(i);
+            sched_fence();
+        }
+        step((KSTEPS - 1) & 1);
+        interleave_from<0, TI * TJ, LAST ? 0 : TI + TJ, LOADS>();
         sched_fence();
     }
 };
@@ -510,6 +631,135 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_kernel(
 }
 
 // --------------------------------------------------------------------------
+// gemm_2s_kernel: every wave loads and multiplies, two-slot rings. Made for
+// large tiles (192 x 256: 27% fewer bytes per MFMA than 256 x 128) whose
+// accumulators leave no registers for separate producer waves. One barrier
+// per K tile, placed before the tile's last MFMA step:
+//   barrier #kt+1: every wave has finished reading the slots of tile kt and
+//   its own loads of tile kt+1 have landed.
+// Right after it each wave issues its share of tile kt+2 into the slots
+// just freed, so a tile's loads have a whole K tile of MFMAs to land in.
+// The epilogue operands are staged in LDS by wave 0 before barrier #0; the
+// output rows go out through LDS (store_rows), staged in the ring.
+// --------------------------------------------------------------------------
+template <class Op, int BM, int BN, int WAVES_M, int WAVES_N, int SWZ, int GROUP_M, int EPI,
+          bool N_VEC, bool HAS_BIAS>
+__global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_2s_kernel(
+    const int8_t *__restrict__ X, const int8_t *__restrict__ W, const float *__restrict__ xs,
+    const float *__restrict__ ws, const uint16_t *__restrict__ bias, int M, int N, int Kb,
+    void *__restrict__ Yout, int tiles_m, int tiles_n) {
+    constexpr int BK = 128;
+    constexpr int NW = WAVES_M * WAVES_N;
+    constexpr int WTM = BM / WAVES_M;
+    constexpr int WTN = BN / WAVES_N;
+    constexpr int TJ = WTM / 32;
+    constexpr int TI = WTN / 32;
+    constexpr int NBX = BM * BK / 1024;
+    constexpr int NBW = BN * BK / 1024;
+    constexpr int LX = NBX / NW;  // 1 KiB DMA blocks per wave and K tile, X
+    constexpr int LW = NBW / NW;  // ... W
+    constexpr int XSLOT = BM * BK;
+    constexpr int WSLOT = BN * BK;
+    constexpr int RING = 2 * (XSLOT + WSLOT);
+    static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be whole 32x32 blocks");
+    static_assert(LX * NW == NBX && LW * NW == NBW, "DMA split");
+    static_assert(LX + LW < 64, "vmcnt range");
+
+    using EpiT = Epi<TI, TJ, EPI, N_VEC, HAS_BIAS>;
+    // The ring; after the last K tile the same bytes stage the waves' output
+    // rows. Then the epilogue operands.
+    constexpr int BODY = RING > NW * EpiT::kStageBytes ? RING : NW * EpiT::kStageBytes;
+    static_assert(BODY + 4 * BM + 6 * BN <= 160 * 1024, "LDS");
+
+    __shared__ __attribute__((aligned(1024))) int8_t smem[BODY + 4 * BM + 6 * BN];
+    int8_t *xring = smem;
+    int8_t *wring = smem + 2 * XSLOT;
+    float *ep_xs = reinterpret_cast<float *>(smem + BODY);
+    float *ep_ws = ep_xs + BM;
+    uint16_t *ep_b = reinterpret_cast<uint16_t *>(ep_ws + BN);
+    keep_args(xs, ws, bias, Yout);
+
+    int tm, tn;
+    map_tile<GROUP_M>(blockIdx.x, tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * BM;
+    const int n0 = tn * BN;
+    const int lane = threadIdx.x & 63;
+    const int wave = wave_id();
+    const int mbase = (wave / WAVES_N) * WTM;
+    const int nbase = (wave % WAVES_N) * WTN;
+    const int rows_x = min(BM, M - m0);
+    const int rows_w = min(BN, N - n0);
+    const int KT = Kb / BK;  // the launcher guarantees BK divides Kb
+
+    const __amdgpu_buffer_rsrc_t rx =
+        make_rsrc(X + static_cast<int64_t>(m0) * Kb, static_cast<uint32_t>(rows_x) * Kb);
+    const __amdgpu_buffer_rsrc_t rw =
+        make_rsrc(W + static_cast<int64_t>(n0) * Kb, static_cast<uint32_t>(rows_w) * Kb);
+    uint32_t off_x[LX], off_w[LW];
+#pragma unroll
+    for (int i = 0; i < LX; ++i) off_x[i] = dma_offset<BK, SWZ>(wave + i * NW, lane, Kb);
+#pragma unroll
+    for (int i = 0; i < LW; ++i) off_w[i] = dma_offset<BK, SWZ>(wave + i * NW, lane, Kb);
+    auto xslot = [&](int kt) { return xring + (kt & 1) * XSLOT; };
+    auto wslot = [&](int kt) { return wring + (kt & 1) * WSLOT; };
+    // Load i of this wave's share of tile kt: W blocks first, then X blocks.
+    auto issue_one = [&](int kt, int i) {
+        if (i < LW)
+            dma16(rw, wslot(kt) + (wave + i * NW) * 1024, off_w[i] + kt * BK);
+        else
+            dma16(rx, xslot(kt) + (wave + (i - LW) * NW) * 1024, off_x[i - LW] + kt * BK);
+    };
+
+    Mma<Op, BM, BK, TI, TJ, SWZ> mma;
+    prefer_agpr_mfma();
+    mma.init(lane, mbase, nbase);
+
+#pragma unroll
+    for (int i = 0; i < LW + LX; ++i) issue_one(0, i);
+    if (EPI != kStoreI32 && wave == 0)
+        EpiT::template fill_lds<BM, BN>(ep_xs, ep_ws, ep_b, xs, ws, bias, m0, rows_x, n0,
+                                        rows_w, lane);
+    wait_vmcnt<0>();
+    wait_lgkmcnt0();
+    barrier();  // #0
+    if (KT > 1) {
+#pragma unroll
+        for (int i = 0; i < LW + LX; ++i) issue_one(1, i);
+    }
+    mma.load2(xslot(0), wslot(0), 0, 0);
+
+    // Tile kt's loads went out at barrier #kt-1 (tiles 0 and 1 in the
+    // prologue). Branch-free loops keep the compiler's own waits exact.
+    auto boundary = [&](int kt) {
+        wait_lgkmcnt0();  // this wave's reads of tile kt's slots are done
+        wait_vmcnt<0>();  // and its loads of tile kt+1 have landed
+        barrier();        // #kt+1
+        mma.load2(xslot(kt + 1), wslot(kt + 1), 0, 0);
+    };
+    int kt = 0;
+    for (; kt + 2 < KT; ++kt)
+        mma.template tile_2s<false, LW + LX>(xslot(kt), wslot(kt), [&] { boundary(kt); },
+                                             [&](int i) { issue_one(kt + 2, i); });
+    if (kt + 1 < KT) {
+        mma.template tile_2s<false, 0>(xslot(kt), wslot(kt), [&] { boundary(kt); },
+                                       [](int) {});
+        ++kt;
+    }
+    mma.template tile_2s<true, 0>(xslot(kt), wslot(kt), [] {}, [](int) {});
+
+    EpiT epi;
+    if constexpr (EPI == kStoreI32) {
+        epi.store(mma.acc, Yout, m0, rows_x, mbase, n0 + nbase, N, lane & 31, lane >> 5);
+    } else {
+        epi.load_lds(ep_xs, ep_ws, ep_b, mbase, nbase, lane & 31, lane >> 5);
+        wait_lgkmcnt0();
+        barrier();  // every wave is done with the ring
+        epi.store_rows(mma.acc, smem + wave * EpiT::kStageBytes, Yout, m0, rows_x, mbase,
+                       n0 + nbase, N, lane & 31, lane >> 5, lane);
+    }
+}
+
+// --------------------------------------------------------------------------
 // gemm_ws_kernel: NPROD producer waves issue the tile loads, WAVES_M x
 // WAVES_N consumer waves multiply. One barrier per K tile hands slots over:
 //   barrier #0: tile 0 has landed;
@@ -626,11 +876,17 @@ __global__ __launch_bounds__((WAVES_M * WAVES_N + NPROD) * 64) void gemm_ws_kern
             mma.load(smem + ((kt + 1) % STAGES) * STAGE, 0, 0);
         });
     mma.template tile<true>(smem + (kt % STAGES) * STAGE, [] {});
-    barrier();  // final: the epilogue operands are in LDS
+    barrier();  // final: the epilogue operands are in LDS and the ring is free
 
     EpiT epi;
-    if (EPI != kStoreI32) epi.load_lds(ep_xs, ep_ws, ep_b, mbase, nbase, lane & 31, lane >> 5);
-    epi.store(mma.acc, Yout, m0, rows_x, mbase, n0 + nbase, N, lane & 31, lane >> 5);
+    if constexpr (EPI == kStoreI32) {
+        epi.store(mma.acc, Yout, m0, rows_x, mbase, n0 + nbase, N, lane & 31, lane >> 5);
+    } else {
+        static_assert(NC * EpiT::kStageBytes <= STAGES * STAGE, "row staging fits the ring");
+        epi.load_lds(ep_xs, ep_ws, ep_b, mbase, nbase, lane & 31, lane >> 5);
+        epi.store_rows(mma.acc, smem + wave * EpiT::kStageBytes, Yout, m0, rows_x, mbase,
+                       n0 + nbase, N, lane & 31, lane >> 5, lane);
+    }
 }
 
 // --------------------------------------------------------------------------
@@ -704,6 +960,21 @@ struct Specialized {
     }
 };
 
+template <class Op, int BM, int BN, int WAVES_M, int WAVES_N, int SWZ, int GROUP_M, int EPI>
+struct TwoSlot {
+    template <bool NV, bool HB>
+    struct K {
+        static const void *fn() {
+            return reinterpret_cast<const void *>(
+                &gemm_2s_kernel<Op, BM, BN, WAVES_M, WAVES_N, SWZ, GROUP_M, EPI, NV, HB>);
+        }
+    };
+    static hipError_t launch(const GemmArgs &a) {
+        if (a.Kb % 128 != 0) return hipErrorInvalidValue;
+        return dispatch<K>(a, EPI == kStoreI32, BM, BN, WAVES_M * WAVES_N * 64);
+    }
+};
+
 // Fraction of the slots of ceil(tiles / 256) full rounds of the 256 CUs
 // (one workgroup per CU) that the tiles of an M x N output fill.
 double round_fill(int M, int N, int BM, int BN) {
@@ -712,19 +983,23 @@ double round_fill(int M, int N, int BM, int BN) {
     return static_cast<double>(tiles) / static_cast<double>(rounds * 256);
 }
 
-// Default configurations.
-//  - K a multiple of 128 bytes (every DiT shape): warp-specialized, 4
-//    consumer waves and 4 producer waves, 3-slot ring of 128-byte K tiles
-//    (full 128-byte cache lines per row), swizzle key (row >> 1) & 7, groups
-//    of 4 tile rows; 256 x 128 tiles (tokens x channels, consumer waves of
-//    128 x 64) unless 192 x 128 tiles (waves of 96 x 64) fill the rounds of
-//    the 256 CUs better (at M = 4608: the N = 4096 projections, 3 full
-//    rounds instead of 2.25).
+// Default configurations (measured on the DiT shapes, M = 4608).
+//  - K a multiple of 128 bytes (every DiT shape):
+//    * 192 x 256 tiles (tokens x channels), every wave loading and
+//      multiplying, when their tiles fill the rounds of the 256 CUs to at
+//      least 85% (N = 16384: 6 full rounds; N = 12288: 4.5);
+//    * otherwise warp-specialized, 4 consumer and 4 producer waves, 3-slot
+//      ring; 192 x 128 tiles (waves of 96 x 64) or 256 x 128 (128 x 64),
+//      whichever fills the rounds better (N = 4096: 192 x 128, 3 full rounds).
+//    All use 128-byte K tiles (full cache lines per row) and the swizzle key
+//    (row >> 1) & 7, groups of 4 tile rows.
 //  - otherwise: every wave loads, 192 x 256 tiles, 4 waves of 192 x 64,
 //    4-slot ring of 64-byte K tiles (BK = 64 divides K), key (row >> 2) & 3.
 template <class Op, int EPI>
 hipError_t launch_default(const GemmArgs &a) {
     if (a.Kb % 128 == 0) {
+        if (round_fill(a.M, a.N, 192, 256) >= 0.85)
+            return TwoSlot<Op, 192, 256, 2, 4, 1, 4, EPI>::launch(a);
         if (round_fill(a.M, a.N, 192, 128) > round_fill(a.M, a.N, 256, 128) + 1e-9)
             return Specialized<Op, 192, 128, 128, 2, 2, 4, 3, 1, 4, EPI>::launch(a);
         return Specialized<Op, 256, 128, 128, 2, 2, 4, 3, 1, 4, EPI>::launch(a);

@@ -126,6 +126,38 @@ def test_gemm_i32_bit_exact(M, N, K):
     assert np.array_equal(C, ref)
 
 
+# Shapes large enough to select the 192 x 256 tiles (at least 85% of the
+# 256 CUs' rounds filled), with ragged M and N (N odd: element stores at the
+# edge) and 1, 2, 3 and 5 K tiles of 128 bytes.
+LARGE_RAGGED = [(4571, 16376, 128), (4600, 16375, 256), (4545, 12290, 384),
+                (4608, 16384, 640)]
+
+
+@pytest.mark.parametrize("M,N,K", LARGE_RAGGED)
+def test_gemm_i32_large_ragged(M, N, K):
+    A = synth.rand_i8([109, M, K], (M, K))
+    B = synth.rand_i8([110, N, K], (N, K))
+    ref = oracle.gemm_i32(A, B, M, N, K)
+    C = host(ops.w8a8_gemm_i32(dev(A), dev(B)))
+    assert np.array_equal(C, ref)
+
+
+@pytest.mark.parametrize("M,N,K", LARGE_RAGGED)
+@pytest.mark.parametrize("with_bias", [True, False])
+def test_w8a8_linear_large_ragged(M, N, K, with_bias):
+    """The dequantizing epilogue (rows staged through LDS) on whole outputs."""
+    A = synth.rand_i8([111, M, K], (M, K))
+    B = synth.rand_i8([112, N, K], (N, K))
+    rng = np.random.default_rng([113, M, N, K])
+    xs = rng.uniform(1e-3, 1e-1, M).astype(np.float32)
+    ws = rng.uniform(1e-4, 1e-2, N).astype(np.float32)
+    b = synth.rand_bf16([114, N], (N,), 0.5) if with_bias else np.zeros(N, np.uint16)
+    acc = oracle.gemm_i32(A, B, M, N, K)
+    Yref = oracle.epilogue(acc, xs, ws, b, M, N)
+    Y = ops.w8a8_linear(dev(A), dev(xs), dev(B), dev(ws), dev_bf16(b) if with_bias else None)
+    check_w8a8_output(host_bits(Y), Yref, acc, xs, ws, b)
+
+
 def test_gemm_i32_extremes():
     """All +-127 codes at K = 16384: |acc| = 127^2 K, the largest sum."""
     M, N, K = 64, 96, 16384
@@ -221,7 +253,8 @@ def test_bf16_linear_small_integers_exact(M, N, K):
     assert np.array_equal(Y, oracle.bf16_linear(X, W, b, M, N, K))
 
 
-@pytest.mark.parametrize("M,N,K", [(64, 512, 256), (300, 520, 1088), (65, 128, 16384)])
+@pytest.mark.parametrize("M,N,K", [(64, 512, 256), (300, 520, 1088), (65, 128, 16384),
+                                   (4571, 16376, 192)])
 def test_bf16_linear_random(M, N, K):
     c = synth.linear_case([114, M, N, K], M, N, K, act="gelu")
     Y = host_bits(ops.bf16_linear(dev_bf16(c["X"]), dev_bf16(c["W"]), dev_bf16(c["bias"])))

@@ -414,15 +414,14 @@ struct Mma {
     typename Op::Acc acc[TI][TJ];
     v4i wf[2][TI];
     v4i xf[2][TJ];
-    int x_base, w_base, w_row, fhalf, fkey;
+    int x_base, w_base, fhalf, fkey;
 
     __device__ __forceinline__ void init(int lane, int mbase, int nbase) {
         const int frow = lane & 31;
         fhalf = lane >> 5;
         fkey = (frow >> SWZ) & (CPR - 1);
         x_base = (mbase + frow) * BK;
-        w_row = (nbase + frow) * BK;
-        w_base = BM * BK + w_row;
+        w_base = BM * BK + (nbase + frow) * BK;
 #pragma unroll
         for (int i = 0; i < TI; ++i)
 #pragma unroll
@@ -436,17 +435,6 @@ struct Mma {
 #pragma unroll
         for (int j = 0; j < TJ; ++j)
             xf[buf][j] = *reinterpret_cast<const v4i *>(slot + x_base + j * 32 * BK + chunk * 16);
-    }
-    // The same from separate X and W slots.
-    __device__ __forceinline__ void load2(const int8_t *xslot, const int8_t *wslot, int s,
-                                          int buf) {
-        const int chunk = (2 * s + fhalf) ^ fkey;
-#pragma unroll
-        for (int i = 0; i < TI; ++i)
-            wf[buf][i] = *reinterpret_cast<const v4i *>(wslot + w_row + i * 32 * BK + chunk * 16);
-#pragma unroll
-        for (int j = 0; j < TJ; ++j)
-            xf[buf][j] = *reinterpret_cast<const v4i *>(xslot + x_base + j * 32 * BK + chunk * 16);
     }
     __device__ __forceinline__ void step(int buf) {
 #pragma unroll
@@ -478,30 +466,81 @@ struct Mma {
         step((KSTEPS - 1) & 1);
         sched_fence();
     }
-    // One K tile for gemm_2s_kernel, from separate X and W slots.
-    // `boundary()` comes before the last MFMA step (as in tile()); right after
-    // it the slots this tile came from are free, and LOADS loads of the tile
-    // after next (`issue(i)`) go out while the last MFMAs run.
-    template <bool LAST, int LOADS, class Boundary, class Issue>
-    __device__ __forceinline__ void tile_2s(const int8_t *xslot, const int8_t *wslot,
-                                            Boundary &&boundary, Issue &&issue) {
-        constexpr int KSTEPS = BK / 32;
-        static_assert(KSTEPS % 2 == 0, "fragment buffer 0 starts every tile");
+};
+
+// MFMA side of one wave of gemm_2s_kernel: like Mma, with separate X and W
+// slots and fragments read two MFMA steps ahead, one register buffer per
+// step of the 4-step (128-byte) K tile. A wave running alone on its SIMD
+// (the other one waiting at the barrier) then still has two steps of MFMAs
+// to cover each LDS read.
+template <class Op, int BK, int TI, int TJ, int SWZ>
+struct Mma2 {
+    static constexpr int CPR = BK / 16;
+    static constexpr int KSTEPS = BK / 32;
+    static_assert(KSTEPS == 4, "four MFMA steps per K tile");
+    typename Op::Acc acc[TI][TJ];
+    v4i wf[KSTEPS][TI];
+    v4i xf[KSTEPS][TJ];
+    int x_row, w_row, fhalf, fkey;
+
+    __device__ __forceinline__ void init(int lane, int mbase, int nbase) {
+        const int frow = lane & 31;
+        fhalf = lane >> 5;
+        fkey = (frow >> SWZ) & (CPR - 1);
+        x_row = (mbase + frow) * BK;
+        w_row = (nbase + frow) * BK;
 #pragma unroll
-        for (int s = 0; s + 1 < KSTEPS; ++s) {
-            load2(xslot, wslot, s + 1, (s + 1) & 1);
-            step(s & 1);
-            interleave_from<0, TI * TJ, TI + TJ, 0>();
-            sched_fence();
-        }
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+            for (int j = 0; j < TJ; ++j) acc[i][j] = typename Op::Acc{};
+    }
+    // Fragments of MFMA step s (0..3) of a K tile into buffer s.
+    template <int S>
+    __device__ __forceinline__ void load(const int8_t *xslot, const int8_t *wslot) {
+        const int chunk = (2 * S + fhalf) ^ fkey;
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+            wf[S][i] = *reinterpret_cast<const v4i *>(wslot + w_row + i * 32 * BK + chunk * 16);
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+            xf[S][j] = *reinterpret_cast<const v4i *>(xslot + x_row + j * 32 * BK + chunk * 16);
+    }
+    template <int S>
+    __device__ __forceinline__ void step() {
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+            for (int j = 0; j < TJ; ++j) acc[i][j] = Op::mma(wf[S][i], xf[S][j], acc[i][j]);
+    }
+    // One K tile. On entry buffers 0 and 1 hold its steps 0 and 1. Steps 0
+    // and 1 read steps 2 and 3; then `boundary()`; then, unless LAST, steps
+    // 2 and 3 read steps 0 and 1 of the next tile from (nxslot, nwslot), and
+    // LOADS loads (`issue(i)`) go out during step 2.
+    template <bool LAST, int LOADS, class Boundary, class Issue>
+    __device__ __forceinline__ void tile(const int8_t *xslot, const int8_t *wslot,
+                                         const int8_t *nxslot, const int8_t *nwslot,
+                                         Boundary &&boundary, Issue &&issue) {
+        load<2>(xslot, wslot);
+        step<0>();
+        interleave_from<0, TI * TJ, TI + TJ, 0>();
+        sched_fence();
+        load<3>(xslot, wslot);
+        step<1>();
+        interleave_from<0, TI * TJ, TI + TJ, 0>();
+        sched_fence();
         if constexpr (!LAST) {
             boundary();
+            sched_fence();
 #pragma unroll
             for (int i = 0; i < LOADS; ++i) issue(i);
-            sched_fence();
+            load<0>(nxslot, nwslot);
         }
-        step((KSTEPS - 1) & 1);
+        step<2>();
         interleave_from<0, TI * TJ, LAST ? 0 : TI + TJ, LOADS>();
+        sched_fence();
+        if constexpr (!LAST) load<1>(nxslot, nwslot);
+        step<3>();
+        interleave_from<0, TI * TJ, LAST ? 0 : TI + TJ, 0>();
         sched_fence();
     }
 };
@@ -634,11 +673,12 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_kernel(
 // gemm_2s_kernel: every wave loads and multiplies, two-slot rings. Made for
 // large tiles (192 x 256: 27% fewer bytes per MFMA than 256 x 128) whose
 // accumulators leave no registers for separate producer waves. One barrier
-// per K tile, placed before the tile's last MFMA step:
+// per K tile, placed before the tile's third MFMA step (fragments are read
+// two steps ahead, so by then every read of the tile has been issued):
 //   barrier #kt+1: every wave has finished reading the slots of tile kt and
 //   its own loads of tile kt+1 have landed.
 // Right after it each wave issues its share of tile kt+2 into the slots
-// just freed, so a tile's loads have a whole K tile of MFMAs to land in.
+// just freed, so a tile's loads have most of a K tile of MFMAs to land in.
 // The epilogue operands are staged in LDS by wave 0 before barrier #0; the
 // output rows go out through LDS (store_rows), staged in the ring.
 // --------------------------------------------------------------------------
@@ -656,13 +696,18 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_2s_kernel(
     constexpr int TI = WTN / 32;
     constexpr int NBX = BM * BK / 1024;
     constexpr int NBW = BN * BK / 1024;
-    constexpr int LX = NBX / NW;  // 1 KiB DMA blocks per wave and K tile, X
-    constexpr int LW = NBW / NW;  // ... W
+    // Waves 0..NI-1 load; a workgroup's waves go round-robin to the 4 SIMDs,
+    // so each SIMD has one loading wave and one that only multiplies (whose
+    // MFMAs keep going while a load instruction waits to issue).
+    constexpr int NI = NW / 2;
+    static_assert(NI == 4, "one loading wave per SIMD");
+    constexpr int LX = NBX / NI;  // 1 KiB DMA blocks per loading wave and K tile, X
+    constexpr int LW = NBW / NI;  // ... W
     constexpr int XSLOT = BM * BK;
     constexpr int WSLOT = BN * BK;
     constexpr int RING = 2 * (XSLOT + WSLOT);
     static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be whole 32x32 blocks");
-    static_assert(LX * NW == NBX && LW * NW == NBW, "DMA split");
+    static_assert(LX * NI == NBX && LW * NI == NBW, "DMA split");
     static_assert(LX + LW < 64, "vmcnt range");
 
     using EpiT = Epi<TI, TJ, EPI, N_VEC, HAS_BIAS>;
@@ -695,22 +740,25 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_2s_kernel(
         make_rsrc(X + static_cast<int64_t>(m0) * Kb, static_cast<uint32_t>(rows_x) * Kb);
     const __amdgpu_buffer_rsrc_t rw =
         make_rsrc(W + static_cast<int64_t>(n0) * Kb, static_cast<uint32_t>(rows_w) * Kb);
+    const bool loader = wave < NI;
+    const int iw = loader ? wave : 0;  // index among the loading waves
     uint32_t off_x[LX], off_w[LW];
 #pragma unroll
-    for (int i = 0; i < LX; ++i) off_x[i] = dma_offset<BK, SWZ>(wave + i * NW, lane, Kb);
+    for (int i = 0; i < LX; ++i) off_x[i] = dma_offset<BK, SWZ>(iw + i * NI, lane, Kb);
 #pragma unroll
-    for (int i = 0; i < LW; ++i) off_w[i] = dma_offset<BK, SWZ>(wave + i * NW, lane, Kb);
+    for (int i = 0; i < LW; ++i) off_w[i] = dma_offset<BK, SWZ>(iw + i * NI, lane, Kb);
     auto xslot = [&](int kt) { return xring + (kt & 1) * XSLOT; };
     auto wslot = [&](int kt) { return wring + (kt & 1) * WSLOT; };
     // Load i of this wave's share of tile kt: W blocks first, then X blocks.
     auto issue_one = [&](int kt, int i) {
+        if (!loader) return;
         if (i < LW)
-            dma16(rw, wslot(kt) + (wave + i * NW) * 1024, off_w[i] + kt * BK);
+            dma16(rw, wslot(kt) + (iw + i * NI) * 1024, off_w[i] + kt * BK);
         else
-            dma16(rx, xslot(kt) + (wave + (i - LW) * NW) * 1024, off_x[i - LW] + kt * BK);
+            dma16(rx, xslot(kt) + (iw + (i - LW) * NI) * 1024, off_x[i - LW] + kt * BK);
     };
 
-    Mma<Op, BM, BK, TI, TJ, SWZ> mma;
+    Mma2<Op, BK, TI, TJ, SWZ> mma;
     prefer_agpr_mfma();
     mma.init(lane, mbase, nbase);
 
@@ -726,26 +774,27 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_2s_kernel(
 #pragma unroll
         for (int i = 0; i < LW + LX; ++i) issue_one(1, i);
     }
-    mma.load2(xslot(0), wslot(0), 0, 0);
+    mma.template load<0>(xslot(0), wslot(0));
+    mma.template load<1>(xslot(0), wslot(0));
 
     // Tile kt's loads went out at barrier #kt-1 (tiles 0 and 1 in the
     // prologue). Branch-free loops keep the compiler's own waits exact.
-    auto boundary = [&](int kt) {
+    auto boundary = [&] {
         wait_lgkmcnt0();  // this wave's reads of tile kt's slots are done
         wait_vmcnt<0>();  // and its loads of tile kt+1 have landed
         barrier();        // #kt+1
-        mma.load2(xslot(kt + 1), wslot(kt + 1), 0, 0);
     };
     int kt = 0;
+    auto issue_kt2 = [&](int i) { issue_one(kt + 2, i); };
     for (; kt + 2 < KT; ++kt)
-        mma.template tile_2s<false, LW + LX>(xslot(kt), wslot(kt), [&] { boundary(kt); },
-                                             [&](int i) { issue_one(kt + 2, i); });
+        mma.template tile<false, LW + LX>(xslot(kt), wslot(kt), xslot(kt + 1), wslot(kt + 1),
+                                          boundary, issue_kt2);
     if (kt + 1 < KT) {
-        mma.template tile_2s<false, 0>(xslot(kt), wslot(kt), [&] { boundary(kt); },
-                                       [](int) {});
+        mma.template tile<false, 0>(xslot(kt), wslot(kt), xslot(kt + 1), wslot(kt + 1),
+                                    boundary, [](int) {});
         ++kt;
     }
-    mma.template tile_2s<true, 0>(xslot(kt), wslot(kt), [] {}, [](int) {});
+    mma.template tile<true, 0>(xslot(kt), wslot(kt), xslot(kt), wslot(kt), [] {}, [](int) {});
 
     EpiT epi;
     if constexpr (EPI == kStoreI32) {

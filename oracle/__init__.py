@@ -68,6 +68,7 @@ def _load():
         "oracle_epilogue": ([P, P, P, P, I64, I64, P], None),
         "oracle_w8a8_linear": ([P, P, P, P, P, I64, I64, I64, P], None),
         "oracle_bf16_linear": ([P, P, P, I64, I64, I64, P], None),
+        "oracle_act_moments": ([P, I64, I64, P], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -198,3 +199,62 @@ def recipe(X, W, bias, M: int, N: int, K: int, alpha: float = 0.5, lam=None):
     Y = epilogue(acc, xs, ws, bias, M, N)
     return {"lambda": lam, "inv_lambda": il, "Wq": Wq, "w_scale": ws,
             "Xq": Xq, "x_scale": xs, "acc": acc, "Y": Y}
+
+
+# --------------------------------------------------------------------------
+# fragility profile and protection (Section 3, "Activation-fragility
+# profiling and protection")
+# --------------------------------------------------------------------------
+
+def act_moments(X, M: int, K: int) -> np.ndarray:
+    """[max |x|, mean, population std, Pearson kurtosis] of the M*K bf16
+    entries of X, binary64, two passes (kurtosis 0 for a constant input)."""
+    X = _c(X, np.uint16)
+    out = np.zeros(4, np.float64)
+    rc = _load().oracle_act_moments(_p(X), M, K, _p(out))
+    if rc != 0:
+        raise MemoryError("oracle_act_moments")
+    return out
+
+
+def fragility_scores(kurtosis) -> np.ndarray:
+    """A layer's fragility score: its activation kurtosis averaged over the
+    profiled denoising steps. kurtosis is [layers][steps]."""
+    k = np.asarray(kurtosis, np.float64)
+    return k.sum(axis=1) / k.shape[1]
+
+
+def top_n(scores, n: int) -> list[int]:
+    """Indices of the n most fragile layers: largest score first, equal
+    scores by lower layer index."""
+    s = [float(v) for v in scores]
+    order = sorted(range(len(s)), key=lambda i: (-s[i], i))
+    return order[:n]
+
+
+def _ranks(v) -> list[float]:
+    """1-based ranks, equal values sharing the mean of their positions."""
+    v = [float(x) for x in v]
+    order = sorted(range(len(v)), key=lambda i: v[i])
+    r = [0.0] * len(v)
+    i = 0
+    while i < len(order):
+        j = i
+        while j + 1 < len(order) and v[order[j + 1]] == v[order[i]]:
+            j += 1
+        for q in range(i, j + 1):
+            r[order[q]] = (i + j) / 2.0 + 1.0
+        i = j + 1
+    return r
+
+
+def spearman(a, b) -> float:
+    """Spearman rank correlation: the Pearson correlation of the ranks (the
+    paper's check that the ranking is stable between early and late steps)."""
+    ra, rb = _ranks(a), _ranks(b)
+    n = len(ra)
+    ma, mb = sum(ra) / n, sum(rb) / n
+    cov = sum((x - ma) * (y - mb) for x, y in zip(ra, rb))
+    va = sum((x - ma) ** 2 for x in ra)
+    vb = sum((y - mb) ** 2 for y in rb)
+    return cov / (va * vb) ** 0.5

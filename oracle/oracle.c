@@ -34,7 +34,10 @@
  *   - the epilogue and the protected linear are computed in binary64 and
  *     rounded once to bf16 (round to nearest even);
  *   - lambda itself is computed in binary64 and rounded once to binary32; a
- *     channel whose activation or weight statistic is zero keeps lambda = 1.
+ *     channel whose activation or weight statistic is zero keeps lambda = 1;
+ *   - the fragility profile of a layer's input is max |x|, the population
+ *     standard deviation and the Pearson kurtosis m4 / m2^2 over all its
+ *     entries, in binary64; a constant input has kurtosis 0.
  *
  * Parallelism: rows are independent and each row is computed by one thread in
  * a fixed order, so results do not depend on the thread count.
@@ -44,6 +47,7 @@
 #include <float.h>
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 #ifdef _OPENMP
 #include <omp.h>
@@ -298,4 +302,75 @@ void oracle_bf16_linear(const uint16_t *X, const uint16_t *W,
                 acc += (double)bf16_to_float(bias[n]);
             Y[t * N + n] = double_to_bf16(acc);
         }
+}
+
+/* ------------------------------------------------------------------ */
+/* Fragility profile (Section 3, "Activation-fragility profiling and    */
+/* protection"): per layer and denoising step, max |x|, standard        */
+/* deviation and kurtosis of the linear's input activations.            */
+/* ------------------------------------------------------------------ */
+
+/* X is [M][K] bf16, n = M*K entries, mean = (1/n) sum x and
+ * m_j = (1/n) sum (x - mean)^j. out[0] = max |x|, out[1] = mean,
+ * out[2] = sqrt(m2) (population standard deviation), out[3] = m4 / m2^2
+ * (Pearson kurtosis: 3 for a Gaussian), 0 when m2 = 0. Two passes in
+ * binary64: the mean first, then the central sums. Each row's sums are
+ * formed by one thread in k order and added in row order, so the result does
+ * not depend on the thread count. Returns 0, or -1 if out of memory. */
+int oracle_act_moments(const uint16_t *X, int64_t M, int64_t K, double *out)
+{
+    double *r1 = (double *)malloc((size_t)(M > 0 ? M : 1) * sizeof(double));
+    double *r2 = (double *)malloc((size_t)(M > 0 ? M : 1) * sizeof(double));
+    double *r4 = (double *)malloc((size_t)(M > 0 ? M : 1) * sizeof(double));
+    float *rmax = (float *)malloc((size_t)(M > 0 ? M : 1) * sizeof(float));
+    int64_t t, k;
+    double n = (double)M * (double)K, s1 = 0.0, s2 = 0.0, s4 = 0.0, mean, m2, m4;
+    float amax = 0.0f;
+    if (!r1 || !r2 || !r4 || !rmax) {
+        free(r1); free(r2); free(r4); free(rmax);
+        return -1;
+    }
+#pragma omp parallel for schedule(static) private(k)
+    for (t = 0; t < M; ++t) {
+        double a = 0.0;
+        float m = 0.0f;
+        for (k = 0; k < K; ++k) {
+            float x = bf16_to_float(X[t * K + k]);
+            a += (double)x;
+            if (fabsf(x) > m)
+                m = fabsf(x);
+        }
+        r1[t] = a;
+        rmax[t] = m;
+    }
+    for (t = 0; t < M; ++t) {
+        s1 += r1[t];
+        if (rmax[t] > amax)
+            amax = rmax[t];
+    }
+    mean = s1 / n;
+#pragma omp parallel for schedule(static) private(k)
+    for (t = 0; t < M; ++t) {
+        double a2 = 0.0, a4 = 0.0;
+        for (k = 0; k < K; ++k) {
+            double d = (double)bf16_to_float(X[t * K + k]) - mean;
+            double d2 = d * d;
+            a2 += d2;
+            a4 += d2 * d2;
+        }
+        r2[t] = a2;
+        r4[t] = a4;
+    }
+    for (t = 0; t < M; ++t) {
+        s2 += r2[t];
+        s4 += r4[t];
+    }
+    m2 = s2 / n;
+    m4 = s4 / n;
+    out[0] = (double)amax;
+    out[1] = mean;
+    out[2] = sqrt(m2);
+    out[3] = m2 > 0.0 ? m4 / (m2 * m2) : 0.0;
+    free(r1); free(r2); free(r4); free(rmax);
+    return 0;
 }

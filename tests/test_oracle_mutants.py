@@ -44,6 +44,14 @@ MUTANTS = {
     "bf16_double_rounding": ("q = nearbyint(ldexp(d, -ulp_exp));", "q = nearbyint(ldexp((double)(float)d, -ulp_exp));"),
     "bf16_subnormal_spacing": ("ulp_exp = -133;", "ulp_exp = -126;"),
     "protected_drops_bias": ("            if (bias)\n                acc += (double)bf16_to_float(bias[n]);\n", ""),
+    "moments_sample_std": ("out[2] = sqrt(m2);", "out[2] = sqrt(s2 / (n - 1.0));"),
+    "moments_excess_kurtosis": ("out[3] = m2 > 0.0 ? m4 / (m2 * m2) : 0.0;",
+                                "out[3] = m2 > 0.0 ? m4 / (m2 * m2) - 3.0 : 0.0;"),
+    "moments_not_centered": ("double d = (double)bf16_to_float(X[t * K + k]) - mean;",
+                             "double d = (double)bf16_to_float(X[t * K + k]);"),
+    "moments_signed_max": ("if (fabsf(x) > m)\n                m = fabsf(x);", "if (x > m)\n                m = x;"),
+    "moments_drops_last_row": ("    for (t = 0; t < M; ++t) {\n        s2 += r2[t];",
+                               "    for (t = 0; t + 1 < M; ++t) {\n        s2 += r2[t];"),
 }
 
 # every pin, with fixed arguments for the parametrized ones
@@ -65,6 +73,10 @@ PINS = [
     pins.test_epilogue_against_exact_rationals,
     pins.test_bf16_linear_small_integers_exact,
     pins.test_bf16_linear_random_vs_numpy_fp64,
+    pins.test_act_moments_against_exact_rationals,
+    pins.test_act_moments_two_point_and_constant,
+    pins.test_act_moments_shift_and_scale,
+    pins.test_act_moments_matches_scipy,
 ]
 
 

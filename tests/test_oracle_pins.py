@@ -378,3 +378,110 @@ def test_tiny_case_digest_is_stable():
     got = {"X": _digest(c["X"]), "W": _digest(c["W"]), "bias": _digest(c["bias"])}
     got.update({k: _digest(v) for k, v in r.items()})
     assert got == want["sha256"]
+
+
+# --------------------------------------------------------------------------
+# fragility profile (Section 3, "Activation-fragility profiling and
+# protection"): max |x|, standard deviation, kurtosis; top-N; Spearman
+# --------------------------------------------------------------------------
+
+def _exact_moments(vals):
+    """max |x|, mean, m2, m4 of bf16 values as exact rationals."""
+    fr = [Fraction(float(v)) for v in vals]
+    n = len(fr)
+    mean = sum(fr) / n
+    m2 = sum((x - mean) ** 2 for x in fr) / n
+    m4 = sum((x - mean) ** 4 for x in fr) / n
+    return max(abs(x) for x in fr), mean, m2, m4
+
+
+def test_act_moments_against_exact_rationals():
+    """Catches a missing centering, a sample (n-1) variance, an excess
+    (minus 3) kurtosis, a signed maximum or a dropped row."""
+    for seed, (M, K) in enumerate([(3, 7), (5, 16), (1, 33)]):
+        X = synth.rand_bf16([120, seed], (M, K), 1.0)
+        X[0, 0] = synth.to_bf16_bits(np.array([-5.25], np.float32))[0]  # largest magnitude, negative
+        X[-1, -1] = synth.to_bf16_bits(np.array([4.5], np.float32))[0]
+        got = oracle.act_moments(X, M, K)
+        amax, mean, m2, m4 = _exact_moments(bf16_to_f64(X.ravel()))
+        assert got[0] == float(amax) == 5.25
+        assert abs(got[1] - float(mean)) <= 1e-15 * max(1.0, abs(float(mean)))
+        assert got[2] == pytest.approx(float(m2) ** 0.5, rel=1e-14)
+        assert got[3] == pytest.approx(float(m4 / (m2 * m2)), rel=1e-13)
+
+
+def test_act_moments_two_point_and_constant():
+    a = synth.to_bf16_bits(np.array([0.375, -0.375], np.float32))
+    got = oracle.act_moments(np.tile(a, 12), 3, 8)
+    assert list(got) == [0.375, 0.0, 0.375, 1.0]        # kurtosis of +-a is exactly 1
+    c = np.full((4, 9), synth.to_bf16_bits(np.array([-2.5], np.float32))[0], np.uint16)
+    assert list(oracle.act_moments(c, 4, 9)) == [2.5, -2.5, 0.0, 0.0]   # constant: kurtosis 0
+
+
+def test_act_moments_textbook_kurtosis():
+    """Sample kurtosis of large bf16 samples against the distributions'
+    values: Gaussian 3, uniform 9/5, Laplace 6 (tolerances ~10 standard
+    errors; bf16 rounding moves them by far less)."""
+    rng = np.random.default_rng(121)
+    n = 1 << 21
+    cases = [(rng.standard_normal(n), 3.0, 0.035), (rng.uniform(-1, 1, n), 1.8, 0.01),
+             (rng.laplace(0, 1, n), 6.0, 0.2)]
+    for x, want, tol in cases:
+        b = synth.to_bf16_bits(x.astype(np.float32)).reshape(1024, -1)
+        got = oracle.act_moments(b, b.shape[0], b.shape[1])
+        assert abs(got[3] - want) < tol, (want, got[3])
+
+
+def test_act_moments_shift_and_scale():
+    """Integer-valued inputs: adding 64 (exact in bf16) shifts the mean only;
+    doubling scales max and std by 2 and leaves the kurtosis."""
+    rng = np.random.default_rng(122)
+    v = rng.integers(-60, 61, (37, 19)).astype(np.float32)
+    base = oracle.act_moments(synth.to_bf16_bits(v), 37, 19)
+    sh = oracle.act_moments(synth.to_bf16_bits(v + 64.0), 37, 19)
+    dbl = oracle.act_moments(synth.to_bf16_bits(2.0 * v), 37, 19)
+    assert sh[1] == pytest.approx(base[1] + 64.0, rel=1e-15)
+    assert sh[2] == pytest.approx(base[2], rel=1e-12)
+    assert sh[3] == pytest.approx(base[3], rel=1e-10)
+    assert dbl[0] == 2 * base[0] and dbl[2] == pytest.approx(2 * base[2], rel=1e-15)
+    assert dbl[3] == pytest.approx(base[3], rel=1e-14)
+
+
+def test_act_moments_matches_scipy():
+    from scipy import stats
+    c = synth.linear_case([123], 64, 8, 512, act="gelu")
+    x = bf16_to_f64(c["X"]).ravel()
+    got = oracle.act_moments(c["X"], 64, 512)
+    assert got[0] == np.abs(x).max()
+    assert got[1] == pytest.approx(x.mean(), rel=1e-13)
+    assert got[2] == pytest.approx(x.std(), rel=1e-13)
+    assert got[3] == pytest.approx(stats.kurtosis(x, fisher=False, bias=True), rel=1e-11)
+
+
+def test_act_moments_thread_invariant():
+    c = synth.linear_case([124], 77, 8, 320, act="gelu")
+    a = oracle.act_moments(c["X"], 77, 320)
+    n = oracle.num_threads()
+    oracle.set_num_threads(1)
+    try:
+        b = oracle.act_moments(c["X"], 77, 320)
+    finally:
+        oracle.set_num_threads(n)
+    assert np.array_equal(a, b)
+
+
+def test_fragility_scores_top_n_and_spearman():
+    from scipy import stats
+    k = np.array([[3.0, 5.0], [10.0, 12.0], [4.0, 4.0], [11.0, 11.0]])
+    assert list(oracle.fragility_scores(k)) == [4.0, 11.0, 4.0, 11.0]
+    assert oracle.top_n(oracle.fragility_scores(k), 3) == [1, 3, 0]   # ties by index
+    rng = np.random.default_rng(125)
+    for _ in range(20):
+        s = rng.integers(0, 6, 30).astype(float)        # many ties
+        n = int(rng.integers(0, 31))
+        brute = sorted(range(30), key=lambda i: (-s[i], i))[:n]
+        assert oracle.top_n(s, n) == brute
+        a, b = rng.integers(0, 8, 25), rng.normal(size=25)
+        assert oracle.spearman(a, b) == pytest.approx(stats.spearmanr(a, b).statistic, abs=1e-12)
+    assert oracle.spearman([1, 2, 3], [10, 20, 30]) == pytest.approx(1.0)
+    assert oracle.spearman([1, 2, 3], [3, 2, 1]) == pytest.approx(-1.0)

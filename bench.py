@@ -34,6 +34,7 @@ sys.path.insert(0, ROOT)
 import synth  # noqa: E402
 from paper_2606_12280_amd import layer as L  # noqa: E402
 from paper_2606_12280_amd import ops  # noqa: E402
+from paper_2606_12280_amd._lib import MOMENTS_WORK_BYTES as _MOMENTS_WORK  # noqa: E402
 
 METRIC = "W8A8 linear TOPS (% INT8 MFMA peak) + act-quant GB/s at DiT FFN shapes"
 PEAK_INT8_TOPS = 5000.0    # MI355X dense INT8 MFMA
@@ -258,6 +259,58 @@ def quant_isolated(lin: Linear, dev, reps: int = 60, rounds: int = 5):
         torch.cuda.synchronize()
         per.append(a.elapsed_time(b) * 1e3 / reps)
     del xs, qs
+    per = np.array(per)
+    return float(np.median(per)), float(per.min()), float(per.max())
+
+
+def moments_isolated(lin: Linear, dev, reps: int = 30, rounds: int = 5):
+    """The fragility-statistics call (two passes over X) alone, inputs
+    rotating over more than 700 MB so that X comes from HBM; back-to-back
+    calls between one pair of events. Median, min, max per call."""
+    M, K = lin.M, lin.lay.K
+    nbuf = max(3, int(np.ceil(700e6 / (2 * M * K))))
+    xs = [lin.xs[i % len(lin.xs)].clone() for i in range(nbuf)]
+    work = torch.empty(_MOMENTS_WORK, dtype=torch.uint8, device=dev)
+    out = torch.empty(4, dtype=torch.float64, device=dev)
+    for i in range(nbuf):
+        ops.w8a8_act_moments(xs[i], work, out=out)
+    torch.cuda.synchronize()
+    per = []
+    for _ in range(rounds):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for r in range(reps):
+            ops.w8a8_act_moments(xs[r % nbuf], work, out=out)
+        b.record()
+        torch.cuda.synchronize()
+        per.append(a.elapsed_time(b) * 1e3 / reps)
+    del xs
+    per = np.array(per)
+    return float(np.median(per)), float(per.min()), float(per.max())
+
+
+def absmax_isolated(lin: Linear, dev, reps: int = 30, rounds: int = 5):
+    """The per-channel absmax (calibration) alone, inputs rotating over more
+    than 700 MB; back-to-back calls between one pair of events."""
+    M, K = lin.M, lin.lay.K
+    nbuf = max(3, int(np.ceil(700e6 / (2 * M * K))))
+    xs = [lin.xs[i % len(lin.xs)].clone() for i in range(nbuf)]
+    s = torch.zeros(K, dtype=torch.float32, device=dev)
+    for i in range(nbuf):
+        ops.w8a8_act_absmax(xs[i], s)
+    torch.cuda.synchronize()
+    per = []
+    for _ in range(rounds):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for r in range(reps):
+            ops.w8a8_act_absmax(xs[r % nbuf], s)
+        b.record()
+        torch.cuda.synchronize()
+        per.append(a.elapsed_time(b) * 1e3 / reps)
+    del xs
     per = np.array(per)
     return float(np.median(per)), float(per.min()), float(per.max())
 
@@ -500,6 +553,20 @@ def main():
             "us": round(med, 2), "us_min": round(lo, 2), "us_max": round(hi, 2),
             "GB_s": round(by / med / 1e3, 1), "frac_hbm": round(by / med / 1e3 / PEAK_HBM_GBS, 4),
             "bytes": by}
+        # per-channel absmax over tokens (calibration of lambda)
+        med, lo, hi = absmax_isolated(lin, dev)
+        kernels[f"act_absmax_{lin.M}x{lin.lay.K}_hbm"] = {
+            "us": round(med, 2), "us_min": round(lo, 2), "us_max": round(hi, 2),
+            "GB_s": round(2 * lin.M * lin.lay.K / med / 1e3, 1),
+            "frac_hbm": round(2 * lin.M * lin.lay.K / med / 1e3 / PEAK_HBM_GBS, 4)}
+        # fragility statistics (calibration-time, not part of the step):
+        # one read of X is the minimum, the kernel reads it twice
+        med, lo, hi = moments_isolated(lin, dev)
+        one = 2 * lin.M * lin.lay.K
+        kernels[f"act_moments_{lin.M}x{lin.lay.K}_hbm"] = {
+            "us": round(med, 2), "us_min": round(lo, 2), "us_max": round(hi, 2),
+            "bytes_read": 2 * one, "GB_s_read": round(2 * one / med / 1e3, 1),
+            "frac_hbm_of_one_read": round(one / med / 1e3 / PEAK_HBM_GBS, 4)}
 
     roofline = None
     if dom is not None:

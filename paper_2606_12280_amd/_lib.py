@@ -21,11 +21,15 @@ _I64 = ctypes.c_int64
 _S = ctypes.c_int
 
 # name -> (argtypes, restype), in the order of include/w8a8.h
+# W8A8_MOMENTS_WORK_BYTES of the header: scratch of w8a8_act_moments.
+MOMENTS_WORK_BYTES = (2 * 1024 + 2) * 8
+
 SIGNATURES = {
     "w8a8_abi_version": ([], ctypes.c_int),
     "w8a8_status_string": ([ctypes.c_int], ctypes.c_char_p),
     "w8a8_last_hip_error": ([], ctypes.c_char_p),
     "w8a8_act_absmax": ([_P, _I64, _I64, _P, _P], _S),
+    "w8a8_act_moments": ([_P, _I64, _I64, _P, _P, _P], _S),
     "w8a8_smooth_factors": ([_P, _P, _I64, _I64, ctypes.c_double, _P, _P], _S),
     "w8a8_prepare_weight": ([_P, _P, _I64, _I64, _P, _P, _P, _P], _S),
     "w8a8_quant_act": ([_P, _P, _I64, _I64, _P, _P, _P], _S),

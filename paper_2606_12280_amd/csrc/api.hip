@@ -100,6 +100,19 @@ w8a8_status w8a8_act_absmax(const uint16_t *X, int64_t M, int64_t K, float *absm
     return hip_status(w8a8::launch_col_absmax(X, M, K, absmax, as_stream(stream)));
 }
 
+w8a8_status w8a8_act_moments(const uint16_t *X, int64_t M, int64_t K, void *work,
+                             double *stats, w8a8_stream stream) {
+    static_assert(W8A8_MOMENTS_WORK_BYTES == (2 * w8a8::kMomentBlocks + 2) * 8,
+                  "workspace size");
+    if (X == nullptr || work == nullptr || stats == nullptr) return W8A8_ERR_NULL;
+    W8A8_TRY(check_rows(M, kMaxRows));
+    W8A8_TRY(check_k(K));
+    if (!aligned(X, 16) || !aligned(work, 8) || !aligned(stats, 8)) return W8A8_ERR_ALIGN;
+    W8A8_TRY(check_alias({{work, W8A8_MOMENTS_WORK_BYTES}, {stats, 32}}, {{X, 2 * M * K}}));
+    return hip_status(w8a8::launch_act_moments(X, M * K, static_cast<double *>(work), stats,
+                                               as_stream(stream)));
+}
+
 w8a8_status w8a8_smooth_factors(const float *act_absmax, const uint16_t *W, int64_t N,
                                 int64_t K, double alpha, float *lambda, w8a8_stream stream) {
     if (act_absmax == nullptr || W == nullptr || lambda == nullptr) return W8A8_ERR_NULL;

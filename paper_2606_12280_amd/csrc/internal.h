@@ -23,6 +23,13 @@ hipError_t launch_reciprocal(const float *lam, int64_t K, float *inv,
 hipError_t launch_col_absmax(const uint16_t *src, int64_t R, int64_t K,
                              float *colmax, hipStream_t stream);
 
+// Fragility statistics of the n bf16 entries of X (8 | n): stats[0..3] =
+// max |x|, mean, population std, Pearson kurtosis (binary64). work holds
+// 2 * kMomentBlocks + 2 doubles of partials.
+constexpr int kMomentBlocks = 1024;
+hipError_t launch_act_moments(const uint16_t *X, int64_t n, double *work, double *stats,
+                              hipStream_t stream);
+
 // dst[k] = 0 for k < K (a fill kernel, so that the call can be captured).
 hipError_t launch_zero_f32(float *dst, int64_t K, hipStream_t stream);
 

@@ -195,34 +195,60 @@ __global__ void zero_kernel(float *__restrict__ dst, int64_t K) {
     if (k < K) dst[k] = 0.0f;
 }
 
-// Column absmax: a thread owns 8 consecutive columns and a strip of `strip`
-// rows; partial maxima merge with an integer atomic max (the bit patterns of
-// non-negative floats order like the floats).
-constexpr int64_t kColRows = 64;      // rows per strip, at least
-constexpr int64_t kColStrips = 32768; // strips (grid height), at most
+// Column absmax: a workgroup covers 64 chunks of 8 columns (512 columns) of a
+// strip of rows; its kColWaves waves take interleaved rows (wave w: r0 + w,
+// r0 + w + kColWaves, ...), each lane 16 bytes of a row with 4 rows in
+// flight, so that every wave load is a contiguous 1 KiB. The waves' maxima
+// combine in LDS and one integer atomic max per column leaves the workgroup
+// (the bit patterns of non-negative floats order like the floats). Strips
+// are sized for about kColBlocks workgroups; atomics on one address
+// serialize, so a column sees at most about kColBlocks / (K / 512) of them.
+constexpr int64_t kColBlocks = 512;
+constexpr int kColWaves = 16;
+constexpr int kColUnroll = 4;
 
-__global__ __launch_bounds__(256) void col_absmax_kernel(const uint16_t *__restrict__ src,
-                                                          int64_t R, int64_t K, int64_t strip,
-                                                          float *__restrict__ colmax) {
-    const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;  // chunk of 8
-    if (j * 8 >= K) return;
+__global__ __launch_bounds__(kColWaves * 64) void col_absmax_kernel(
+    const uint16_t *__restrict__ src, int64_t R, int64_t K, int64_t strip,
+    float *__restrict__ colmax) {
+    __shared__ float red[kColWaves][64][9];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int64_t j = static_cast<int64_t>(blockIdx.x) * 64 + lane;  // chunk of 8 columns
+    const bool ok = j * 8 < K;
     const int64_t r0 = static_cast<int64_t>(blockIdx.y) * strip;
     const int64_t r1 = r0 + strip < R ? r0 + strip : R;
     float m[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int64_t r = r0; r < r1; ++r) {
-        const uint4 x = reinterpret_cast<const uint4 *>(src + r * K)[j];
-        m[0] = fmaxf(m[0], fabsf(bf16_lo(x.x)));
-        m[1] = fmaxf(m[1], fabsf(bf16_hi(x.x)));
-        m[2] = fmaxf(m[2], fabsf(bf16_lo(x.y)));
-        m[3] = fmaxf(m[3], fabsf(bf16_hi(x.y)));
-        m[4] = fmaxf(m[4], fabsf(bf16_lo(x.z)));
-        m[5] = fmaxf(m[5], fabsf(bf16_hi(x.z)));
-        m[6] = fmaxf(m[6], fabsf(bf16_lo(x.w)));
-        m[7] = fmaxf(m[7], fabsf(bf16_hi(x.w)));
+    for (int64_t r = r0 + wave; r < r1; r += kColWaves * kColUnroll) {
+        uint4 x[kColUnroll];
+#pragma unroll
+        for (int u = 0; u < kColUnroll; ++u) {
+            const int64_t ru = r + kColWaves * u;
+            x[u] = (ok && ru < r1) ? reinterpret_cast<const uint4 *>(src + ru * K)[j]
+                                   : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int u = 0; u < kColUnroll; ++u) {
+            m[0] = fmaxf(m[0], fabsf(bf16_lo(x[u].x)));
+            m[1] = fmaxf(m[1], fabsf(bf16_hi(x[u].x)));
+            m[2] = fmaxf(m[2], fabsf(bf16_lo(x[u].y)));
+            m[3] = fmaxf(m[3], fabsf(bf16_hi(x[u].y)));
+            m[4] = fmaxf(m[4], fabsf(bf16_lo(x[u].z)));
+            m[5] = fmaxf(m[5], fabsf(bf16_hi(x[u].z)));
+            m[6] = fmaxf(m[6], fabsf(bf16_lo(x[u].w)));
+            m[7] = fmaxf(m[7], fabsf(bf16_hi(x[u].w)));
+        }
     }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) red[wave][lane][e] = m[e];
+    __syncthreads();
+    if (wave != 0 || !ok) return;
     unsigned int *dst = reinterpret_cast<unsigned int *>(colmax) + j * 8;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) atomicMax(dst + e, __float_as_uint(m[e]));
+    for (int e = 0; e < 8; ++e) {
+        float v = red[0][lane][e];
+        for (int w = 1; w < kColWaves; ++w) v = fmaxf(v, red[w][lane][e]);
+        atomicMax(dst + e, __float_as_uint(v));
+    }
 }
 
 __global__ void lambda_kernel(const float *__restrict__ s, float *__restrict__ lam, int64_t K,
@@ -277,10 +303,16 @@ hipError_t launch_zero_f32(float *dst, int64_t K, hipStream_t stream) {
 
 hipError_t launch_col_absmax(const uint16_t *src, int64_t R, int64_t K, float *colmax,
                              hipStream_t stream) {
-    int64_t strip = (R + kColStrips - 1) / kColStrips;
-    if (strip < kColRows) strip = kColRows;
-    const dim3 grid(blocks_for(K / 8, 256), static_cast<unsigned>((R + strip - 1) / strip));
-    hipLaunchKernelGGL(col_absmax_kernel, grid, dim3(256), 0, stream, src, R, K, strip, colmax);
+    const int64_t gx = (K / 8 + 63) / 64;
+    int64_t strips = (kColBlocks + gx - 1) / gx;
+    const int64_t max_strips = (R + kColWaves - 1) / kColWaves;  // a row per wave at least
+    if (strips > max_strips) strips = max_strips;
+    if (strips > 65535) strips = 65535;
+    if (strips < 1) strips = 1;
+    const int64_t strip = (R + strips - 1) / strips;
+    const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>((R + strip - 1) / strip));
+    hipLaunchKernelGGL(col_absmax_kernel, grid, dim3(kColWaves * 64), 0, stream, src, R, K,
+                       strip, colmax);
     return hipGetLastError();
 }
 

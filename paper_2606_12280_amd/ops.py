@@ -9,7 +9,7 @@ from __future__ import annotations
 
 import torch
 
-from ._lib import check, load
+from ._lib import MOMENTS_WORK_BYTES, check, load
 
 __all__ = [
     "w8a8_act_absmax", "w8a8_smooth_factors", "w8a8_prepare_weight", "w8a8_quant_act",
@@ -62,6 +62,26 @@ def w8a8_act_absmax(X: torch.Tensor, absmax: torch.Tensor) -> torch.Tensor:
         check("w8a8_act_absmax",
               lib.w8a8_act_absmax(_ptr(X), M, K, _ptr(absmax), _stream(X.device)))
     return absmax
+
+
+def w8a8_act_moments(X: torch.Tensor, work: torch.Tensor | None = None,
+                     out: torch.Tensor | None = None) -> torch.Tensor:
+    """Fragility statistics of a linear's input: float64 [max |x|, mean,
+    population std, Pearson kurtosis] on X's device. `work` (uint8, at least
+    MOMENTS_WORK_BYTES) may be passed to avoid allocating it per call."""
+    _need(X, "X", torch.bfloat16, 2)
+    M, K = X.shape
+    stats = _out(out, (4,), torch.float64, X.device, "out")
+    if work is None:
+        work = torch.empty(MOMENTS_WORK_BYTES, dtype=torch.uint8, device=X.device)
+    _need(work, "work", torch.uint8, 1, X.device)
+    if work.numel() < MOMENTS_WORK_BYTES:
+        raise ValueError(f"work needs {MOMENTS_WORK_BYTES} bytes")
+    lib = load()
+    with torch.cuda.device(X.device):
+        check("w8a8_act_moments",
+              lib.w8a8_act_moments(_ptr(X), M, K, _ptr(work), _ptr(stats), _stream(X.device)))
+    return stats
 
 
 def w8a8_smooth_factors(act_absmax: torch.Tensor, W: torch.Tensor, alpha: float = 0.5,

@@ -106,6 +106,23 @@ def test_calibration_validation(lib):
     assert g(A + 2, 8, 64, C, None) == ALIGN
 
 
+def test_moments_validation(lib):
+    f = lib.w8a8_act_moments
+    assert f(None, 8, 64, B, C, None) == NULL
+    assert f(A, 8, 64, None, C, None) == NULL
+    assert f(A, 8, 64, B, None, None) == NULL
+    assert f(A, 0, 64, B, C, None) == SHAPE
+    assert f(A, 8, 0, B, C, None) == SHAPE
+    assert f(A, 8, 96, B, C, None) == UNSUP          # K % 64 != 0
+    assert f(A + 2, 8, 64, B, C, None) == ALIGN
+    assert f(A, 8, 64, B + 4, C, None) == ALIGN
+    assert f(A, 8, 64, B, C + 4, None) == ALIGN
+    assert f(A, 8, 64, A + 512, C, None) == ALIAS     # workspace inside X (1 KiB)
+    assert f(A, 8, 64, B, B + 1024, None) == ALIAS    # stats inside the workspace
+    assert f(A, 8, 64, B, A, None) == ALIAS
+    assert _lib.MOMENTS_WORK_BYTES == (2 * 1024 + 2) * 8
+
+
 def test_binding_rejects_host_tensors():
     X = torch.zeros(4, 64, dtype=torch.bfloat16)
     il = torch.ones(64)

@@ -15,7 +15,7 @@ import torch
 
 import oracle
 import synth
-from parity import (check_bf16_output, check_w8a8_output, dev, dev_bf16, host,
+from parity import (DEV, check_bf16_output, check_w8a8_output, dev, dev_bf16, host,
                     host_bits)
 
 pytestmark = pytest.mark.gpu
@@ -107,6 +107,86 @@ def test_smooth_factors(alpha):
     assert ulps.max() <= 1
     if alpha == 0.5:
         assert np.array_equal(lam, lam_ref)     # sqrt and divide are correctly rounded
+
+
+# --------------------------------------------------------------------------
+# fragility profile (Section 3, "Activation-fragility profiling and
+# protection")
+# --------------------------------------------------------------------------
+
+def _check_moments(got, ref):
+    """max |x| bit-exact; mean, std and kurtosis to binary64 summation-order
+    error (the GPU adds in a different order than the oracle)."""
+    assert got[0] == ref[0]
+    assert abs(got[1] - ref[1]) <= 1e-13 * ref[2] + 1e-15 * abs(ref[1])
+    assert got[2] == pytest.approx(ref[2], rel=1e-12)
+    assert got[3] == pytest.approx(ref[3], rel=1e-10)
+
+
+@pytest.mark.parametrize("M,K,act", [(1, 64, "normal"), (3, 192, "gelu"), (257, 1088, "gelu"),
+                                     (64, 4096, "outlier"), (1000, 16384, "gelu")])
+def test_act_moments_parity(M, K, act):
+    c = synth.linear_case([115, M, K], M, 8, K, act=act)
+    ref = oracle.act_moments(c["X"], M, K)
+    got = host(ops.w8a8_act_moments(dev_bf16(c["X"])))
+    _check_moments(got, ref)
+
+
+def test_act_moments_special_inputs():
+    """Constant input (std 0, kurtosis 0), +-a (kurtosis exactly 1), a single
+    outlier entry, and the largest bf16 magnitudes."""
+    two = synth.to_bf16_bits(np.array([0.75, -0.75], np.float32))
+    big = synth.to_bf16_bits(np.array([3.0e38, -3.0e38], np.float32))
+    cases = [np.full((5, 64), 0x4040, np.uint16), np.tile(two, (7, 64)),
+             np.tile(big, (2, 64))]
+    one = np.zeros((9, 128), np.uint16)
+    one[4, 77] = 0x4480                                  # 1024.0
+    cases.append(one)
+    for X in cases:
+        M, K = X.shape
+        ref = oracle.act_moments(X, M, K)
+        got = host(ops.w8a8_act_moments(dev_bf16(X)))
+        if ref[2] == 0.0:
+            assert list(got) == list(ref)
+        else:
+            _check_moments(got, ref)
+    assert list(host(ops.w8a8_act_moments(dev_bf16(np.tile(two, (7, 64)))))) == [0.75, 0.0, 0.75, 1.0]
+
+
+def test_act_moments_full_size_and_deterministic():
+    c = synth.ffn_down_case()
+    X = dev_bf16(c["X"])
+    ref = oracle.act_moments(c["X"], c["M"], c["K"])
+    work = torch.empty(_lib_work_bytes(), dtype=torch.uint8, device=DEV)
+    a = host(ops.w8a8_act_moments(X, work))
+    b = host(ops.w8a8_act_moments(X, work))
+    assert np.array_equal(a, b)                          # same bits on every call
+    _check_moments(a, ref)
+
+
+def test_profile_selects_like_the_oracle():
+    """A 6-layer, 3-step profile through fragility.Profile: the selected
+    layers equal the oracle's top-2 of the oracle's own statistics."""
+    from paper_2606_12280_amd import fragility
+    L, T, M, K = 6, 3, 64, 256
+    prof = fragility.Profile(L, T, DEV)
+    kurt = np.zeros((L, T))
+    for layer in range(L):
+        for step in range(T):
+            act = "gelu" if layer in (1, 4) else "normal"
+            c = synth.linear_case([116, layer, step], M, 8, K, act=act)
+            prof.record(layer, step, dev_bf16(c["X"]))
+            kurt[layer, step] = oracle.act_moments(c["X"], M, K)[3]
+    table = prof.table()
+    assert np.allclose(table[:, :, 3], kurt, rtol=1e-10)
+    want = oracle.top_n(oracle.fragility_scores(kurt), 2)
+    assert fragility.select_protected(prof.scores(), 2) == want
+    assert sorted(want) == [1, 4]
+
+
+def _lib_work_bytes():
+    from paper_2606_12280_amd import _lib
+    return _lib.MOMENTS_WORK_BYTES
 
 
 # --------------------------------------------------------------------------

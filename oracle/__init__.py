@@ -69,6 +69,10 @@ def _load():
         "oracle_w8a8_linear": ([P, P, P, P, P, I64, I64, I64, P], None),
         "oracle_bf16_linear": ([P, P, P, I64, I64, I64, P], None),
         "oracle_act_moments": ([P, I64, I64, P], ctypes.c_int),
+        "oracle_float_to_half": ([ctypes.c_float], ctypes.c_uint16),
+        "oracle_half_to_float": ([ctypes.c_uint16], ctypes.c_float),
+        "oracle_q8_0_quantize": ([P, I64, I64, P, P], None),
+        "oracle_q8_0_dequantize": ([P, P, I64, I64, P], None),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -258,3 +262,42 @@ def spearman(a, b) -> float:
     va = sum((x - ma) ** 2 for x in ra)
     vb = sum((y - mb) ** 2 for y in rb)
     return cov / (va * vb) ** 0.5
+
+
+# --------------------------------------------------------------------------
+# GGUF Q8_0 weight-only (Section 3, "GGUF k-quants")
+# --------------------------------------------------------------------------
+
+Q8_0_BLOCK = 32
+
+
+def float_to_half(f: float) -> int:
+    return int(_load().oracle_float_to_half(float(f)))
+
+
+def half_to_float(h: int) -> float:
+    return float(_load().oracle_half_to_float(int(h)))
+
+
+def q8_0_quantize(W, N: int, K: int):
+    """W [N][K] bf16 bits -> (codes int8 [N][K], scales binary16 bits [N][K/32])."""
+    W = _c(W, np.uint16)
+    qs = np.zeros(N * K, np.int8)
+    d = np.zeros(N * (K // Q8_0_BLOCK), np.uint16)
+    _load().oracle_q8_0_quantize(_p(W), N, K, _p(qs), _p(d))
+    return qs.reshape(N, K), d.reshape(N, K // Q8_0_BLOCK)
+
+
+def q8_0_dequantize(qs, d, N: int, K: int) -> np.ndarray:
+    """bf16 bits [N][K] of bf16(d * q)."""
+    qs = _c(qs, np.int8)
+    d = _c(d, np.uint16)
+    W = np.zeros(N * K, np.uint16)
+    _load().oracle_q8_0_dequantize(_p(qs), _p(d), N, K, _p(W))
+    return W.reshape(N, K)
+
+
+def q8_0_linear(X, qs, d, bias, M: int, N: int, K: int) -> np.ndarray:
+    """The weight-only linear: bf16 X times the dequantized weights (the
+    protected-layer arithmetic on bf16(d * q))."""
+    return bf16_linear(X, q8_0_dequantize(qs, d, N, K), bias, M, N, K)

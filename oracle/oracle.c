@@ -37,7 +37,11 @@
  *     channel whose activation or weight statistic is zero keeps lambda = 1;
  *   - the fragility profile of a layer's input is max |x|, the population
  *     standard deviation and the Pearson kurtosis m4 / m2^2 over all its
- *     entries, in binary64; a constant input has kurtosis 0.
+ *     entries, in binary64; a constant input has kurtosis 0;
+ *   - GGUF Q8_0 (Section 3, "GGUF k-quants"): blocks of 32 consecutive
+ *     weights of a row; d = RN16(min(RN32(amax / 127), 65504)), codes
+ *     clamp(rint(w * RN32(1 / d)), -127, 127) with the stored d (all zero when
+ *     d is 0); a weight reads back as bf16(d * q).
  *
  * Parallelism: rows are independent and each row is computed by one thread in
  * a fixed order, so results do not depend on the thread count.
@@ -373,4 +377,107 @@ int oracle_act_moments(const uint16_t *X, int64_t M, int64_t K, double *out)
     out[3] = m2 > 0.0 ? m4 / (m2 * m2) : 0.0;
     free(r1); free(r2); free(r4); free(rmax);
     return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* GGUF Q8_0 weight-only format (Section 3, "GGUF k-quants": 8.5 bits    */
+/* per weight, round to nearest).                                       */
+/* ------------------------------------------------------------------ */
+
+#define ORACLE_Q8_0_BLOCK 32
+#define ORACLE_HALF_MAX 65504.0f
+
+/* binary16 (1 sign, 5 exponent, 10 fraction bits) <-> binary32. */
+static float half_to_float(uint16_t h)
+{
+    int e = (h >> 10) & 0x1f;
+    double m = (double)(h & 0x3ff);
+    double v;
+    if (e == 0)
+        v = ldexp(m, -24);                       /* subnormal: m * 2^-24 */
+    else if (e == 31)
+        v = m == 0.0 ? INFINITY : NAN;
+    else
+        v = ldexp(1024.0 + m, e - 25);           /* (1 + m/1024) * 2^(e-15) */
+    return (float)((h & 0x8000) ? -v : v);
+}
+
+/* Round a finite binary32 value to the nearest binary16, ties to even, in a
+ * single rounding (11 significant bits, subnormals spaced 2^-24). Values
+ * that round past 65504 give infinity. */
+static uint16_t float_to_half(float f)
+{
+    double d = (double)f, q, r;
+    int e, ulp_exp;
+    uint16_t sign = signbit(d) ? 0x8000u : 0u;
+    if (d == 0.0)
+        return sign;
+    frexp(fabs(d), &e);                          /* |d| = m * 2^e, m in [0.5, 1) */
+    ulp_exp = e - 11;
+    if (ulp_exp < -24)
+        ulp_exp = -24;
+    q = nearbyint(ldexp(fabs(d), -ulp_exp));     /* exact scaling, ties to even */
+    r = ldexp(q, ulp_exp);
+    if (r > 65504.0)
+        return sign | 0x7c00u;
+    if (r < 0x1p-14)                             /* subnormal (or rounds to 2^-14) */
+        return sign | (uint16_t)ldexp(r, 24);
+    frexp(r, &e);                                /* r = m * 2^e */
+    return sign | (uint16_t)(((e + 14) << 10) | ((uint32_t)ldexp(r, 11 - e) & 0x3ff));
+}
+
+uint16_t oracle_float_to_half(float f) { return float_to_half(f); }
+float oracle_half_to_float(uint16_t h) { return half_to_float(h); }
+
+/* W [N][K] bf16 (K a multiple of 32) -> codes qs [N][K] int8 and one scale
+ * d [N][K/32] binary16 per block of 32 consecutive weights of a row:
+ *   amax = max |w| over the block, d = RN16(min(RN32(amax / 127), 65504)),
+ *   q = clamp(rint(w * RN32(1 / float(d))), -127, 127), all q = 0 if d = 0.
+ * Binary32, one rounding per operation. */
+void oracle_q8_0_quantize(const uint16_t *W, int64_t N, int64_t K, int8_t *qs,
+                          uint16_t *d)
+{
+    int64_t n;
+#pragma omp parallel for schedule(static)
+    for (n = 0; n < N; ++n) {
+        int64_t b;
+        for (b = 0; b < K / ORACLE_Q8_0_BLOCK; ++b) {
+            const uint16_t *w = W + n * K + b * ORACLE_Q8_0_BLOCK;
+            int8_t *q = qs + n * K + b * ORACLE_Q8_0_BLOCK;
+            float amax = 0.0f, s, inv, ds;
+            int j;
+            for (j = 0; j < ORACLE_Q8_0_BLOCK; ++j)
+                if (fabsf(bf16_to_float(w[j])) > amax)
+                    amax = fabsf(bf16_to_float(w[j]));
+            s = amax / 127.0f;
+            if (s > ORACLE_HALF_MAX)
+                s = ORACLE_HALF_MAX;
+            d[n * (K / ORACLE_Q8_0_BLOCK) + b] = float_to_half(s);
+            ds = half_to_float(d[n * (K / ORACLE_Q8_0_BLOCK) + b]);
+            inv = ds != 0.0f ? 1.0f / ds : 0.0f;
+            for (j = 0; j < ORACLE_Q8_0_BLOCK; ++j) {
+                float c = rintf(bf16_to_float(w[j]) * inv);
+                if (c > 127.0f)
+                    c = 127.0f;
+                if (c < -127.0f)
+                    c = -127.0f;
+                q[j] = (int8_t)c;
+            }
+        }
+    }
+}
+
+/* W'[n][k] = bf16(float(d[n][k / 32]) * qs[n][k]) (the product is exact in
+ * binary32: 11 x 8 significant bits; one rounding to bf16). */
+void oracle_q8_0_dequantize(const int8_t *qs, const uint16_t *d, int64_t N, int64_t K,
+                            uint16_t *W)
+{
+    int64_t n, k;
+#pragma omp parallel for schedule(static) private(k)
+    for (n = 0; n < N; ++n)
+        for (k = 0; k < K; ++k) {
+            float v = half_to_float(d[n * (K / ORACLE_Q8_0_BLOCK) + k / ORACLE_Q8_0_BLOCK]) *
+                      (float)qs[n * K + k];
+            W[n * K + k] = double_to_bf16((double)v);
+        }
 }

@@ -50,6 +50,14 @@ MUTANTS = {
     "moments_not_centered": ("double d = (double)bf16_to_float(X[t * K + k]) - mean;",
                              "double d = (double)bf16_to_float(X[t * K + k]);"),
     "moments_signed_max": ("if (fabsf(x) > m)\n                m = fabsf(x);", "if (x > m)\n                m = x;"),
+    "half_truncates": ("q = nearbyint(ldexp(fabs(d), -ulp_exp));", "q = floor(ldexp(fabs(d), -ulp_exp));"),
+    "half_no_subnormals": ("    if (ulp_exp < -24)\n        ulp_exp = -24;\n    q = nearbyint(ldexp(fabs(d), -ulp_exp));",
+                           "    if (ulp_exp < -14)\n        ulp_exp = -14;\n    q = nearbyint(ldexp(fabs(d), -ulp_exp));"),
+    "q8_0_codes_from_unrounded_scale": ("inv = ds != 0.0f ? 1.0f / ds : 0.0f;", "inv = s != 0.0f ? 1.0f / s : 0.0f;"),
+    "q8_0_no_clamp": ("                if (c > 127.0f)\n                    c = 127.0f;\n", ""),
+    "q8_0_no_scale_cap": ("            if (s > ORACLE_HALF_MAX)\n                s = ORACLE_HALF_MAX;\n", ""),
+    "q8_0_dequant_drops_scale": ("float v = half_to_float(d[n * (K / ORACLE_Q8_0_BLOCK) + k / ORACLE_Q8_0_BLOCK]) *\n                      (float)qs[n * K + k];",
+                                 "float v = (float)qs[n * K + k];"),
     "moments_drops_last_row": ("    for (t = 0; t < M; ++t) {\n        s2 += r2[t];",
                                "    for (t = 0; t + 1 < M; ++t) {\n        s2 += r2[t];"),
 }
@@ -77,6 +85,11 @@ PINS = [
     pins.test_act_moments_two_point_and_constant,
     pins.test_act_moments_shift_and_scale,
     pins.test_act_moments_matches_scipy,
+    pins.test_half_conversion_matches_numpy,
+    pins.test_q8_0_invariants,
+    pins.test_q8_0_exact_grid_and_ties,
+    pins.test_q8_0_special_blocks,
+    pins.test_q8_0_dequantize_is_one_rounding,
 ]
 
 

@@ -485,3 +485,111 @@ def test_fragility_scores_top_n_and_spearman():
         assert oracle.spearman(a, b) == pytest.approx(stats.spearmanr(a, b).statistic, abs=1e-12)
     assert oracle.spearman([1, 2, 3], [10, 20, 30]) == pytest.approx(1.0)
     assert oracle.spearman([1, 2, 3], [3, 2, 1]) == pytest.approx(-1.0)
+
+
+# --------------------------------------------------------------------------
+# GGUF Q8_0 weight-only (Section 3, "GGUF k-quants": 8.5 bits per weight,
+# round to nearest)
+# --------------------------------------------------------------------------
+
+def test_half_conversion_matches_numpy():
+    """binary16 rounding (ties to even, subnormals, overflow) against numpy,
+    and widening of every finite bit pattern."""
+    rng = np.random.default_rng(140)
+    vals = np.concatenate([rng.normal(0, 1, 2000), rng.normal(0, 1e-5, 2000),
+                           rng.uniform(-70000, 70000, 2000), 2.0 ** rng.uniform(-26, -13, 2000),
+                           [65504.0, 65519.9, 65520.0, 2.0 ** -24, 2.0 ** -25, 3 * 2.0 ** -26,
+                            2.0 ** -14 * (1 - 2.0 ** -11), 1 + 2.0 ** -11, 1 + 3 * 2.0 ** -11]]
+                          ).astype(np.float32)
+    with np.errstate(over="ignore"):
+        want = vals.astype(np.float16).view(np.uint16)
+    got = np.array([oracle.float_to_half(float(v)) for v in vals], np.uint16)
+    assert np.array_equal(got, want)
+    bits = np.arange(0x10000, dtype=np.uint32).astype(np.uint16)
+    finite = (bits & 0x7c00) != 0x7c00
+    wide = np.array([oracle.half_to_float(int(b)) for b in bits[finite]], np.float32)
+    assert np.array_equal(wide, bits[finite].view(np.float16).astype(np.float32))
+
+
+def _f16(bits) -> np.ndarray:
+    return np.asarray(bits, np.uint16).view(np.float16).astype(np.float32)
+
+
+def test_q8_0_invariants():
+    """Codes in [-127, 127], 127 reached in every block, scale = amax/127
+    to binary16 precision, reconstruction within half a step."""
+    N, K = 48, 256
+    W = synth.rand_bf16([141], (N, K), 0.02)
+    qs, d = oracle.q8_0_quantize(W, N, K)
+    w = bf16_to_f64(W).reshape(N, K // 32, 32)
+    q = qs.reshape(N, K // 32, 32).astype(np.float64)
+    ds = _f16(d).astype(np.float64)[..., None]
+    amax = np.abs(w).max(axis=2)
+    assert np.abs(q).max() <= 127
+    assert np.array_equal(np.abs(q).max(axis=2), np.full_like(amax, 127))
+    assert np.allclose(ds[..., 0], amax / 127, rtol=2.0 ** -11)
+    assert np.all(np.abs(w - ds * q) <= ds * (0.5 + 2.0 ** -12))
+
+
+def test_q8_0_exact_grid_and_ties():
+    """Multiples of 1/16 with a block maximum of 127/16: the scale is exact
+    and every weight reads back exactly. With scale 1: +-0.5, 2.5, 3.5 tie
+    to even."""
+    rng = np.random.default_rng(142)
+    k = rng.integers(-127, 128, (8, 64)).astype(np.float32)
+    k[:, 0] = 127
+    k[:, 32] = -127
+    W = synth.to_bf16_bits(k / 16)
+    qs, d = oracle.q8_0_quantize(W, 8, 64)
+    assert np.all(_f16(d) == 1 / 16)
+    assert np.array_equal(qs, k.astype(np.int8))
+    assert np.array_equal(oracle.q8_0_dequantize(qs, d, 8, 64), W)
+    t = np.array([127.0, 0.5, -0.5, 1.5, 2.5, -2.5, 3.5, 126.5] + [0.0] * 24, np.float32)
+    qs, d = oracle.q8_0_quantize(synth.to_bf16_bits(t), 1, 32)
+    assert _f16(d)[0, 0] == 1.0
+    assert list(qs[0, :8]) == [127, 0, 0, 2, 2, -2, 4, 126]
+
+
+def test_q8_0_special_blocks():
+    """A zero block (scale 0, zero codes), a block whose scale underflows
+    binary16 (zero codes), and a block whose scale is capped at 65504 (codes
+    clamp at +-127)."""
+    W = np.zeros((1, 96), np.float32)
+    W[0, 32:64] = 2.0 ** -30
+    W[0, 64] = 9.0e6
+    W[0, 65] = -1.0e6
+    B = synth.to_bf16_bits(W)
+    qs, d = oracle.q8_0_quantize(B, 1, 96)
+    assert d[0, 0] == 0 and not qs[0, :32].any()
+    assert d[0, 1] == 0 and not qs[0, 32:64].any()
+    assert _f16(d)[0, 2] == 65504.0
+    assert qs[0, 64] == 127 and qs[0, 65] == round(-1.0e6 / 65504.0)
+
+
+def test_q8_0_dequantize_is_one_rounding():
+    rng = np.random.default_rng(143)
+    qs = rng.integers(-127, 128, (5, 64)).astype(np.int8)
+    d = np.array([[oracle.float_to_half(float(v)) for v in rng.lognormal(-6, 3, 2)] for _ in range(5)],
+                 np.uint16)
+    got = oracle.q8_0_dequantize(qs, d, 5, 64)
+    for n in range(5):
+        for kk in range(64):
+            exact = Fraction(float(_f16(d[n, kk // 32]))) * int(qs[n, kk])
+            assert got[n, kk] == round_bf16_exact(exact)
+
+
+def test_q8_0_linear_against_numpy_fp64():
+    """The weight-only linear against binary64 X W'^T + b on the decoded
+    weights, within the binary32 summation bound plus one bf16 rounding."""
+    c = synth.linear_case([144], 33, 40, 256)
+    qs, d = oracle.q8_0_quantize(c["W"], 40, 256)
+    Wd = oracle.q8_0_dequantize(qs, d, 40, 256)
+    Y = oracle.q8_0_linear(c["X"], qs, d, c["bias"], 33, 40, 256)
+    X = bf16_to_f64(c["X"]).reshape(33, 256)
+    ref = X @ bf16_to_f64(Wd).reshape(40, 256).T + bf16_to_f64(c["bias"])[None, :]
+    y = bf16_to_f64(Y).reshape(33, 40)
+    assert np.all(np.abs(y - ref) <= np.abs(ref) * 2.0 ** -8 + 1e-30)
+    # and the quantization error of the weights stays within half a step
+    Wf = bf16_to_f64(c["W"]).reshape(40, 8, 32)
+    step = _f16(d).astype(np.float64)[..., None]
+    assert np.all(np.abs(bf16_to_f64(Wd).reshape(40, 8, 32) - Wf) <= step * 0.5 + np.abs(Wf) * 2.0 ** -8)

@@ -135,6 +135,11 @@ def device_inputs(M, K, dev, gen, n, gelu: bool):
 
 
 def build_workload(name: str, dev, pool: int):
+    if name == "q8_0_ffn_up":
+        c = synth.ffn_up_case()
+        lin = host_case_linear("ffn_up", c, dev, pool, True, 2)
+        lin.lay = L.prepare_q8_0(lin.lay.W, lin.lay.bias)  # the bf16 copy is dropped
+        return [lin]
     if name == "ffn_up":
         return [host_case_linear("ffn_up", synth.ffn_up_case(), dev, pool, False, 2)]
     if name == "ffn_down":
@@ -181,6 +186,13 @@ def run_step(layers, it: int, ws: L.Workspace, events=None):
                 events[li][0].record()
                 events[li][1].record()
             ops.bf16_linear(X, lin.lay.W, lin.lay.bias, out=lin.Y)
+        elif lin.lay.q8_0:
+            if events is not None:
+                events[li][0].record()
+            ops.q8_0_dequantize(lin.lay.q8_qs, lin.lay.q8_d, out=ws.weights(lin.lay.N, lin.lay.K))
+            if events is not None:
+                events[li][1].record()
+            ops.bf16_linear(X, ws.weights(lin.lay.N, lin.lay.K), lin.lay.bias, out=lin.Y)
         else:
             Xq, xs = ws.get(lin.M, lin.lay.K)
             if events is not None:
@@ -474,7 +486,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="ffn_up",
-                    choices=["ffn_up", "ffn_down", "dit_block", "backbone"])
+                    choices=["ffn_up", "ffn_down", "dit_block", "backbone", "q8_0_ffn_up"])
     ap.add_argument("--pool", type=int, default=4, help="distinct inputs rotated over steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -517,10 +529,22 @@ def main():
     total_ops = sum(lin.ops for lin in layers)
     value = total_ops / (step_ms * 1e-3) / 1e12
 
-    w8 = [i for i, lin in enumerate(layers) if not lin.lay.protected]
+    w8 = [i for i, lin in enumerate(layers) if not lin.lay.protected and not lin.lay.q8_0]
     prot = [i for i, lin in enumerate(layers) if lin.lay.protected]
+    q8 = [i for i, lin in enumerate(layers) if lin.lay.q8_0]
     dom = max(w8, key=lambda i: gemm_us[i]) if w8 else None
     kernels = {}
+    for i in q8:
+        lin = layers[i]
+        M, N, K = lin.M, lin.lay.N, lin.lay.K
+        g, q = float(gemm_us[i]), float(quant_us[i])
+        dq_bytes = N * K + N * K // 16 + 2 * N * K   # codes + scales in, bf16 out
+        kernels[f"q8_0_dequantize_{N}x{K}_in_step"] = {
+            "us": round(q, 2), "GB_s": round(dq_bytes / q / 1e3, 1),
+            "frac_hbm": round(dq_bytes / q / 1e3 / PEAK_HBM_GBS, 4)}
+        kernels[f"q8_0_bf16_gemm_{M}x{K}x{N}"] = {
+            "us": round(g, 2), "TFLOPS": round(2 * M * N * K / g / 1e6, 1),
+            "frac_bf16_peak": round(2 * M * N * K / g / 1e6 / PEAK_BF16_TFLOPS, 4)}
     for shape_key in sorted({(layers[i].M, layers[i].lay.N, layers[i].lay.K) for i in w8}):
         idx = [i for i in w8 if (layers[i].M, layers[i].lay.N, layers[i].lay.K) == shape_key]
         M, N, K = shape_key
@@ -569,6 +593,13 @@ def main():
             "frac_hbm_of_one_read": round(one / med / 1e3 / PEAK_HBM_GBS, 4)}
 
     roofline = None
+    if dom is None and q8:
+        i = q8[0]
+        ach = layers[i].ops / (gemm_us[i] * 1e-6) / 1e12
+        roofline = {"bound": "mfma", "kernel": "bf16 GEMM of the Q8_0 weight-only linear",
+                    "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                    "ops_per_launch": layers[i].ops, "avg_launch_us": round(float(gemm_us[i]), 2)}
     if dom is not None:
         lin = layers[dom]
         ach = lin.ops / (gemm_us[dom] * 1e-6) / 1e12
@@ -587,14 +618,16 @@ def main():
     cfg = {"workload": {"ffn_up": "DiT FFN up-projection 4608x4096->16384, one branch",
                         "ffn_down": "DiT FFN down-projection 4608x16384->4096, W8A8 and protected bf16",
                         "dit_block": "one DiT block (qkv, attn_out, ffn_up, ffn_down protected), both CFG branches",
-                        "backbone": "211 linears x 2 branches, 17 protected per branch"}[args.workload],
+                        "backbone": "211 linears x 2 branches, 17 protected per branch",
+                        "q8_0_ffn_up": "DiT FFN up-projection 4608x4096->16384 with GGUF Q8_0 weights"}[args.workload],
            "tokens": M0, "linears": len(layers), "protected": len(prot),
            "input_pool": args.pool if args.workload in ("ffn_up", "ffn_down") else None,
            "smoothquant_alpha": 0.5}
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TOPS", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int8",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if q8 and not w8 else "int8",
         "data": "synthetic", "config": cfg, "roofline": roofline, "cpu_baseline": cpu,
         "kernels": kernels, "ms_per_step_with_kernel_events": round(step_ms_ev, 4),
         "host_wall_ms_per_step": round(wall_ms, 4),

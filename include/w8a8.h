@@ -165,6 +165,37 @@ w8a8_status bf16_linear(const uint16_t *X, const uint16_t *W,
                         const uint16_t *bias, int64_t M, int64_t N, int64_t K,
                         uint16_t *Y, w8a8_stream stream);
 
+/* ---------------------------------------------------------------------- */
+/* GGUF Q8_0 weight-only (Section 3, "GGUF k-quants": 8.5 bits per weight, */
+/* round to nearest). A row of W [N][K] is cut into blocks of 32           */
+/* consecutive weights; a block keeps 32 int8 codes and a binary16 scale.  */
+/* Stored planar: qs [N][K] int8 and d [N][K/32] binary16 bits.            */
+/* ---------------------------------------------------------------------- */
+
+/* Encode, per block: amax = max |w|, d = RN16(min(RN32(amax / 127), 65504)),
+ * q = clamp(rint(w * RN32(1 / float(d))), -127, 127) (all 0 if d == 0), in
+ * binary32 with one rounding per operation. W [N][K] bf16 (16-byte aligned)
+ * -> qs [N][K] int8 (16-byte aligned), d [N][K/32] (2-byte aligned). Same N
+ * and K limits as w8a8_prepare_weight (K % 64 == 0). */
+w8a8_status q8_0_quantize(const uint16_t *W, int64_t N, int64_t K, int8_t *qs,
+                          uint16_t *d, w8a8_stream stream);
+
+/* Decode: W[n][k] = bf16_rne(float(d[n][k/32]) * qs[n][k]) (the product is
+ * exact in binary32). qs, d as above -> W [N][K] bf16 (16-byte aligned). */
+w8a8_status q8_0_dequantize(const int8_t *qs, const uint16_t *d, int64_t N,
+                            int64_t K, uint16_t *W, w8a8_stream stream);
+
+/* The weight-only linear: Y = bf16_linear(X, decode(qs, d), bias), i.e.
+ *   Y[t][n] = bf16_rne(sum_k X[t][k] * W'[n][k] + bias[n]), W' = decode(qs, d),
+ * bf16 products accumulated in binary32. The decoded weights go to `work`
+ * (caller-owned, 2 N K bytes, 16-byte aligned, overwritten): weights stay
+ * resident at 8.5 bits per weight and only the layer being run is decoded.
+ * X [M][K] bf16, bias [N] bf16 or NULL -> Y [M][N] bf16. Same limits as
+ * bf16_linear. */
+w8a8_status q8_0_linear(const uint16_t *X, const int8_t *qs, const uint16_t *d,
+                        const uint16_t *bias, int64_t M, int64_t N, int64_t K,
+                        uint16_t *work, uint16_t *Y, w8a8_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

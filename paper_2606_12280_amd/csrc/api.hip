@@ -207,4 +207,44 @@ w8a8_status bf16_linear(const uint16_t *X, const uint16_t *W, const uint16_t *bi
     return hip_status(w8a8::launch_gemm_bf16(X, W, bias, M, N, K, Y, as_stream(stream)));
 }
 
+w8a8_status q8_0_quantize(const uint16_t *W, int64_t N, int64_t K, int8_t *qs, uint16_t *d,
+                          w8a8_stream stream) {
+    if (W == nullptr || qs == nullptr || d == nullptr) return W8A8_ERR_NULL;
+    W8A8_TRY(check_rows(N, kMaxRows));
+    W8A8_TRY(check_k(K));
+    if (!aligned(W, 16) || !aligned(qs, 16) || !aligned(d, 2)) return W8A8_ERR_ALIGN;
+    W8A8_TRY(check_alias({{qs, N * K}, {d, N * (K / 32) * 2}}, {{W, 2 * N * K}}));
+    return hip_status(w8a8::launch_q8_0_quantize(W, N, K, qs, d, as_stream(stream)));
+}
+
+w8a8_status q8_0_dequantize(const int8_t *qs, const uint16_t *d, int64_t N, int64_t K,
+                            uint16_t *W, w8a8_stream stream) {
+    if (qs == nullptr || d == nullptr || W == nullptr) return W8A8_ERR_NULL;
+    W8A8_TRY(check_rows(N, kMaxRows));
+    W8A8_TRY(check_k(K));
+    if (!aligned(W, 16) || !aligned(qs, 16) || !aligned(d, 2)) return W8A8_ERR_ALIGN;
+    W8A8_TRY(check_alias({{W, 2 * N * K}}, {{qs, N * K}, {d, N * (K / 32) * 2}}));
+    return hip_status(w8a8::launch_q8_0_dequantize(qs, d, N, K, W, as_stream(stream)));
+}
+
+w8a8_status q8_0_linear(const uint16_t *X, const int8_t *qs, const uint16_t *d,
+                        const uint16_t *bias, int64_t M, int64_t N, int64_t K, uint16_t *work,
+                        uint16_t *Y, w8a8_stream stream) {
+    if (X == nullptr || qs == nullptr || d == nullptr || work == nullptr || Y == nullptr)
+        return W8A8_ERR_NULL;
+    W8A8_TRY(check_rows(M, kMaxRows));
+    W8A8_TRY(check_rows(N, kMaxN));
+    if (M * N > kMaxMN) return W8A8_ERR_SHAPE;
+    W8A8_TRY(check_k(K));
+    if (!aligned(X, 16) || !aligned(qs, 16) || !aligned(d, 2) || !aligned(work, 16) ||
+        !aligned(Y, 16) || !aligned(bias, 2))
+        return W8A8_ERR_ALIGN;
+    W8A8_TRY(check_alias({{work, 2 * N * K}, {Y, 2 * M * N}},
+                         {{X, 2 * M * K}, {qs, N * K}, {d, N * (K / 32) * 2},
+                          {bias, bias ? 2 * N : 0}}));
+    const hipStream_t s = as_stream(stream);
+    W8A8_TRY(hip_status(w8a8::launch_q8_0_dequantize(qs, d, N, K, work, s)));
+    return hip_status(w8a8::launch_gemm_bf16(X, work, bias, M, N, K, Y, s));
+}
+
 }  // extern "C"

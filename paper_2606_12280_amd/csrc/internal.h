@@ -30,6 +30,13 @@ constexpr int kMomentBlocks = 1024;
 hipError_t launch_act_moments(const uint16_t *X, int64_t n, double *work, double *stats,
                               hipStream_t stream);
 
+// GGUF Q8_0: codes qs [N][K] and binary16 scales d [N][K/32] of W [N][K]
+// bf16 (32 | K), and back to bf16(d * q).
+hipError_t launch_q8_0_quantize(const uint16_t *W, int64_t N, int64_t K, int8_t *qs,
+                                uint16_t *d, hipStream_t stream);
+hipError_t launch_q8_0_dequantize(const int8_t *qs, const uint16_t *d, int64_t N, int64_t K,
+                                  uint16_t *W, hipStream_t stream);
+
 // dst[k] = 0 for k < K (a fill kernel, so that the call can be captured).
 hipError_t launch_zero_f32(float *dst, int64_t K, hipStream_t stream);
 

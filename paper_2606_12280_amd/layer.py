@@ -1,7 +1,8 @@
-"""One linear of the DiT routed through the W8A8 recipe or the protected bf16
-path (paper Section 3: every linear is W8A8 except the top-N most fragile
-layers, N = 17 of 211 per branch, which stay bf16 with no activation
-quantization). Host-side bookkeeping only: the arithmetic runs in the
+"""One linear of the DiT routed through the W8A8 recipe, the protected bf16
+path, or the GGUF Q8_0 weight-only format (paper Section 3: every linear is
+W8A8 except the top-N most fragile layers, N = 17 of 211 per branch, which
+stay bf16 with no activation quantization; independently, a checkpoint can
+be stored as Q8_0). Host-side bookkeeping only: the arithmetic runs in the
 library's kernels through ops."""
 from __future__ import annotations
 
@@ -23,9 +24,15 @@ class PreparedLinear:
     Wq: torch.Tensor | None = None           # int8 [N, K]
     w_scale: torch.Tensor | None = None      # fp32 [N]
     inv_lambda: torch.Tensor | None = None   # fp32 [K]
+    q8_qs: torch.Tensor | None = None        # int8 [N, K], Q8_0 layers only
+    q8_d: torch.Tensor | None = None         # fp16 [N, K/32]
+
+    @property
+    def q8_0(self) -> bool:
+        return self.q8_qs is not None
 
     def nbytes(self) -> int:
-        ts = [self.W, self.Wq, self.w_scale, self.inv_lambda, self.bias]
+        ts = [self.W, self.Wq, self.w_scale, self.inv_lambda, self.bias, self.q8_qs, self.q8_d]
         return sum(t.numel() * t.element_size() for t in ts if t is not None)
 
 
@@ -42,14 +49,28 @@ def prepare_linear(W: torch.Tensor, bias: torch.Tensor | None, lam: torch.Tensor
     return PreparedLinear(False, N, K, bias, Wq=Wq, w_scale=ws, inv_lambda=il)
 
 
+def prepare_q8_0(W: torch.Tensor, bias: torch.Tensor | None) -> PreparedLinear:
+    """Encode W once (offline) as GGUF Q8_0: 8.5 bits per weight."""
+    N, K = W.shape
+    qs, d = ops.q8_0_quantize(W)
+    return PreparedLinear(False, N, K, bias, q8_qs=qs, q8_d=d)
+
+
 class Workspace:
-    """Reusable activation buffers (Xq, x_scale) so that a forward allocates
-    nothing once the largest shape has been seen."""
+    """Reusable buffers (Xq, x_scale, and the decoded bf16 weights of a Q8_0
+    layer) so that a forward allocates nothing once the largest shape has
+    been seen."""
 
     def __init__(self, device):
         self.device = device
         self._xq = None
         self._xs = None
+        self._wd = None
+
+    def weights(self, N: int, K: int) -> torch.Tensor:
+        if self._wd is None or self._wd.numel() < N * K:
+            self._wd = torch.empty(N * K, dtype=torch.bfloat16, device=self.device)
+        return self._wd[: N * K].view(N, K)
 
     def get(self, M: int, K: int):
         need = M * K
@@ -62,9 +83,13 @@ class Workspace:
 
 def route(layer: PreparedLinear, X: torch.Tensor, out: torch.Tensor | None = None,
           ws: Workspace | None = None) -> torch.Tensor:
-    """Y = layer(X): bf16_linear for a protected layer, else quant + W8A8 GEMM."""
+    """Y = layer(X): bf16_linear for a protected layer, the weight-only
+    linear for a Q8_0 layer, else quant + W8A8 GEMM."""
     if layer.protected:
         return ops.bf16_linear(X, layer.W, layer.bias, out=out)
+    if layer.q8_0:
+        work = ws.weights(layer.N, layer.K) if ws is not None else None
+        return ops.q8_0_linear(X, layer.q8_qs, layer.q8_d, layer.bias, work=work, out=out)
     M = X.shape[0]
     if ws is None:
         Xq = x_scale = None

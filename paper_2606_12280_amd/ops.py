@@ -189,3 +189,64 @@ def bf16_linear(X: torch.Tensor, W: torch.Tensor, bias: torch.Tensor | None = No
         check("bf16_linear",
               lib.bf16_linear(_ptr(X), _ptr(W), _ptr(bias), M, N, K, _ptr(Y), _stream(X.device)))
     return Y
+
+
+# --------------------------------------------------------------------------
+# GGUF Q8_0 weight-only
+# --------------------------------------------------------------------------
+
+Q8_0_BLOCK = 32
+
+
+def q8_0_quantize(W: torch.Tensor) -> tuple[torch.Tensor, torch.Tensor]:
+    """W [N, K] bf16 -> (codes int8 [N, K], scales float16 [N, K/32])."""
+    _need(W, "W", torch.bfloat16, 2)
+    N, K = W.shape
+    qs = torch.empty(N, K, dtype=torch.int8, device=W.device)
+    d = torch.empty(N, K // Q8_0_BLOCK, dtype=torch.float16, device=W.device)
+    lib = load()
+    with torch.cuda.device(W.device):
+        check("q8_0_quantize", lib.q8_0_quantize(_ptr(W), N, K, _ptr(qs), _ptr(d),
+                                                 _stream(W.device)))
+    return qs, d
+
+
+def q8_0_dequantize(qs: torch.Tensor, d: torch.Tensor,
+                    out: torch.Tensor | None = None) -> torch.Tensor:
+    """bf16(d * q) as bf16 [N, K]."""
+    _need(qs, "qs", torch.int8, 2)
+    N, K = qs.shape
+    _need(d, "d", torch.float16, 2, qs.device)
+    if tuple(d.shape) != (N, K // Q8_0_BLOCK):
+        raise ValueError("d must be [N, K/32]")
+    W = _out(out, (N, K), torch.bfloat16, qs.device, "out")
+    lib = load()
+    with torch.cuda.device(qs.device):
+        check("q8_0_dequantize", lib.q8_0_dequantize(_ptr(qs), _ptr(d), N, K, _ptr(W),
+                                                     _stream(qs.device)))
+    return W
+
+
+def q8_0_linear(X: torch.Tensor, qs: torch.Tensor, d: torch.Tensor,
+                bias: torch.Tensor | None = None, work: torch.Tensor | None = None,
+                out: torch.Tensor | None = None) -> torch.Tensor:
+    """Y = X W'^T + bias with W' = bf16(d * q) decoded into `work` (bf16
+    [N, K], allocated if not given)."""
+    _need(X, "X", torch.bfloat16, 2)
+    M, K = X.shape
+    _need(qs, "qs", torch.int8, 2, X.device)
+    N = qs.shape[0]
+    if qs.shape[1] != K:
+        raise ValueError("qs must be [N, K]")
+    _need(d, "d", torch.float16, 2, X.device)
+    if tuple(d.shape) != (N, K // Q8_0_BLOCK):
+        raise ValueError("d must be [N, K/32]")
+    if bias is not None:
+        _need(bias, "bias", torch.bfloat16, 1, X.device)
+    work = _out(work, (N, K), torch.bfloat16, X.device, "work")
+    Y = _out(out, (M, N), torch.bfloat16, X.device, "out")
+    lib = load()
+    with torch.cuda.device(X.device):
+        check("q8_0_linear", lib.q8_0_linear(_ptr(X), _ptr(qs), _ptr(d), _ptr(bias), M, N, K,
+                                             _ptr(work), _ptr(Y), _stream(X.device)))
+    return Y

@@ -123,6 +123,29 @@ def test_moments_validation(lib):
     assert _lib.MOMENTS_WORK_BYTES == (2 * 1024 + 2) * 8
 
 
+def test_q8_0_validation(lib):
+    q = lib.q8_0_quantize
+    assert q(None, 8, 64, B, C, None) == NULL
+    assert q(A, 0, 64, B, C, None) == SHAPE
+    assert q(A, 8, 32, B, C, None) == UNSUP             # K % 64 != 0
+    assert q(A + 2, 8, 64, B, C, None) == ALIGN
+    assert q(A, 8, 64, B + 8, C, None) == ALIGN
+    assert q(A, 8, 64, B, C + 1, None) == ALIGN
+    assert q(A, 8, 64, A + 64, C, None) == ALIAS        # codes inside W
+    assert q(A, 8, 64, B, B + 256, None) == ALIAS       # scales inside the codes
+    dq = lib.q8_0_dequantize
+    assert dq(A, B, 8, 64, None, None) == NULL
+    assert dq(A, B, 8, 64, A, None) == ALIAS
+    assert dq(A, B, 8, 64, C + 8, None) == ALIGN
+    f = lib.q8_0_linear
+    assert f(A, B, C, None, 4, 8, 64, D, None, None) == NULL
+    assert f(A, B, C, None, 4, 8, 64, None, E, None) == NULL
+    assert f(A, B, C, None, 4, 8, 64, D, D, None) == ALIAS          # Y inside work
+    assert f(A, B, C, None, 4, 8, 64, B, E, None) == ALIAS          # work over the codes
+    assert f(A, B, C, None, 4, 8, 64, D + 8, E, None) == ALIGN
+    assert f(A, B, C, None, 4, 8, 96, D, E, None) == UNSUP
+
+
 def test_binding_rejects_host_tensors():
     X = torch.zeros(4, 64, dtype=torch.bfloat16)
     il = torch.ones(64)

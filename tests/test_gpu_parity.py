@@ -419,3 +419,71 @@ def test_full_size_dit_block(branch):
             acc = oracle.gemm_i32(Xq_ref, Wq_ref, len(rows), N, K)
             Y_ref = oracle.epilogue(acc, xs_ref, ws_ref, c["bias"], len(rows), N)
             check_w8a8_output(Y[rows], Y_ref, acc, xs_ref, ws_ref, c["bias"])
+
+
+# --------------------------------------------------------------------------
+# GGUF Q8_0 weight-only (Section 3, "GGUF k-quants")
+# --------------------------------------------------------------------------
+
+def _q8_case(seed, N, K):
+    W = synth.rand_bf16(seed, (N, K), 0.02)
+    if N > 1 and K >= 128:                      # a zero block and a large one
+        W[0, :32] = 0
+        W[1, 64:96] = synth.rand_bf16([seed, 1], (32,), 40.0)
+    return W
+
+
+@pytest.mark.parametrize("N,K", [(1, 64), (7, 256), (33, 1088), (512, 4096)])
+def test_q8_0_codes_scales_and_decode_bit_exact(N, K):
+    W = _q8_case([150, N, K], N, K)
+    qs_ref, d_ref = oracle.q8_0_quantize(W, N, K)
+    qs, d = ops.q8_0_quantize(dev_bf16(W))
+    assert np.array_equal(host(qs), qs_ref)
+    assert np.array_equal(host(d).view(np.uint16), d_ref)
+    Wd = ops.q8_0_dequantize(qs, d)
+    assert np.array_equal(host_bits(Wd), oracle.q8_0_dequantize(qs_ref, d_ref, N, K))
+
+
+def test_q8_0_special_blocks_on_gpu():
+    """Zero, underflowing (scale 0) and capped (scale 65504, codes clamp)
+    blocks, and round-half-even ties with scale 1."""
+    W = np.zeros((2, 128), np.float32)
+    W[0, 32:64] = 2.0 ** -30
+    W[0, 64] = 9.0e6
+    W[0, 65] = -1.0e6
+    W[1, :8] = [127.0, 0.5, -0.5, 1.5, 2.5, -2.5, 3.5, 126.5]
+    B = synth.to_bf16_bits(W)
+    qs_ref, d_ref = oracle.q8_0_quantize(B, 2, 128)
+    qs, d = ops.q8_0_quantize(dev_bf16(B))
+    assert np.array_equal(host(qs), qs_ref)
+    assert np.array_equal(host(d).view(np.uint16), d_ref)
+    assert list(host(qs)[1, :8]) == [127, 0, 0, 2, 2, -2, 4, 126]
+
+
+@pytest.mark.parametrize("M,N,K", [(64, 512, 256), (257, 129, 192), (300, 520, 1088)])
+def test_q8_0_linear(M, N, K):
+    c = synth.linear_case([151, M, N, K], M, N, K, act="gelu")
+    qs_ref, d_ref = oracle.q8_0_quantize(c["W"], N, K)
+    Wd = oracle.q8_0_dequantize(qs_ref, d_ref, N, K)
+    qs, d = ops.q8_0_quantize(dev_bf16(c["W"]))
+    Y = host_bits(ops.q8_0_linear(dev_bf16(c["X"]), qs, d, dev_bf16(c["bias"])))
+    check_bf16_output(Y, c["X"].reshape(M, K), Wd, c["bias"])
+    ref = oracle.q8_0_linear(c["X"], qs_ref, d_ref, c["bias"], M, N, K)
+    from bf16ref import ulp_distance
+    assert (ulp_distance(Y, ref) <= 1).mean() > 0.999
+
+
+def test_q8_0_full_size_ffn_up():
+    """FFN up weights 16384 x 4096: codes and scales bit-exact on the whole
+    tensor; the linear on 24 sampled token rows."""
+    c = synth.ffn_up_case()
+    M, N, K = c["M"], c["N"], c["K"]
+    qs_ref, d_ref = oracle.q8_0_quantize(c["W"], N, K)
+    qs, d = ops.q8_0_quantize(dev_bf16(c["W"]))
+    assert np.array_equal(host(qs), qs_ref)
+    assert np.array_equal(host(d).view(np.uint16), d_ref)
+    X = c["X"].reshape(M, K)
+    Y = host_bits(ops.q8_0_linear(dev_bf16(X), qs, d, dev_bf16(c["bias"])))
+    rows = np.random.default_rng(152).choice(M, 24, replace=False)
+    Wd = oracle.q8_0_dequantize(qs_ref, d_ref, N, K)
+    check_bf16_output(Y[rows], X[rows], Wd, c["bias"])

@@ -73,6 +73,8 @@ def _load():
         "oracle_half_to_float": ([ctypes.c_uint16], ctypes.c_float),
         "oracle_q8_0_quantize": ([P, I64, I64, P, P], None),
         "oracle_q8_0_dequantize": ([P, P, I64, I64, P], None),
+        "oracle_q4_k_quantize": ([P, I64, I64, P, P, P, P, P], None),
+        "oracle_q4_k_dequantize": ([P, P, P, P, P, I64, I64, P], None),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -301,3 +303,37 @@ def q8_0_linear(X, qs, d, bias, M: int, N: int, K: int) -> np.ndarray:
     """The weight-only linear: bf16 X times the dequantized weights (the
     protected-layer arithmetic on bf16(d * q))."""
     return bf16_linear(X, q8_0_dequantize(qs, d, N, K), bias, M, N, K)
+
+
+Q4_K_SUPER = 256
+Q4_K_SUB = 32
+
+
+def q4_k_quantize(W, N: int, K: int):
+    """W [N][K] bf16 bits -> dict of the Q4_K planes: qs uint8 [N][K/2] (two
+    4-bit codes per byte, even k low), sc and mn uint8 [N][K/32], d and dmin
+    binary16 bits [N][K/256]."""
+    W = _c(W, np.uint16)
+    qs = np.zeros(N * K // 2, np.uint8)
+    sc = np.zeros(N * (K // Q4_K_SUB), np.uint8)
+    mn = np.zeros(N * (K // Q4_K_SUB), np.uint8)
+    d = np.zeros(N * (K // Q4_K_SUPER), np.uint16)
+    dmin = np.zeros(N * (K // Q4_K_SUPER), np.uint16)
+    _load().oracle_q4_k_quantize(_p(W), N, K, _p(qs), _p(sc), _p(mn), _p(d), _p(dmin))
+    return {"qs": qs.reshape(N, K // 2), "sc": sc.reshape(N, K // Q4_K_SUB),
+            "mn": mn.reshape(N, K // Q4_K_SUB), "d": d.reshape(N, K // Q4_K_SUPER),
+            "dmin": dmin.reshape(N, K // Q4_K_SUPER)}
+
+
+def q4_k_dequantize(q, N: int, K: int) -> np.ndarray:
+    """bf16 bits [N][K] of bf16(RN32(d * sc * code - dmin * mn))."""
+    planes = [_c(q["qs"], np.uint8), _c(q["sc"], np.uint8), _c(q["mn"], np.uint8),
+              _c(q["d"], np.uint16), _c(q["dmin"], np.uint16)]
+    W = np.zeros(N * K, np.uint16)
+    _load().oracle_q4_k_dequantize(*[_p(a) for a in planes], N, K, _p(W))
+    return W.reshape(N, K)
+
+
+def q4_k_linear(X, q, bias, M: int, N: int, K: int) -> np.ndarray:
+    """The weight-only linear on the decoded Q4_K weights."""
+    return bf16_linear(X, q4_k_dequantize(q, N, K), bias, M, N, K)

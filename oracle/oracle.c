@@ -41,7 +41,12 @@
  *   - GGUF Q8_0 (Section 3, "GGUF k-quants"): blocks of 32 consecutive
  *     weights of a row; d = RN16(min(RN32(amax / 127), 65504)), codes
  *     clamp(rint(w * RN32(1 / d)), -127, 127) with the stored d (all zero when
- *     d is 0); a weight reads back as bf16(d * q).
+ *     d is 0); a weight reads back as bf16(d * q);
+ *   - GGUF Q4_K (same passage; the paper's encoder is its own and is not
+ *     spelled out): round to nearest on a min-max grid per sub-block of 32,
+ *     6-bit sub-block scales and offsets against binary16 super-block scales
+ *     (256 weights), 4-bit codes against the stored grid; a weight reads
+ *     back as bf16(RN32(d*sc*q - dmin*m)).
  *
  * Parallelism: rows are independent and each row is computed by one thread in
  * a fixed order, so results do not depend on the thread count.
@@ -478,6 +483,126 @@ void oracle_q8_0_dequantize(const int8_t *qs, const uint16_t *d, int64_t N, int6
         for (k = 0; k < K; ++k) {
             float v = half_to_float(d[n * (K / ORACLE_Q8_0_BLOCK) + k / ORACLE_Q8_0_BLOCK]) *
                       (float)qs[n * K + k];
+            W[n * K + k] = double_to_bf16((double)v);
+        }
+}
+
+/* ------------------------------------------------------------------ */
+/* GGUF Q4_K weight-only format (Section 3, "GGUF k-quants": 4-bit      */
+/* codes in super-blocks, the paper's own super-block quantizer).        */
+/* A super-block is 256 consecutive weights of a row, cut into 8         */
+/* sub-blocks of 32. A sub-block j reads back as                          */
+/*   w = d * sc_j * q - dmin * m_j,  q in [0, 15], sc_j and m_j in [0, 63] */
+/* with d and dmin binary16 per super-block. Stored planar:               */
+/*   qs [N][K/2] (k even in the low nibble), sc and mn [N][K/32] bytes,    */
+/*   d and dmin [N][K/256] binary16 bits.                                 */
+/* ------------------------------------------------------------------ */
+
+#define ORACLE_Q4_K_SUPER 256
+#define ORACLE_Q4_K_SUB 32
+
+static float cap_half(float v) { return v > ORACLE_HALF_MAX ? ORACLE_HALF_MAX : v; }
+
+/* Round-to-nearest quantizer of one super-block, in three steps (binary32,
+ * one rounding per operation):
+ *   1. each sub-block's range: lo = min(0, min w), hi = max w,
+ *      a_j = (hi - lo) / 15 (the step that spans it with 16 codes), b_j = -lo;
+ *   2. the super-block scales: d = RN16(min(max_j a_j / 63, 65504)),
+ *      dmin = RN16(min(max_j b_j / 63, 65504)); then the 6-bit sub-block
+ *      scales sc_j = min(rint(a_j * RN32(1/d)), 63), m_j = min(rint(b_j * RN32(1/dmin)), 63)
+ *      against the stored d and dmin (0 where d or dmin is 0);
+ *   3. the codes against the stored grid: with s_j = d * sc_j and
+ *      o_j = dmin * m_j (both exact), q = clamp(rint((w + o_j) * RN32(1/s_j)), 0, 15),
+ *      q = 0 where s_j = 0. */
+static void q4_k_super_block(const uint16_t *w, uint8_t *codes, uint8_t *sc, uint8_t *mn,
+                             uint16_t *d, uint16_t *dmin)
+{
+    float a[8], b[8], amax = 0.0f, bmax = 0.0f, fd, fdm, inv_d, inv_dm;
+    int j, i;
+    for (j = 0; j < 8; ++j) {
+        float lo = 0.0f, hi = -INFINITY;
+        for (i = 0; i < ORACLE_Q4_K_SUB; ++i) {
+            float v = bf16_to_float(w[j * ORACLE_Q4_K_SUB + i]);
+            if (v < lo)
+                lo = v;
+            if (v > hi)
+                hi = v;
+        }
+        a[j] = (hi - lo) / 15.0f;
+        b[j] = -lo;
+        if (a[j] > amax)
+            amax = a[j];
+        if (b[j] > bmax)
+            bmax = b[j];
+    }
+    *d = float_to_half(cap_half(amax / 63.0f));
+    *dmin = float_to_half(cap_half(bmax / 63.0f));
+    fd = half_to_float(*d);
+    fdm = half_to_float(*dmin);
+    inv_d = fd != 0.0f ? 1.0f / fd : 0.0f;
+    inv_dm = fdm != 0.0f ? 1.0f / fdm : 0.0f;
+    for (j = 0; j < 8; ++j) {
+        float cs = rintf(a[j] * inv_d), cm = rintf(b[j] * inv_dm), s, o, inv;
+        if (cs > 63.0f)
+            cs = 63.0f;
+        if (cm > 63.0f)
+            cm = 63.0f;
+        sc[j] = (uint8_t)cs;
+        mn[j] = (uint8_t)cm;
+        s = fd * cs;
+        o = fdm * cm;
+        inv = s != 0.0f ? 1.0f / s : 0.0f;
+        for (i = 0; i < ORACLE_Q4_K_SUB; ++i) {
+            float c = rintf((bf16_to_float(w[j * ORACLE_Q4_K_SUB + i]) + o) * inv);
+            if (c > 15.0f)
+                c = 15.0f;
+            if (c < 0.0f)
+                c = 0.0f;
+            codes[j * ORACLE_Q4_K_SUB + i] = (uint8_t)c;
+        }
+    }
+}
+
+/* W [N][K] bf16 (K a multiple of 256) -> qs [N][K/2], sc, mn [N][K/32],
+ * d, dmin [N][K/256]. */
+void oracle_q4_k_quantize(const uint16_t *W, int64_t N, int64_t K, uint8_t *qs, uint8_t *sc,
+                          uint8_t *mn, uint16_t *d, uint16_t *dmin)
+{
+    int64_t n;
+#pragma omp parallel for schedule(static)
+    for (n = 0; n < N; ++n) {
+        int64_t sb, k;
+        uint8_t codes[ORACLE_Q4_K_SUPER];
+        for (sb = 0; sb < K / ORACLE_Q4_K_SUPER; ++sb) {
+            const int64_t sub = n * (K / ORACLE_Q4_K_SUB) + sb * 8;
+            const int64_t sup = n * (K / ORACLE_Q4_K_SUPER) + sb;
+            q4_k_super_block(W + n * K + sb * ORACLE_Q4_K_SUPER, codes, sc + sub, mn + sub,
+                             d + sup, dmin + sup);
+            for (k = 0; k < ORACLE_Q4_K_SUPER; k += 2)
+                qs[(n * K + sb * ORACLE_Q4_K_SUPER + k) / 2] =
+                    (uint8_t)(codes[k] | (codes[k + 1] << 4));
+        }
+    }
+}
+
+/* W'[n][k] = bf16(RN32(d * sc_j * q - dmin * m_j)): d * sc_j * q (at most
+ * 11 + 6 + 4 significant bits) and dmin * m_j are exact in binary32, their
+ * difference is rounded once to binary32, then to bf16. */
+void oracle_q4_k_dequantize(const uint8_t *qs, const uint8_t *sc, const uint8_t *mn,
+                            const uint16_t *d, const uint16_t *dmin, int64_t N, int64_t K,
+                            uint16_t *W)
+{
+    int64_t n, k;
+#pragma omp parallel for schedule(static) private(k)
+    for (n = 0; n < N; ++n)
+        for (k = 0; k < K; ++k) {
+            const int64_t j = n * (K / ORACLE_Q4_K_SUB) + k / ORACLE_Q4_K_SUB;
+            const int64_t t = n * (K / ORACLE_Q4_K_SUPER) + k / ORACLE_Q4_K_SUPER;
+            const uint8_t byte = qs[(n * K + k) / 2];
+            const float q = (float)((k & 1) ? byte >> 4 : byte & 15);
+            const float s = half_to_float(d[t]) * (float)sc[j];
+            const float o = half_to_float(dmin[t]) * (float)mn[j];
+            const float v = s * q - o;
             W[n * K + k] = double_to_bf16((double)v);
         }
 }

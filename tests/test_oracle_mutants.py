@@ -58,6 +58,18 @@ MUTANTS = {
     "q8_0_no_scale_cap": ("            if (s > ORACLE_HALF_MAX)\n                s = ORACLE_HALF_MAX;\n", ""),
     "q8_0_dequant_drops_scale": ("float v = half_to_float(d[n * (K / ORACLE_Q8_0_BLOCK) + k / ORACLE_Q8_0_BLOCK]) *\n                      (float)qs[n * K + k];",
                                  "float v = (float)qs[n * K + k];"),
+    "q4_k_nibbles_swapped": ("(uint8_t)(codes[k] | (codes[k + 1] << 4));", "(uint8_t)(codes[k + 1] | (codes[k] << 4));"),
+    "q4_k_offset_sign": ("float c = rintf((bf16_to_float(w[j * ORACLE_Q4_K_SUB + i]) + o) * inv);",
+                         "float c = rintf((bf16_to_float(w[j * ORACLE_Q4_K_SUB + i]) - o) * inv);"),
+    "q4_k_codes_from_unrounded_step": ("inv = s != 0.0f ? 1.0f / s : 0.0f;\n        for (i = 0;",
+                                       "inv = a[j] != 0.0f ? 1.0f / a[j] : 0.0f;\n        for (i = 0;"),
+    "q4_k_scale_floor": ("float cs = rintf(a[j] * inv_d)", "float cs = floorf(a[j] * inv_d)"),
+    "q4_k_offset_floor": ("cm = rintf(b[j] * inv_dm)", "cm = floorf(b[j] * inv_dm)"),
+    "q4_k_super_scale_over_64": ("*d = float_to_half(cap_half(amax / 63.0f));", "*d = float_to_half(cap_half(amax / 64.0f));"),
+    "q4_k_step_over_16": ("a[j] = (hi - lo) / 15.0f;", "a[j] = (hi - lo) / 16.0f;"),
+    "q4_k_min_not_clamped_to_zero": ("float lo = 0.0f, hi = -INFINITY;", "float lo = INFINITY, hi = -INFINITY;"),
+    "q4_k_decode_drops_offset": ("const float v = s * q - o;", "const float v = s * q;"),
+    "q4_k_no_code_clamp": ("            if (c > 15.0f)\n                c = 15.0f;\n", ""),
     "moments_drops_last_row": ("    for (t = 0; t < M; ++t) {\n        s2 += r2[t];",
                                "    for (t = 0; t + 1 < M; ++t) {\n        s2 += r2[t];"),
 }
@@ -90,6 +102,12 @@ PINS = [
     pins.test_q8_0_exact_grid_and_ties,
     pins.test_q8_0_special_blocks,
     pins.test_q8_0_dequantize_is_one_rounding,
+    pins.test_q4_k_exact_grid_round_trip,
+    pins.test_q4_k_codes_are_nearest_on_the_stored_grid,
+    pins.test_q4_k_error_bound_and_scale_ranges,
+    pins.test_q4_k_grid_spans_each_sub_block,
+    pins.test_q4_k_special_blocks,
+    pins.test_q4_k_dequantize_is_binary32_then_bf16,
 ]
 
 

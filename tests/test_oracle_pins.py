@@ -593,3 +593,189 @@ def test_q8_0_linear_against_numpy_fp64():
     Wf = bf16_to_f64(c["W"]).reshape(40, 8, 32)
     step = _f16(d).astype(np.float64)[..., None]
     assert np.all(np.abs(bf16_to_f64(Wd).reshape(40, 8, 32) - Wf) <= step * 0.5 + np.abs(Wf) * 2.0 ** -8)
+
+
+# --------------------------------------------------------------------------
+# GGUF Q4_K weight-only (Section 3, "GGUF k-quants": 4-bit codes in
+# super-blocks of 256 weights, 8 sub-blocks of 32 with 6-bit scales and
+# offsets under binary16 super-block scales)
+# --------------------------------------------------------------------------
+
+def _q4_k_grid(q, N, K):
+    """Per-weight step s = d*sc and offset o = dmin*mn, and the codes, as
+    float64 arrays [N][K] (from the stored planes, not from the weights)."""
+    rep_sub = lambda a: np.repeat(a.astype(np.float64), 32, axis=1)
+    rep_sup = lambda a: np.repeat(_f16(a).astype(np.float64), 256, axis=1)
+    s = rep_sup(q["d"]) * rep_sub(q["sc"])
+    o = rep_sup(q["dmin"]) * rep_sub(q["mn"])
+    codes = np.empty((N, K), np.float64)
+    codes[:, 0::2] = q["qs"] & 15
+    codes[:, 1::2] = q["qs"] >> 4
+    return s, o, codes
+
+
+def _bf16_exact(v) -> bool:
+    return float(bf16_to_f64(synth.to_bf16_bits(np.array([v], np.float32)))[0]) == v
+
+
+def test_q4_k_exact_grid_round_trip():
+    """Weights built as d*sc*q - dmin*m from chosen d = dmin = 2^-8, 6-bit
+    sc and m (63 reached by both in every super-block) and 4-bit q (0 and
+    15 reached in every sub-block), all exactly representable in bf16: the
+    quantizer must give back exactly those planes and the decoder exactly
+    those weights. Catches a wrong step (/15), a wrong super-scale (/63), a
+    lost or sign-flipped offset, and swapped nibbles."""
+    rng = np.random.default_rng(150)
+    N, K = 6, 512
+    h = 2.0 ** -8
+    W = np.zeros((N, K), np.float32)
+    want_sc = np.zeros((N, K // 32), np.uint8)
+    want_mn = np.zeros((N, K // 32), np.uint8)
+    want_q = np.zeros((N, K), np.uint8)
+    for n in range(N):
+        for sb in range(K // 256):
+            j63, m63 = rng.choice(8, 2, replace=False)
+            for j in range(8):
+                while True:
+                    sc = 63 if j == j63 else int(rng.integers(1, 64))
+                    m = 63 if j == m63 else int(rng.integers(0, 64))
+                    ok = [c for c in range(16) if _bf16_exact(h * (sc * c - m))]
+                    if 0 in ok and 15 in ok and len(ok) >= 4:
+                        break
+                codes = rng.choice(ok, 32)
+                codes[rng.choice(32, 2, replace=False)] = [0, 15]
+                col = sb * 256 + j * 32
+                W[n, col:col + 32] = h * (sc * codes - m)
+                want_sc[n, col // 32], want_mn[n, col // 32] = sc, m
+                want_q[n, col:col + 32] = codes
+    B = synth.to_bf16_bits(W)
+    assert np.array_equal(bf16_to_f64(B).reshape(N, K), W.astype(np.float64))
+    q = oracle.q4_k_quantize(B, N, K)
+    assert np.all(_f16(q["d"]) == h) and np.all(_f16(q["dmin"]) == h)
+    assert np.array_equal(q["sc"], want_sc) and np.array_equal(q["mn"], want_mn)
+    assert np.array_equal(q["qs"], (want_q[:, 0::2] | (want_q[:, 1::2] << 4)).astype(np.uint8))
+    assert np.array_equal(oracle.q4_k_dequantize(q, N, K), B)
+
+
+def _q4_k_random_weights(seed, N, K):
+    rng = np.random.default_rng(seed)
+    W = rng.normal(0, 0.02, (N, K)).astype(np.float32)
+    W[:, rng.choice(K, K // 64, replace=False)] *= 12        # outlier channels
+    W[: N // 4] += 0.01                                       # rows with a mean offset
+    W[N // 4: N // 2] = np.abs(W[N // 4: N // 2])             # all-positive rows
+    return synth.to_bf16_bits(W)
+
+
+def test_q4_k_codes_are_nearest_on_the_stored_grid():
+    """Brute force over the 16 codes: each stored code is a nearest grid point
+    s*q - o of the stored grid (up to the binary32 rounding of (w + o)/s).
+    Catches codes taken from the unrounded sub-block step, a wrong clamp
+    range, and a flipped offset."""
+    N, K = 64, 1024
+    B = _q4_k_random_weights(151, N, K)
+    q = oracle.q4_k_quantize(B, N, K)
+    s, o, codes = _q4_k_grid(q, N, K)
+    w = bf16_to_f64(B).reshape(N, K)
+    err = np.abs(s * codes - o - w)
+    best = np.min(np.abs(s[..., None] * np.arange(16.0) - o[..., None] - w[..., None]), axis=2)
+    assert np.all(err <= best + s * 2.0 ** -20 + 1e-30)
+    assert codes.max() == 15 and codes.min() == 0
+
+
+def test_q4_k_error_bound_and_scale_ranges():
+    """Every weight reads back within half a step plus what rounding the
+    sub-block step to 6 bits of d can clip (15 * d/2) and what rounding the
+    offset can shift (dmin/2), plus the bf16 rounding of the read-back
+    value; 6-bit planes stay in [0, 63] and reach 62 or 63 in every
+    super-block (d is max step / 63 up to binary16 rounding). Catches a
+    floor in place of round-to-nearest for the 6-bit scales and offsets."""
+    N, K = 64, 1024
+    B = _q4_k_random_weights(152, N, K)
+    q = oracle.q4_k_quantize(B, N, K)
+    s, o, _ = _q4_k_grid(q, N, K)
+    w = bf16_to_f64(B).reshape(N, K)
+    r = bf16_to_f64(oracle.q4_k_dequantize(q, N, K)).reshape(N, K)
+    d = np.repeat(_f16(q["d"]).astype(np.float64), 256, axis=1)
+    dm = np.repeat(_f16(q["dmin"]).astype(np.float64), 256, axis=1)
+    bound = s / 2 + 7.5 * d + dm / 2 + np.abs(r) * 2.0 ** -8
+    assert np.all(np.abs(r - w) <= bound * (1 + 2.0 ** -12))
+    for plane in (q["sc"], q["mn"]):
+        assert plane.max() <= 63
+    tops = q["sc"].reshape(N, K // 256, 8).max(axis=2)
+    assert np.all((tops == 63) | (tops == 62))
+    # the all-positive rows need no offset: every sub-block minimum is >= 0
+    assert not q["mn"][N // 4: N // 2].any() and not q["dmin"][N // 4: N // 2].any()
+
+
+def test_q4_k_grid_spans_each_sub_block():
+    """The stored grid reproduces each sub-block's span: its lowest point
+    -dmin*m lies within dmin/2 of min(0, min w), its step d*sc within d/2 of
+    (max w - min(0, min w)) / 15 (where the 6-bit values are below 63), and
+    the largest step equals 63 d to binary16 precision. Catches rounding the
+    6-bit offsets or scales down instead of to nearest."""
+    N, K = 64, 1024
+    B = _q4_k_random_weights(155, N, K)
+    q = oracle.q4_k_quantize(B, N, K)
+    w = bf16_to_f64(B).reshape(N, K // 32, 32)
+    lo = np.minimum(w.min(axis=2), 0.0)
+    span = (w.max(axis=2) - lo) / 15
+    d = np.repeat(_f16(q["d"]).astype(np.float64), 8, axis=1)
+    dm = np.repeat(_f16(q["dmin"]).astype(np.float64), 8, axis=1)
+    tol = 1 + 2.0 ** -10
+    ok_m = q["mn"] < 63
+    assert np.all(np.abs(-dm * q["mn"] - lo)[ok_m] <= (dm / 2 * tol)[ok_m])
+    ok_s = q["sc"] < 63
+    assert np.all(np.abs(d * q["sc"] - span)[ok_s] <= (d / 2 * tol)[ok_s])
+    top = span.reshape(N, K // 256, 8).max(axis=2)
+    assert np.allclose(63 * _f16(q["d"]).astype(np.float64), top, rtol=2.0 ** -10)
+
+
+def test_q4_k_special_blocks():
+    """A zero super-block (all planes 0, reads back 0); a constant negative
+    sub-block (step 0, codes 0, read back as -dmin*m); a super-block whose
+    step caps d at 65504 (codes clamp at 15 and 0)."""
+    W = np.zeros((1, 768), np.float32)
+    W[0, 256:288] = -0.75
+    W[0, 288:512] = np.linspace(-0.5, 0.5, 224)
+    W[0, 512] = 3.0e9
+    W[0, 513] = -1.0e6
+    B = synth.to_bf16_bits(W)
+    q = oracle.q4_k_quantize(B, 1, 768)
+    r = bf16_to_f64(oracle.q4_k_dequantize(q, 1, 768))[0]
+    assert q["d"][0, 0] == 0 and q["dmin"][0, 0] == 0
+    assert not q["sc"][0, :8].any() and not q["mn"][0, :8].any() and not q["qs"][0, :128].any()
+    assert not r[:256].any()
+    assert q["sc"][0, 8] == 0 and not q["qs"][0, 128:144].any()
+    assert abs(r[256] + 0.75) <= float(_f16(q["dmin"])[0, 1]) / 2
+    assert _f16(q["d"])[0, 2] == 65504.0 and q["sc"][0, 16] == 63
+    assert (q["qs"][0, 256] & 15) == 15 and (q["qs"][0, 256] >> 4) == 0
+
+
+def test_q4_k_dequantize_is_binary32_then_bf16():
+    """Read-back against torch's own conversions of the exact value
+    d*sc*q - dmin*m (exact in binary64): binary64 -> binary32 -> bf16."""
+    import torch
+    rng = np.random.default_rng(153)
+    N, K = 4, 512
+    q = {"qs": rng.integers(0, 256, (N, K // 2)).astype(np.uint8),
+         "sc": rng.integers(0, 64, (N, K // 32)).astype(np.uint8),
+         "mn": rng.integers(0, 64, (N, K // 32)).astype(np.uint8),
+         "d": np.array([[oracle.float_to_half(float(v)) for v in rng.lognormal(-7, 2, K // 256)]
+                        for _ in range(N)], np.uint16),
+         "dmin": np.array([[oracle.float_to_half(float(v)) for v in rng.lognormal(-7, 2, K // 256)]
+                           for _ in range(N)], np.uint16)}
+    s, o, codes = _q4_k_grid(q, N, K)
+    exact = torch.from_numpy(s * codes - o)
+    want = exact.to(torch.float32).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(oracle.q4_k_dequantize(q, N, K), want)
+
+
+def test_q4_k_linear_against_numpy_fp64():
+    c = synth.linear_case([154], 33, 40, 512)
+    q = oracle.q4_k_quantize(c["W"], 40, 512)
+    Wd = oracle.q4_k_dequantize(q, 40, 512)
+    Y = oracle.q4_k_linear(c["X"], q, c["bias"], 33, 40, 512)
+    X = bf16_to_f64(c["X"]).reshape(33, 512)
+    ref = X @ bf16_to_f64(Wd).reshape(40, 512).T + bf16_to_f64(c["bias"])[None, :]
+    y = bf16_to_f64(Y).reshape(33, 40)
+    assert np.all(np.abs(y - ref) <= np.abs(ref) * 2.0 ** -8 + 1e-30)

@@ -135,10 +135,11 @@ def device_inputs(M, K, dev, gen, n, gelu: bool):
 
 
 def build_workload(name: str, dev, pool: int):
-    if name == "q8_0_ffn_up":
+    if name in ("q8_0_ffn_up", "q4_k_ffn_up"):
         c = synth.ffn_up_case()
         lin = host_case_linear("ffn_up", c, dev, pool, True, 2)
-        lin.lay = L.prepare_q8_0(lin.lay.W, lin.lay.bias)  # the bf16 copy is dropped
+        prep = L.prepare_q8_0 if name == "q8_0_ffn_up" else L.prepare_q4_k
+        lin.lay = prep(lin.lay.W, lin.lay.bias)  # the bf16 copy is dropped
         return [lin]
     if name == "ffn_up":
         return [host_case_linear("ffn_up", synth.ffn_up_case(), dev, pool, False, 2)]
@@ -186,10 +187,13 @@ def run_step(layers, it: int, ws: L.Workspace, events=None):
                 events[li][0].record()
                 events[li][1].record()
             ops.bf16_linear(X, lin.lay.W, lin.lay.bias, out=lin.Y)
-        elif lin.lay.q8_0:
+        elif lin.lay.weight_only:
             if events is not None:
                 events[li][0].record()
-            ops.q8_0_dequantize(lin.lay.q8_qs, lin.lay.q8_d, out=ws.weights(lin.lay.N, lin.lay.K))
+            if lin.lay.q8_0:
+                ops.q8_0_dequantize(lin.lay.q8_qs, lin.lay.q8_d, out=ws.weights(lin.lay.N, lin.lay.K))
+            else:
+                ops.q4_k_dequantize(lin.lay.q4k, out=ws.weights(lin.lay.N, lin.lay.K))
             if events is not None:
                 events[li][1].record()
             ops.bf16_linear(X, ws.weights(lin.lay.N, lin.lay.K), lin.lay.bias, out=lin.Y)
@@ -331,6 +335,14 @@ def quant_bytes(M, K) -> int:
     """Algorithmic bytes of one quant launch: read X (bf16) and inv_lambda,
     write Xq (int8) and x_scale."""
     return 2 * M * K + M * K + 4 * M + 4 * K
+
+
+def dequant_bytes(fmt: str, N: int, K: int) -> int:
+    """Algorithmic HBM bytes of decoding a GGUF weight [N, K] to bf16: the
+    planes read once, the bf16 weights written once."""
+    if fmt == "q8_0":
+        return N * K + 2 * (N * K // 32) + 2 * N * K
+    return N * K // 2 + 2 * (N * K // 32) + 4 * (N * K // 256) + 2 * N * K
 
 
 # --------------------------------------------------------------------------
@@ -486,7 +498,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="ffn_up",
-                    choices=["ffn_up", "ffn_down", "dit_block", "backbone", "q8_0_ffn_up"])
+                    choices=["ffn_up", "ffn_down", "dit_block", "backbone", "q8_0_ffn_up",
+                             "q4_k_ffn_up"])
     ap.add_argument("--pool", type=int, default=4, help="distinct inputs rotated over steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -529,20 +542,21 @@ def main():
     total_ops = sum(lin.ops for lin in layers)
     value = total_ops / (step_ms * 1e-3) / 1e12
 
-    w8 = [i for i, lin in enumerate(layers) if not lin.lay.protected and not lin.lay.q8_0]
+    w8 = [i for i, lin in enumerate(layers) if not lin.lay.protected and not lin.lay.weight_only]
     prot = [i for i, lin in enumerate(layers) if lin.lay.protected]
-    q8 = [i for i, lin in enumerate(layers) if lin.lay.q8_0]
+    gg = [i for i, lin in enumerate(layers) if lin.lay.weight_only]
     dom = max(w8, key=lambda i: gemm_us[i]) if w8 else None
     kernels = {}
-    for i in q8:
+    for i in gg:
         lin = layers[i]
         M, N, K = lin.M, lin.lay.N, lin.lay.K
         g, q = float(gemm_us[i]), float(quant_us[i])
-        dq_bytes = N * K + N * K // 16 + 2 * N * K   # codes + scales in, bf16 out
-        kernels[f"q8_0_dequantize_{N}x{K}_in_step"] = {
+        fmt = "q8_0" if lin.lay.q8_0 else "q4_k"
+        dq_bytes = dequant_bytes(fmt, N, K)
+        kernels[f"{fmt}_dequantize_{N}x{K}_in_step"] = {
             "us": round(q, 2), "GB_s": round(dq_bytes / q / 1e3, 1),
             "frac_hbm": round(dq_bytes / q / 1e3 / PEAK_HBM_GBS, 4)}
-        kernels[f"q8_0_bf16_gemm_{M}x{K}x{N}"] = {
+        kernels[f"{fmt}_bf16_gemm_{M}x{K}x{N}"] = {
             "us": round(g, 2), "TFLOPS": round(2 * M * N * K / g / 1e6, 1),
             "frac_bf16_peak": round(2 * M * N * K / g / 1e6 / PEAK_BF16_TFLOPS, 4)}
     for shape_key in sorted({(layers[i].M, layers[i].lay.N, layers[i].lay.K) for i in w8}):
@@ -593,10 +607,11 @@ def main():
             "frac_hbm_of_one_read": round(one / med / 1e3 / PEAK_HBM_GBS, 4)}
 
     roofline = None
-    if dom is None and q8:
-        i = q8[0]
+    if dom is None and gg:
+        i = gg[0]
         ach = layers[i].ops / (gemm_us[i] * 1e-6) / 1e12
-        roofline = {"bound": "mfma", "kernel": "bf16 GEMM of the Q8_0 weight-only linear",
+        fmt = "Q8_0" if layers[i].lay.q8_0 else "Q4_K"
+        roofline = {"bound": "mfma", "kernel": f"bf16 GEMM of the {fmt} weight-only linear",
                     "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                     "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None,
                     "ops_per_launch": layers[i].ops, "avg_launch_us": round(float(gemm_us[i]), 2)}
@@ -619,7 +634,8 @@ def main():
                         "ffn_down": "DiT FFN down-projection 4608x16384->4096, W8A8 and protected bf16",
                         "dit_block": "one DiT block (qkv, attn_out, ffn_up, ffn_down protected), both CFG branches",
                         "backbone": "211 linears x 2 branches, 17 protected per branch",
-                        "q8_0_ffn_up": "DiT FFN up-projection 4608x4096->16384 with GGUF Q8_0 weights"}[args.workload],
+                        "q8_0_ffn_up": "DiT FFN up-projection 4608x4096->16384 with GGUF Q8_0 weights",
+                        "q4_k_ffn_up": "DiT FFN up-projection 4608x4096->16384 with GGUF Q4_K weights"}[args.workload],
            "tokens": M0, "linears": len(layers), "protected": len(prot),
            "input_pool": args.pool if args.workload in ("ffn_up", "ffn_down") else None,
            "smoothquant_alpha": 0.5}
@@ -627,7 +643,7 @@ def main():
         "metric": METRIC, "value": round(value, 2), "unit": "TOPS", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16" if q8 and not w8 else "int8",
+        "dtype": "bf16" if gg and not w8 else "int8",
         "data": "synthetic", "config": cfg, "roofline": roofline, "cpu_baseline": cpu,
         "kernels": kernels, "ms_per_step_with_kernel_events": round(step_ms_ev, 4),
         "host_wall_ms_per_step": round(wall_ms, 4),

@@ -28,7 +28,7 @@ CFLAGS = ["-O2", "-fno-fast-math", "-ffp-contract=off", "-fopenmp",
 
 def build() -> str:
     """Compile liboracle.so with gcc (always recompiles)."""
-    tmp = _LIB_PATH + ".tmp"
+    tmp = f"{_LIB_PATH}.{os.getpid()}.tmp"   # parallel test workers each build their own
     subprocess.run(["gcc", *CFLAGS, "-o", tmp, _SRC, "-lm"], check=True)
     os.replace(tmp, _LIB_PATH)
     return _LIB_PATH

@@ -1,0 +1,162 @@
+// GGUF Q4_K weight-only format (paper Section 3, "GGUF k-quants": 4-bit
+// codes in super-blocks, quantized by the paper's own super-block encoder).
+// A super-block is 256 consecutive weights of a row, cut into 8 sub-blocks
+// of 32; sub-block j reads back as
+//   w = d * sc_j * q - dmin * m_j,   q in [0, 15], sc_j and m_j in [0, 63],
+// with binary16 d and dmin per super-block. Round to nearest on a min-max
+// grid, in binary32 with one rounding per operation:
+//   1. per sub-block: lo = min(0, min w), hi = max w, a_j = (hi - lo) / 15,
+//      b_j = -lo;
+//   2. d = RN16(min(max_j a_j / 63, 65504)), dmin likewise from the b_j;
+//      sc_j = min(rint(a_j * RN32(1/d)), 63), m_j = min(rint(b_j * RN32(1/dmin)), 63)
+//      against the stored d and dmin (0 where they are 0);
+//   3. s_j = d * sc_j and o_j = dmin * m_j (exact),
+//      q = clamp(rint((w + o_j) * RN32(1/s_j)), 0, 15)   (0 where s_j = 0).
+// A weight reads back as bf16(RN32(s_j * q - o_j)) (s_j * q is exact).
+// Stored planar: qs [N][K/2] (even k in the low nibble), sc and mn
+// [N][K/32] bytes, d and dmin [N][K/256] binary16: 4.625 bits per weight.
+//
+// Dequantize is an HBM-bound stream: per weight 1/2 byte of codes and 1/16
+// of 6-bit planes in, 2 bytes of bf16 out.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "internal.h"
+
+namespace w8a8 {
+namespace {
+
+constexpr int kSub = 32;
+constexpr int kSubs = 8;  // sub-blocks per super-block
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ uint32_t bf16_pair(float a, float b) {
+    return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(a))) |
+           static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(b))) << 16;
+}
+
+__device__ __forceinline__ float half_bits_to_float(uint16_t h) {
+    return static_cast<float>(__builtin_bit_cast(_Float16, h));
+}
+
+__device__ __forceinline__ uint16_t float_to_half_bits(float f) {
+    return __builtin_bit_cast(uint16_t, static_cast<_Float16>(f));  // round to nearest even
+}
+
+// The larger of a and b, keeping a unless b is strictly larger (so that a
+// +0 start is never replaced by -0).
+__device__ __forceinline__ float keep_max(float a, float b) { return b > a ? b : a; }
+
+__device__ __forceinline__ float group8_max(float v) {
+#pragma unroll
+    for (int m = 1; m < kSubs; m <<= 1) v = keep_max(v, __shfl_xor(v, m, 64));
+    return v;
+}
+
+// One thread per sub-block; the 8 threads of a super-block are 8
+// consecutive lanes and agree on d and dmin through lane shuffles.
+__global__ __launch_bounds__(256) void q4_k_quantize_kernel(
+    const uint16_t *__restrict__ W, int64_t subs, uint8_t *__restrict__ qs,
+    uint8_t *__restrict__ sc, uint8_t *__restrict__ mn, uint16_t *__restrict__ d,
+    uint16_t *__restrict__ dmin) {
+    const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    // subs is a multiple of 8 and groups of 8 lanes are aligned, so a
+    // super-block's lanes are either all in range or all out.
+    if (j >= subs) return;
+    const uint4 *src = reinterpret_cast<const uint4 *>(W + j * kSub);
+    float v[kSub];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const uint4 x = src[c];
+        const uint32_t words[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            v[8 * c + 2 * e] = bf16_lo(words[e]);
+            v[8 * c + 2 * e + 1] = bf16_hi(words[e]);
+        }
+    }
+    float lo = 0.0f, hi = -__builtin_inff();
+#pragma unroll
+    for (int i = 0; i < kSub; ++i) {
+        lo = v[i] < lo ? v[i] : lo;
+        hi = v[i] > hi ? v[i] : hi;
+    }
+    const float a = (hi - lo) / 15.0f;
+    const float b = -lo;
+    const float amax = group8_max(keep_max(0.0f, a));
+    const float bmax = group8_max(keep_max(0.0f, b));
+    const uint16_t hd = float_to_half_bits(fminf(amax / 63.0f, 65504.0f));
+    const uint16_t hdm = float_to_half_bits(fminf(bmax / 63.0f, 65504.0f));
+    if ((j & (kSubs - 1)) == 0) {
+        d[j / kSubs] = hd;
+        dmin[j / kSubs] = hdm;
+    }
+    const float fd = half_bits_to_float(hd), fdm = half_bits_to_float(hdm);
+    const float inv_d = fd != 0.0f ? 1.0f / fd : 0.0f;
+    const float inv_dm = fdm != 0.0f ? 1.0f / fdm : 0.0f;
+    const float cs = fminf(rintf(a * inv_d), 63.0f);
+    const float cm = fminf(rintf(b * inv_dm), 63.0f);
+    sc[j] = static_cast<uint8_t>(cs);
+    mn[j] = static_cast<uint8_t>(cm);
+    const float s = fd * cs, o = fdm * cm;
+    const float inv = s != 0.0f ? 1.0f / s : 0.0f;
+    uint32_t packed[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < kSub; ++i) {
+        const float c = fminf(fmaxf(rintf((v[i] + o) * inv), 0.0f), 15.0f);
+        packed[i / 8] |= static_cast<uint32_t>(c) << (4 * (i % 8));
+    }
+    reinterpret_cast<uint4 *>(qs)[j] = make_uint4(packed[0], packed[1], packed[2], packed[3]);
+}
+
+// One thread per 8 weights: 4 bytes of codes, the sub-block's two 6-bit
+// values and the super-block's two scales in, 16 bytes of bf16 out, so a
+// wave's stores cover 1 KiB contiguously.
+__global__ __launch_bounds__(256) void q4_k_dequantize_kernel(
+    const uint32_t *__restrict__ qs, const uint8_t *__restrict__ sc,
+    const uint8_t *__restrict__ mn, const uint16_t *__restrict__ d,
+    const uint16_t *__restrict__ dmin, int64_t octets, u32x4 *__restrict__ W) {
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (t >= octets) return;
+    const int64_t j = t >> 2;  // sub-block (4 octets each)
+    const int64_t g = t >> 5;  // super-block (32 octets each)
+    const float s = half_bits_to_float(d[g]) * static_cast<float>(sc[j]);
+    const float o = half_bits_to_float(dmin[g]) * static_cast<float>(mn[j]);
+    const uint32_t q = __builtin_nontemporal_load(qs + t);
+    uint32_t out[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float q0 = static_cast<float>((q >> (8 * e)) & 15u);
+        const float q1 = static_cast<float>((q >> (8 * e + 4)) & 15u);
+        out[e] = bf16_pair(s * q0 - o, s * q1 - o);
+    }
+    __builtin_nontemporal_store(u32x4{out[0], out[1], out[2], out[3]}, W + t);
+}
+
+unsigned grid_for(int64_t n) { return static_cast<unsigned>((n + 255) / 256); }
+
+}  // namespace
+
+hipError_t launch_q4_k_quantize(const uint16_t *W, int64_t N, int64_t K, uint8_t *qs, uint8_t *sc,
+                                uint8_t *mn, uint16_t *d, uint16_t *dmin, hipStream_t stream) {
+    const int64_t subs = N * (K / kSub);
+    hipLaunchKernelGGL(q4_k_quantize_kernel, dim3(grid_for(subs)), dim3(256), 0, stream, W, subs,
+                       qs, sc, mn, d, dmin);
+    return hipGetLastError();
+}
+
+hipError_t launch_q4_k_dequantize(const uint8_t *qs, const uint8_t *sc, const uint8_t *mn,
+                                  const uint16_t *d, const uint16_t *dmin, int64_t N, int64_t K,
+                                  uint16_t *W, hipStream_t stream) {
+    const int64_t octets = N * K / 8;
+    hipLaunchKernelGGL(q4_k_dequantize_kernel, dim3(grid_for(octets)), dim3(256), 0, stream,
+                       reinterpret_cast<const uint32_t *>(qs), sc, mn, d, dmin, octets,
+                       reinterpret_cast<u32x4 *>(W));
+    return hipGetLastError();
+}
+
+}  // namespace w8a8

@@ -1,8 +1,8 @@
 """One linear of the DiT routed through the W8A8 recipe, the protected bf16
-path, or the GGUF Q8_0 weight-only format (paper Section 3: every linear is
-W8A8 except the top-N most fragile layers, N = 17 of 211 per branch, which
-stay bf16 with no activation quantization; independently, a checkpoint can
-be stored as Q8_0). Host-side bookkeeping only: the arithmetic runs in the
+path, or a GGUF weight-only format, Q8_0 or Q4_K (paper Section 3: every
+linear is W8A8 except the top-N most fragile layers, N = 17 of 211 per
+branch, which stay bf16 with no activation quantization; independently, a
+checkpoint can be stored as Q8_0 or Q4_K). Host-side bookkeeping only: the arithmetic runs in the
 library's kernels through ops."""
 from __future__ import annotations
 
@@ -26,14 +26,21 @@ class PreparedLinear:
     inv_lambda: torch.Tensor | None = None   # fp32 [K]
     q8_qs: torch.Tensor | None = None        # int8 [N, K], Q8_0 layers only
     q8_d: torch.Tensor | None = None         # fp16 [N, K/32]
+    q4k: ops.Q4K | None = None               # Q4_K planes, Q4_K layers only
 
     @property
     def q8_0(self) -> bool:
         return self.q8_qs is not None
 
+    @property
+    def weight_only(self) -> bool:
+        """A GGUF layer: decoded to bf16, then the bf16 linear."""
+        return self.q8_qs is not None or self.q4k is not None
+
     def nbytes(self) -> int:
         ts = [self.W, self.Wq, self.w_scale, self.inv_lambda, self.bias, self.q8_qs, self.q8_d]
-        return sum(t.numel() * t.element_size() for t in ts if t is not None)
+        n = sum(t.numel() * t.element_size() for t in ts if t is not None)
+        return n + (self.q4k.nbytes if self.q4k is not None else 0)
 
 
 def prepare_linear(W: torch.Tensor, bias: torch.Tensor | None, lam: torch.Tensor | None,
@@ -56,8 +63,15 @@ def prepare_q8_0(W: torch.Tensor, bias: torch.Tensor | None) -> PreparedLinear:
     return PreparedLinear(False, N, K, bias, q8_qs=qs, q8_d=d)
 
 
+def prepare_q4_k(W: torch.Tensor, bias: torch.Tensor | None) -> PreparedLinear:
+    """Encode W once (offline) as GGUF Q4_K: 4-bit codes in super-blocks of
+    256 (4.625 bits per weight in the planar layout)."""
+    N, K = W.shape
+    return PreparedLinear(False, N, K, bias, q4k=ops.q4_k_quantize(W))
+
+
 class Workspace:
-    """Reusable buffers (Xq, x_scale, and the decoded bf16 weights of a Q8_0
+    """Reusable buffers (Xq, x_scale, and the decoded bf16 weights of a GGUF
     layer) so that a forward allocates nothing once the largest shape has
     been seen."""
 
@@ -84,12 +98,15 @@ class Workspace:
 def route(layer: PreparedLinear, X: torch.Tensor, out: torch.Tensor | None = None,
           ws: Workspace | None = None) -> torch.Tensor:
     """Y = layer(X): bf16_linear for a protected layer, the weight-only
-    linear for a Q8_0 layer, else quant + W8A8 GEMM."""
+    linear for a Q8_0 or Q4_K layer, else quant + W8A8 GEMM."""
     if layer.protected:
         return ops.bf16_linear(X, layer.W, layer.bias, out=out)
     if layer.q8_0:
         work = ws.weights(layer.N, layer.K) if ws is not None else None
         return ops.q8_0_linear(X, layer.q8_qs, layer.q8_d, layer.bias, work=work, out=out)
+    if layer.q4k is not None:
+        work = ws.weights(layer.N, layer.K) if ws is not None else None
+        return ops.q4_k_linear(X, layer.q4k, layer.bias, work=work, out=out)
     M = X.shape[0]
     if ws is None:
         Xq = x_scale = None

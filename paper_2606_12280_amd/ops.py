@@ -250,3 +250,93 @@ def q8_0_linear(X: torch.Tensor, qs: torch.Tensor, d: torch.Tensor,
         check("q8_0_linear", lib.q8_0_linear(_ptr(X), _ptr(qs), _ptr(d), _ptr(bias), M, N, K,
                                              _ptr(work), _ptr(Y), _stream(X.device)))
     return Y
+
+
+# --------------------------------------------------------------------------
+# GGUF Q4_K weight-only
+# --------------------------------------------------------------------------
+
+Q4_K_SUPER = 256
+Q4_K_SUB = 32
+
+
+class Q4K:
+    """The planes of a Q4_K weight [N, K]: qs uint8 [N, K/2] (two 4-bit codes
+    per byte, even k low), sc and mn uint8 [N, K/32] (6-bit sub-block scales
+    and offsets), d and dmin float16 [N, K/256] (super-block scales)."""
+
+    __slots__ = ("qs", "sc", "mn", "d", "dmin")
+
+    def __init__(self, qs, sc, mn, d, dmin):
+        self.qs, self.sc, self.mn, self.d, self.dmin = qs, sc, mn, d, dmin
+
+    @property
+    def shape(self) -> tuple[int, int]:
+        return self.qs.shape[0], 2 * self.qs.shape[1]
+
+    @property
+    def nbytes(self) -> int:
+        return sum(t.numel() * t.element_size() for t in (self.qs, self.sc, self.mn, self.d, self.dmin))
+
+    def check(self, device=None) -> tuple[int, int]:
+        _need(self.qs, "qs", torch.uint8, 2, device)
+        N, K = self.shape
+        dev = self.qs.device
+        for name, t, dt, cols in (("sc", self.sc, torch.uint8, K // Q4_K_SUB),
+                                  ("mn", self.mn, torch.uint8, K // Q4_K_SUB),
+                                  ("d", self.d, torch.float16, K // Q4_K_SUPER),
+                                  ("dmin", self.dmin, torch.float16, K // Q4_K_SUPER)):
+            _need(t, name, dt, 2, dev)
+            if tuple(t.shape) != (N, cols):
+                raise ValueError(f"{name} must be [{N}, {cols}], got {tuple(t.shape)}")
+        return N, K
+
+    def ptrs(self):
+        return [_ptr(t) for t in (self.qs, self.sc, self.mn, self.d, self.dmin)]
+
+
+def q4_k_quantize(W: torch.Tensor) -> Q4K:
+    """W [N, K] bf16 (256 | K) -> its Q4_K planes."""
+    _need(W, "W", torch.bfloat16, 2)
+    N, K = W.shape
+    dev = W.device
+    q = Q4K(torch.empty(N, K // 2, dtype=torch.uint8, device=dev),
+            torch.empty(N, K // Q4_K_SUB, dtype=torch.uint8, device=dev),
+            torch.empty(N, K // Q4_K_SUB, dtype=torch.uint8, device=dev),
+            torch.empty(N, K // Q4_K_SUPER, dtype=torch.float16, device=dev),
+            torch.empty(N, K // Q4_K_SUPER, dtype=torch.float16, device=dev))
+    lib = load()
+    with torch.cuda.device(dev):
+        check("q4_k_quantize", lib.q4_k_quantize(_ptr(W), N, K, *q.ptrs(), _stream(dev)))
+    return q
+
+
+def q4_k_dequantize(q: Q4K, out: torch.Tensor | None = None) -> torch.Tensor:
+    """bf16(d * sc * code - dmin * mn) as bf16 [N, K]."""
+    N, K = q.check()
+    dev = q.qs.device
+    W = _out(out, (N, K), torch.bfloat16, dev, "out")
+    lib = load()
+    with torch.cuda.device(dev):
+        check("q4_k_dequantize", lib.q4_k_dequantize(*q.ptrs(), N, K, _ptr(W), _stream(dev)))
+    return W
+
+
+def q4_k_linear(X: torch.Tensor, q: Q4K, bias: torch.Tensor | None = None,
+                work: torch.Tensor | None = None, out: torch.Tensor | None = None) -> torch.Tensor:
+    """Y = X W'^T + bias with W' the decoded Q4_K weights, decoded into
+    `work` (bf16 [N, K], allocated if not given)."""
+    _need(X, "X", torch.bfloat16, 2)
+    M, K = X.shape
+    N, Kq = q.check(X.device)
+    if Kq != K:
+        raise ValueError(f"the weights are [{N}, {Kq}], X has K = {K}")
+    if bias is not None:
+        _need(bias, "bias", torch.bfloat16, 1, X.device)
+    work = _out(work, (N, K), torch.bfloat16, X.device, "work")
+    Y = _out(out, (M, N), torch.bfloat16, X.device, "out")
+    lib = load()
+    with torch.cuda.device(X.device):
+        check("q4_k_linear", lib.q4_k_linear(_ptr(X), *q.ptrs(), _ptr(bias), M, N, K,
+                                             _ptr(work), _ptr(Y), _stream(X.device)))
+    return Y

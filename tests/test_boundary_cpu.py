@@ -146,6 +146,35 @@ def test_q8_0_validation(lib):
     assert f(A, B, C, None, 4, 8, 96, D, E, None) == UNSUP
 
 
+def test_q4_k_validation(lib):
+    F = 0x7F0500000000
+    G = 0x7F0600000000
+    q = lib.q4_k_quantize
+    assert q(None, 8, 256, B, C, D, E, F, None) == NULL
+    assert q(A, 8, 256, B, C, D, E, None, None) == NULL
+    assert q(A, 0, 256, B, C, D, E, F, None) == SHAPE
+    assert q(A, 8, 128, B, C, D, E, F, None) == UNSUP          # K % 256 != 0
+    assert q(A, 8, 96, B, C, D, E, F, None) == UNSUP
+    assert q(A + 2, 8, 256, B, C, D, E, F, None) == ALIGN
+    assert q(A, 8, 256, B + 8, C, D, E, F, None) == ALIGN       # codes
+    assert q(A, 8, 256, B, C, D, E + 1, F, None) == ALIGN       # d
+    assert q(A, 8, 256, A + 64, C, D, E, F, None) == ALIAS      # codes inside W
+    assert q(A, 8, 256, B, B + 512, D, E, F, None) == ALIAS     # sc inside the codes (1 KiB)
+    assert q(A, 8, 256, B, C, C + 32, E, F, None) == ALIAS      # mn inside sc (64 B)
+    assert q(A, 8, 256, B, C, D, E, E + 8, None) == ALIAS       # dmin inside d (16 B)
+    dq = lib.q4_k_dequantize
+    assert dq(A, B, C, D, E, 8, 256, None, None) == NULL
+    assert dq(A, B, C, D, E, 8, 256, A + 16, None) == ALIAS
+    assert dq(A, B, C, D, E, 8, 256, F + 8, None) == ALIGN
+    f = lib.q4_k_linear
+    assert f(A, B, C, D, E, F, None, 4, 8, 256, G, None, None) == NULL
+    assert f(A, B, C, D, E, F, None, 4, 8, 256, None, G, None) == NULL
+    assert f(A, B, C, D, E, F, None, 4, 8, 256, G, G, None) == ALIAS     # Y inside work
+    assert f(A, B, C, D, E, F, None, 4, 8, 256, B, G, None) == ALIAS     # work over the codes
+    assert f(A, B, C, D, E, F, None, 4, 8, 512 + 64, G, 0x7F0700000000, None) == UNSUP
+    assert f(A, B, C, D, E, F, None, 0, 8, 256, G, 0x7F0700000000, None) == SHAPE
+
+
 def test_binding_rejects_host_tensors():
     X = torch.zeros(4, 64, dtype=torch.bfloat16)
     il = torch.ones(64)

@@ -15,6 +15,7 @@ import torch
 
 import oracle
 import synth
+from bf16ref import bf16_to_f64
 from parity import (DEV, check_bf16_output, check_w8a8_output, dev, dev_bf16, host,
                     host_bits)
 
@@ -487,3 +488,84 @@ def test_q8_0_full_size_ffn_up():
     rows = np.random.default_rng(152).choice(M, 24, replace=False)
     Wd = oracle.q8_0_dequantize(qs_ref, d_ref, N, K)
     check_bf16_output(Y[rows], X[rows], Wd, c["bias"])
+
+
+# --------------------------------------------------------------------------
+# GGUF Q4_K weight-only (Section 3, "GGUF k-quants")
+# --------------------------------------------------------------------------
+
+def _q4k_case(seed, N, K):
+    W = synth.rand_bf16(seed, (N, K), 0.02).reshape(N, K)
+    Wf = bf16_to_f64(W).reshape(N, K).astype(np.float32)
+    rng = np.random.default_rng(seed)
+    Wf[:, rng.choice(K, max(1, K // 64), replace=False)] *= 12     # outlier channels
+    if N >= 4:
+        Wf[1] = np.abs(Wf[1])                                       # no offsets needed
+        Wf[2] += 0.01                                               # a mean offset
+    if K >= 512 and N >= 4:
+        Wf[3, :256] = 0                                             # a zero super-block
+        Wf[3, 256:288] = -0.75                                      # a constant sub-block
+        Wf[3, 300] = 3.0e9                                          # d capped at 65504
+    return synth.to_bf16_bits(Wf)
+
+
+def _q4k_host(q):
+    return {"qs": host(q.qs), "sc": host(q.sc), "mn": host(q.mn),
+            "d": host(q.d).view(np.uint16), "dmin": host(q.dmin).view(np.uint16)}
+
+
+def _check_q4k_planes(q, ref):
+    got = _q4k_host(q)
+    for name in ("qs", "sc", "mn", "d", "dmin"):
+        assert np.array_equal(got[name], ref[name]), name
+
+
+@pytest.mark.parametrize("N,K", [(1, 256), (7, 512), (33, 1280), (512, 4096)])
+def test_q4_k_planes_and_decode_bit_exact(N, K):
+    W = _q4k_case([160, N, K], N, K)
+    ref = oracle.q4_k_quantize(W, N, K)
+    q = ops.q4_k_quantize(dev_bf16(W))
+    _check_q4k_planes(q, ref)
+    assert np.array_equal(host_bits(ops.q4_k_dequantize(q)), oracle.q4_k_dequantize(ref, N, K))
+
+
+def test_q4_k_decode_of_arbitrary_planes():
+    """Decoding planes the encoder would not produce (every code, 6-bit
+    value and a wide range of binary16 scales) matches the oracle."""
+    rng = np.random.default_rng(161)
+    N, K = 16, 1024
+    ref = {"qs": rng.integers(0, 256, (N, K // 2)).astype(np.uint8),
+           "sc": rng.integers(0, 64, (N, K // 32)).astype(np.uint8),
+           "mn": rng.integers(0, 64, (N, K // 32)).astype(np.uint8),
+           "d": rng.lognormal(-6, 3, (N, K // 256)).astype(np.float16).view(np.uint16),
+           "dmin": rng.lognormal(-6, 3, (N, K // 256)).astype(np.float16).view(np.uint16)}
+    q = ops.Q4K(dev(ref["qs"]), dev(ref["sc"]), dev(ref["mn"]),
+                dev(ref["d"].view(np.float16)), dev(ref["dmin"].view(np.float16)))
+    assert np.array_equal(host_bits(ops.q4_k_dequantize(q)), oracle.q4_k_dequantize(ref, N, K))
+
+
+@pytest.mark.parametrize("M,N,K", [(64, 512, 256), (257, 129, 512), (300, 520, 1280)])
+def test_q4_k_linear(M, N, K):
+    c = synth.linear_case([162, M, N, K], M, N, K, act="gelu")
+    ref = oracle.q4_k_quantize(c["W"], N, K)
+    Wd = oracle.q4_k_dequantize(ref, N, K)
+    q = ops.q4_k_quantize(dev_bf16(c["W"]))
+    _check_q4k_planes(q, ref)
+    Y = host_bits(ops.q4_k_linear(dev_bf16(c["X"]), q, dev_bf16(c["bias"])))
+    check_bf16_output(Y, c["X"].reshape(M, K), Wd, c["bias"])
+    from bf16ref import ulp_distance
+    assert (ulp_distance(Y, oracle.q4_k_linear(c["X"], ref, c["bias"], M, N, K)) <= 1).mean() > 0.999
+
+
+def test_q4_k_full_size_ffn_up():
+    """FFN up weights 16384 x 4096: every plane bit-exact on the whole
+    tensor; the linear on 24 sampled token rows."""
+    c = synth.ffn_up_case()
+    M, N, K = c["M"], c["N"], c["K"]
+    ref = oracle.q4_k_quantize(c["W"], N, K)
+    q = ops.q4_k_quantize(dev_bf16(c["W"]))
+    _check_q4k_planes(q, ref)
+    X = c["X"].reshape(M, K)
+    Y = host_bits(ops.q4_k_linear(dev_bf16(X), q, dev_bf16(c["bias"])))
+    rows = np.random.default_rng(163).choice(M, 24, replace=False)
+    check_bf16_output(Y[rows], X[rows], oracle.q4_k_dequantize(ref, N, K), c["bias"])

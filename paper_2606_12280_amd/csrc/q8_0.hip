@@ -19,6 +19,8 @@ namespace w8a8 {
 namespace {
 
 constexpr int kBlock = 32;
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -77,21 +79,21 @@ __global__ __launch_bounds__(256) void q8_0_quantize_kernel(const uint16_t *__re
     }
 }
 
-// One thread per 16 codes (half a block): 16 bytes of codes and the block's
-// scale in, 32 bytes of bf16 out.
-__global__ __launch_bounds__(256) void q8_0_dequantize_kernel(const int8_t *__restrict__ qs,
+// One thread per 8 codes: 8 bytes of codes and the block's scale in, 16
+// bytes of bf16 out, so a wave's stores cover 1 KiB contiguously. Codes in
+// and weights out carry nontemporal hints (streamed once).
+__global__ __launch_bounds__(256) void q8_0_dequantize_kernel(const u32x2 *__restrict__ qs,
                                                               const uint16_t *__restrict__ d,
-                                                              int64_t halves,
-                                                              uint16_t *__restrict__ W) {
-    const int64_t h = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-    if (h >= halves) return;
-    const float ds = static_cast<float>(__builtin_bit_cast(_Float16, d[h >> 1]));
-    const uint4 q = reinterpret_cast<const uint4 *>(qs)[h];
-    const uint32_t words[4] = {q.x, q.y, q.z, q.w};
-    uint32_t out[8];
+                                                              int64_t octets,
+                                                              u32x4 *__restrict__ W) {
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (t >= octets) return;
+    const float ds = static_cast<float>(__builtin_bit_cast(_Float16, d[t >> 2]));
+    const u32x2 q = __builtin_nontemporal_load(qs + t);
+    uint32_t out[4];
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-        const int32_t v = static_cast<int32_t>(words[w]);
+    for (int w = 0; w < 2; ++w) {
+        const int32_t v = static_cast<int32_t>(q[w]);
         const float c0 = static_cast<float>((v << 24) >> 24);
         const float c1 = static_cast<float>((v << 16) >> 24);
         const float c2 = static_cast<float>((v << 8) >> 24);
@@ -99,9 +101,7 @@ __global__ __launch_bounds__(256) void q8_0_dequantize_kernel(const int8_t *__re
         out[2 * w] = bf16_pair(ds * c0, ds * c1);
         out[2 * w + 1] = bf16_pair(ds * c2, ds * c3);
     }
-    uint4 *dst = reinterpret_cast<uint4 *>(W) + 2 * h;
-    dst[0] = make_uint4(out[0], out[1], out[2], out[3]);
-    dst[1] = make_uint4(out[4], out[5], out[6], out[7]);
+    __builtin_nontemporal_store(u32x4{out[0], out[1], out[2], out[3]}, W + t);
 }
 
 unsigned grid_for(int64_t n) { return static_cast<unsigned>((n + 255) / 256); }
@@ -118,9 +118,10 @@ hipError_t launch_q8_0_quantize(const uint16_t *W, int64_t N, int64_t K, int8_t 
 
 hipError_t launch_q8_0_dequantize(const int8_t *qs, const uint16_t *d, int64_t N, int64_t K,
                                   uint16_t *W, hipStream_t stream) {
-    const int64_t halves = N * K / 16;
-    hipLaunchKernelGGL(q8_0_dequantize_kernel, dim3(grid_for(halves)), dim3(256), 0, stream, qs,
-                       d, halves, W);
+    const int64_t octets = N * K / 8;
+    hipLaunchKernelGGL(q8_0_dequantize_kernel, dim3(grid_for(octets)), dim3(256), 0, stream,
+                       reinterpret_cast<const u32x2 *>(qs), d, octets,
+                       reinterpret_cast<u32x4 *>(W));
     return hipGetLastError();
 }
 

@@ -73,6 +73,7 @@ def _load():
         "oracle_half_to_float": ([ctypes.c_uint16], ctypes.c_float),
         "oracle_q8_0_quantize": ([P, I64, I64, P, P], None),
         "oracle_q8_0_dequantize": ([P, P, I64, I64, P], None),
+        "oracle_adaln_modulate": ([P, P, P, I64, I64, ctypes.c_double, P], None),
         "oracle_q4_k_quantize": ([P, I64, I64, P, P, P, P, P], None),
         "oracle_q4_k_dequantize": ([P, P, P, P, P, I64, I64, P], None),
     }
@@ -149,6 +150,22 @@ def quant_act(X, inv_lam, M: int, K: int):
     xs = np.empty(M, np.float32)
     _load().oracle_quant_act(_p(X), _p(il), M, K, _p(Xq), _p(xs))
     return Xq, xs
+
+
+def adaln_modulate(X, shift, scale, M: int, K: int, eps: float = 1e-6) -> np.ndarray:
+    """bf16 bits [M][K] of LayerNorm(X) * (1 + scale) + shift (binary64, one
+    rounding to bf16)."""
+    X = _c(X, np.uint16)
+    H = np.empty((M, K), np.uint16)
+    _load().oracle_adaln_modulate(_p(X), _p(_c(shift, np.uint16)), _p(_c(scale, np.uint16)),
+                                  M, K, float(eps), _p(H))
+    return H
+
+
+def adaln_quant_act(X, shift, scale, inv_lam, M: int, K: int, eps: float = 1e-6):
+    """The W8A8 activation side on the adaLN-modulated input: quant_act of
+    adaln_modulate(X). Returns (Xq, x_scale)."""
+    return quant_act(adaln_modulate(X, shift, scale, M, K, eps), inv_lam, M, K)
 
 
 def gemm_i32(Xq, Wq, M: int, N: int, K: int) -> np.ndarray:

@@ -42,6 +42,10 @@
  *     weights of a row; d = RN16(min(RN32(amax / 127), 65504)), codes
  *     clamp(rint(w * RN32(1 / d)), -127, 127) with the stored d (all zero when
  *     d is 0); a weight reads back as bf16(d * q);
+ *   - adaLN modulation before a quantized linear: LayerNorm without affine
+ *     terms over the features, times (1 + scale), plus shift, in binary64,
+ *     rounded once to bf16; the W8A8 activation quantization then runs on
+ *     that bf16 tensor unchanged;
  *   - GGUF Q4_K (same passage; the paper's encoder is its own and is not
  *     spelled out): round to nearest on a min-max grid per sub-block of 32,
  *     6-bit sub-block scales and offsets against binary16 super-block scales
@@ -232,6 +236,40 @@ void oracle_quant_act(const uint16_t *X, const float *inv_lambda, int64_t M,
 #pragma omp parallel for schedule(static)
     for (t = 0; t < M; ++t)
         smooth_quantize_row(X + t * K, inv_lambda, K, Xq + t * K, &x_scale[t]);
+}
+
+/* adaLN modulation of a DiT block's input (the runtime-generated
+ * modulation that Section 2 names as the reason smoothing is applied at
+ * run time): h = LayerNorm(x) * (1 + scale) + shift per token, the norm over
+ * the K features with no affine terms, then rounded once to bf16, the dtype
+ * the model runs in. In binary64, in this order:
+ *   mean = sum_k x_k / K,  var = sum_k (x_k - mean)^2 / K  (two passes),
+ *   rstd = 1 / sqrt(var + eps),
+ *   h_k = bf16(((x_k - mean) * rstd) * (1 + scale_k) + shift_k).
+ * X [M][K], shift [K], scale [K] bf16 -> H [M][K] bf16. */
+void oracle_adaln_modulate(const uint16_t *X, const uint16_t *shift, const uint16_t *scale,
+                           int64_t M, int64_t K, double eps, uint16_t *H)
+{
+    int64_t t;
+#pragma omp parallel for schedule(static)
+    for (t = 0; t < M; ++t) {
+        const uint16_t *x = X + t * K;
+        double sum = 0.0, ss = 0.0, mean, rstd;
+        int64_t k;
+        for (k = 0; k < K; ++k)
+            sum += (double)bf16_to_float(x[k]);
+        mean = sum / (double)K;
+        for (k = 0; k < K; ++k) {
+            const double c = (double)bf16_to_float(x[k]) - mean;
+            ss += c * c;
+        }
+        rstd = 1.0 / sqrt(ss / (double)K + eps);
+        for (k = 0; k < K; ++k) {
+            const double n = ((double)bf16_to_float(x[k]) - mean) * rstd;
+            const double m = n * (1.0 + (double)bf16_to_float(scale[k]));
+            H[t * K + k] = double_to_bf16(m + (double)bf16_to_float(shift[k]));
+        }
+    }
 }
 
 /* ------------------------------------------------------------------ */

@@ -70,6 +70,14 @@ MUTANTS = {
     "q4_k_min_not_clamped_to_zero": ("float lo = 0.0f, hi = -INFINITY;", "float lo = INFINITY, hi = -INFINITY;"),
     "q4_k_decode_drops_offset": ("const float v = s * q - o;", "const float v = s * q;"),
     "q4_k_no_code_clamp": ("            if (c > 15.0f)\n                c = 15.0f;\n", ""),
+    "adaln_sample_variance": ("rstd = 1.0 / sqrt(ss / (double)K + eps);", "rstd = 1.0 / sqrt(ss / (double)(K - 1) + eps);"),
+    "adaln_eps_outside_root": ("rstd = 1.0 / sqrt(ss / (double)K + eps);", "rstd = 1.0 / (sqrt(ss / (double)K) + eps);"),
+    "adaln_scale_without_one": ("const double m = n * (1.0 + (double)bf16_to_float(scale[k]));",
+                                "const double m = n * (double)bf16_to_float(scale[k]);"),
+    "adaln_shift_scale_swapped": ("const double m = n * (1.0 + (double)bf16_to_float(scale[k]));\n            H[t * K + k] = double_to_bf16(m + (double)bf16_to_float(shift[k]));",
+                                  "const double m = n * (1.0 + (double)bf16_to_float(shift[k]));\n            H[t * K + k] = double_to_bf16(m + (double)bf16_to_float(scale[k]));"),
+    "adaln_uncentered_variance": ("const double c = (double)bf16_to_float(x[k]) - mean;", "const double c = (double)bf16_to_float(x[k]);"),
+    "adaln_not_centered": ("const double n = ((double)bf16_to_float(x[k]) - mean) * rstd;", "const double n = (double)bf16_to_float(x[k]) * rstd;"),
     "moments_drops_last_row": ("    for (t = 0; t < M; ++t) {\n        s2 += r2[t];",
                                "    for (t = 0; t + 1 < M; ++t) {\n        s2 += r2[t];"),
 }
@@ -102,6 +110,9 @@ PINS = [
     pins.test_q8_0_exact_grid_and_ties,
     pins.test_q8_0_special_blocks,
     pins.test_q8_0_dequantize_is_one_rounding,
+    pins.test_adaln_matches_torch_layer_norm_fp64,
+    pins.test_adaln_special_rows_and_modulation,
+    pins.test_adaln_eps_enters_under_the_root,
     pins.test_q4_k_exact_grid_round_trip,
     pins.test_q4_k_codes_are_nearest_on_the_stored_grid,
     pins.test_q4_k_error_bound_and_scale_ranges,

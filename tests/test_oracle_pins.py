@@ -779,3 +779,78 @@ def test_q4_k_linear_against_numpy_fp64():
     ref = X @ bf16_to_f64(Wd).reshape(40, 512).T + bf16_to_f64(c["bias"])[None, :]
     y = bf16_to_f64(Y).reshape(33, 40)
     assert np.all(np.abs(y - ref) <= np.abs(ref) * 2.0 ** -8 + 1e-30)
+
+
+# --------------------------------------------------------------------------
+# adaLN modulation ahead of the activation quantization (Section 2: the
+# modulation is generated at run time, so smoothing stays a runtime step)
+# --------------------------------------------------------------------------
+
+def _adaln_case(seed, M, K):
+    rng = np.random.default_rng(seed)
+    X = rng.normal(0, 1, (M, K)).astype(np.float32)
+    X[:, rng.choice(K, max(1, K // 100), replace=False)] *= 20     # outlier channels
+    X[M // 2:] += rng.normal(0, 3, (M - M // 2, 1)).astype(np.float32)   # row offsets
+    shift = rng.normal(0, 0.05, K).astype(np.float32)
+    scale = rng.normal(0, 0.1, K).astype(np.float32)
+    return synth.to_bf16_bits(X), synth.to_bf16_bits(shift), synth.to_bf16_bits(scale)
+
+
+def test_adaln_matches_torch_layer_norm_fp64():
+    """Against torch's float64 layer_norm (its own mean, variance and eps
+    handling), times (1 + scale) plus shift, rounded once to bf16 by exact
+    rational rounding. Catches a sample variance, eps outside the root, a
+    missing centering, '1 + scale' as 'scale', and shift/scale swapped."""
+    import torch
+    M, K = 12, 384
+    X, shift, scale = _adaln_case(170, M, K)
+    eps = 1e-6
+    H = oracle.adaln_modulate(X, shift, scale, M, K, eps)
+    x = torch.from_numpy(bf16_to_f64(X).reshape(M, K))
+    ln = torch.nn.functional.layer_norm(x, (K,), eps=eps)
+    ref = ln * (1 + torch.from_numpy(bf16_to_f64(scale))) + torch.from_numpy(bf16_to_f64(shift))
+    want = np.array([[round_bf16_exact(float(v)) for v in row] for row in ref.numpy()], np.uint16)
+    assert np.array_equal(H, want)
+
+
+def test_adaln_special_rows_and_modulation():
+    """A constant row normalizes to zero, so it reads back as bf16(shift)
+    exactly; scale = -1 cancels the norm everywhere; with shift = scale = 0
+    and eps = 0 every row has mean ~0 and population variance ~1."""
+    M, K = 6, 256
+    X, shift, scale = _adaln_case(171, M, K)
+    Xc = X.copy()
+    Xc[0] = Xc[0, 0]
+    H = oracle.adaln_modulate(Xc, shift, scale, M, K, 1e-6)
+    assert np.array_equal(H[0], shift)
+    minus_one = np.full(K, 0xBF80, np.uint16)
+    assert np.array_equal(oracle.adaln_modulate(X, shift, minus_one, M, K, 1e-6),
+                          np.broadcast_to(shift, (M, K)))
+    zero = np.zeros(K, np.uint16)
+    h = bf16_to_f64(oracle.adaln_modulate(X, zero, zero, M, K, 0.0)).reshape(M, K)
+    assert np.all(np.abs(h.mean(axis=1)) < 2e-3)
+    assert np.allclose(h.var(axis=1), 1.0, atol=5e-3)
+
+
+def test_adaln_eps_enters_under_the_root():
+    """A row of +-a has variance a^2 exactly, so x - mean = +-a and the norm
+    is a / sqrt(a^2 + eps): with a = 2^-10 and eps = 3 * 2^-20 it is exactly
+    1/2 (no rounding anywhere)."""
+    K = 64
+    a = 2.0 ** -10
+    X = synth.to_bf16_bits(np.tile(np.array([a, -a], np.float32), K // 2)[None, :])
+    zero = np.zeros(K, np.uint16)
+    h = bf16_to_f64(oracle.adaln_modulate(X, zero, zero, 1, K, 3 * 2.0 ** -20))
+    assert np.array_equal(h.reshape(K), np.tile([0.5, -0.5], K // 2))
+
+
+def test_adaln_quant_act_is_quant_act_of_the_modulated_row():
+    M, K = 8, 256
+    X, shift, scale = _adaln_case(172, M, K)
+    il = np.random.default_rng(173).uniform(0.5, 2.0, K).astype(np.float32)
+    Xq, xs = oracle.adaln_quant_act(X, shift, scale, il, M, K, 1e-6)
+    H = bf16_to_f64(oracle.adaln_modulate(X, shift, scale, M, K, 1e-6)).reshape(M, K)
+    v = (H.astype(np.float32) * il).astype(np.float64)
+    amax = np.abs(v).max(axis=1)
+    assert np.allclose(xs, amax / 127, rtol=2.0 ** -23)
+    assert np.all(np.abs(Xq * xs[:, None].astype(np.float64) - v) <= xs[:, None] * QUANT_SLACK)

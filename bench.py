@@ -71,6 +71,14 @@ class Linear:
         self.xs = xs
         self.M = xs[0].shape[0]
         self.Y = torch.empty(self.M, lay.N, dtype=torch.bfloat16, device=xs[0].device)
+        self.mod = None   # (shift, scale) bf16 [K]: the input is adaLN-modulated first
+
+    def quant(self, X, Xq, xs):
+        """The activation step of this layer (fused with adaLN if modulated)."""
+        if self.mod is None:
+            return ops.w8a8_quant_act(X, self.lay.inv_lambda, Xq=Xq, x_scale=xs)
+        return ops.w8a8_adaln_quant_act(X, self.mod[0], self.mod[1], self.lay.inv_lambda,
+                                        Xq=Xq, x_scale=xs)
 
     @property
     def ops(self) -> int:
@@ -143,6 +151,13 @@ def build_workload(name: str, dev, pool: int):
         return [lin]
     if name == "ffn_up":
         return [host_case_linear("ffn_up", synth.ffn_up_case(), dev, pool, False, 2)]
+    if name == "adaln_ffn_up":
+        c = synth.ffn_up_case()
+        lin = host_case_linear("adaln_ffn_up", c, dev, pool, False, 2)
+        rng = np.random.default_rng([2, 77])
+        lin.mod = tuple(to_dev_bf16(synth.to_bf16_bits(rng.normal(0, sd, c["K"]).astype(np.float32)), dev)
+                        for sd in (0.05, 0.1))
+        return [lin]
     if name == "ffn_down":
         c = synth.ffn_down_case()
         return [host_case_linear("ffn_down_w8a8", c, dev, pool, False, 3),
@@ -201,7 +216,7 @@ def run_step(layers, it: int, ws: L.Workspace, events=None):
             Xq, xs = ws.get(lin.M, lin.lay.K)
             if events is not None:
                 events[li][0].record()
-            ops.w8a8_quant_act(X, lin.lay.inv_lambda, Xq=Xq, x_scale=xs)
+            lin.quant(X, Xq, xs)
             if events is not None:
                 events[li][1].record()
             ops.w8a8_linear(Xq, xs, lin.lay.Wq, lin.lay.w_scale, lin.lay.bias, out=lin.Y)
@@ -261,7 +276,7 @@ def quant_isolated(lin: Linear, dev, reps: int = 60, rounds: int = 5):
     qs = [torch.empty(M, K, dtype=torch.int8, device=dev) for _ in range(nbuf)]
     sc = torch.empty(M, dtype=torch.float32, device=dev)
     for i in range(nbuf):
-        ops.w8a8_quant_act(xs[i], lin.lay.inv_lambda, Xq=qs[i], x_scale=sc)
+        lin.quant(xs[i], qs[i], sc)
     torch.cuda.synchronize()
     per = []
     for _ in range(rounds):
@@ -270,7 +285,7 @@ def quant_isolated(lin: Linear, dev, reps: int = 60, rounds: int = 5):
         a.record()
         for r in range(reps):
             i = r % nbuf
-            ops.w8a8_quant_act(xs[i], lin.lay.inv_lambda, Xq=qs[i], x_scale=sc)
+            lin.quant(xs[i], qs[i], sc)
         b.record()
         torch.cuda.synchronize()
         per.append(a.elapsed_time(b) * 1e3 / reps)
@@ -335,6 +350,15 @@ def quant_bytes(M, K) -> int:
     """Algorithmic bytes of one quant launch: read X (bf16) and inv_lambda,
     write Xq (int8) and x_scale."""
     return 2 * M * K + M * K + 4 * M + 4 * K
+
+
+def quant_name_bytes(lin) -> tuple[str, int]:
+    """Name and algorithmic bytes of a layer's activation step; the adaLN
+    version also reads the two bf16 modulation vectors."""
+    M, K = lin.M, lin.lay.K
+    if lin.mod is None:
+        return "w8a8_quant_act", quant_bytes(M, K)
+    return "w8a8_adaln_quant_act", quant_bytes(M, K) + 4 * K
 
 
 def dequant_bytes(fmt: str, N: int, K: int) -> int:
@@ -499,7 +523,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="ffn_up",
                     choices=["ffn_up", "ffn_down", "dit_block", "backbone", "q8_0_ffn_up",
-                             "q4_k_ffn_up"])
+                             "q4_k_ffn_up", "adaln_ffn_up"])
     ap.add_argument("--pool", type=int, default=4, help="distinct inputs rotated over steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -567,9 +591,10 @@ def main():
         kernels[f"w8a8_linear_{M}x{K}x{N}"] = {
             "us": round(g, 2), "TOPS": round(2 * M * N * K / g / 1e6, 1),
             "frac_int8_peak": round(2 * M * N * K / g / 1e6 / PEAK_INT8_TOPS, 4), "count": len(idx)}
-        kernels[f"w8a8_quant_act_{M}x{K}_in_step"] = {
-            "us": round(q, 2), "GB_s": round(quant_bytes(M, K) / q / 1e3, 1),
-            "frac_hbm": round(quant_bytes(M, K) / q / 1e3 / PEAK_HBM_GBS, 4)}
+        qname, qb = quant_name_bytes(layers[idx[0]])
+        kernels[f"{qname}_{M}x{K}_in_step"] = {
+            "us": round(q, 2), "GB_s": round(qb / q / 1e3, 1),
+            "frac_hbm": round(qb / q / 1e3 / PEAK_HBM_GBS, 4)}
     for shape_key in sorted({(layers[i].M, layers[i].lay.N, layers[i].lay.K) for i in prot}):
         idx = [i for i in prot if (layers[i].M, layers[i].lay.N, layers[i].lay.K) == shape_key]
         M, N, K = shape_key
@@ -586,8 +611,8 @@ def main():
             continue
         seen.add(lin.lay.K)
         med, lo, hi = quant_isolated(lin, dev)
-        by = quant_bytes(lin.M, lin.lay.K)
-        kernels[f"w8a8_quant_act_{lin.M}x{lin.lay.K}_hbm"] = {
+        qname, by = quant_name_bytes(lin)
+        kernels[f"{qname}_{lin.M}x{lin.lay.K}_hbm"] = {
             "us": round(med, 2), "us_min": round(lo, 2), "us_max": round(hi, 2),
             "GB_s": round(by / med / 1e3, 1), "frac_hbm": round(by / med / 1e3 / PEAK_HBM_GBS, 4),
             "bytes": by}
@@ -634,10 +659,11 @@ def main():
                         "ffn_down": "DiT FFN down-projection 4608x16384->4096, W8A8 and protected bf16",
                         "dit_block": "one DiT block (qkv, attn_out, ffn_up, ffn_down protected), both CFG branches",
                         "backbone": "211 linears x 2 branches, 17 protected per branch",
+                        "adaln_ffn_up": "DiT FFN up-projection 4608x4096->16384 behind its adaLN modulation (fused into the activation quantization)",
                         "q8_0_ffn_up": "DiT FFN up-projection 4608x4096->16384 with GGUF Q8_0 weights",
                         "q4_k_ffn_up": "DiT FFN up-projection 4608x4096->16384 with GGUF Q4_K weights"}[args.workload],
            "tokens": M0, "linears": len(layers), "protected": len(prot),
-           "input_pool": args.pool if args.workload in ("ffn_up", "ffn_down") else None,
+           "input_pool": args.pool if args.workload in ("ffn_up", "ffn_down", "adaln_ffn_up") else None,
            "smoothquant_alpha": 0.5}
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TOPS", "n_gpus": 1,

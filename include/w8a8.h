@@ -137,6 +137,25 @@ w8a8_status w8a8_quant_act(const uint16_t *X, const float *inv_lambda,
                            int64_t M, int64_t K, int8_t *Xq, float *x_scale,
                            w8a8_stream stream);
 
+/* The same activation step on the adaLN-modulated input of a DiT block's QKV
+ * or FFN-up projection (Section 2: the modulation is generated at run time,
+ * which is why smoothing is applied at run time), fused so that the
+ * modulated tensor never goes to memory. Per token row t, in binary64:
+ *   mean = sum_k X[t][k] / K,  var = sum_k (X[t][k] - mean)^2 / K,
+ *   rstd = 1 / sqrt(var + eps),
+ *   H[t][k] = bf16(((X[t][k] - mean) * rstd) * (1 + scale[k]) + shift[k])
+ * (LayerNorm without affine terms, one rounding to bf16); then
+ * exactly w8a8_quant_act(H, inv_lambda). X [M][K], shift [K], scale [K]
+ * bf16, inv_lambda [K] fp32 -> Xq [M][K] int8, x_scale [M] fp32. K must be
+ * a multiple of 64 and at most 8192 (the DiT's modulated inputs have
+ * K = 4096), eps finite and >= 0, else
+ * W8A8_ERR_UNSUPPORTED. Alignment as w8a8_quant_act, shift and scale
+ * 16-byte aligned. */
+w8a8_status w8a8_adaln_quant_act(const uint16_t *X, const uint16_t *shift,
+                                 const uint16_t *scale, const float *inv_lambda,
+                                 int64_t M, int64_t K, double eps, int8_t *Xq,
+                                 float *x_scale, w8a8_stream stream);
+
 /* Steps (3) INT8 GEMM and (4) fused epilogue:
  *   acc[t][n] = sum_k Xq[t][k] * Wq[n][k]   (exact int32),
  *   Y[t][n]   = bf16_rne(float(acc) * (x_scale[t] * w_scale[n]) + bias[n])

@@ -39,6 +39,7 @@ SIGNATURES = {
     "q8_0_quantize": ([_P, _I64, _I64, _P, _P, _P], _S),
     "q8_0_dequantize": ([_P, _P, _I64, _I64, _P, _P], _S),
     "q8_0_linear": ([_P, _P, _P, _P, _I64, _I64, _I64, _P, _P, _P], _S),
+    "w8a8_adaln_quant_act": ([_P, _P, _P, _P, _I64, _I64, ctypes.c_double, _P, _P, _P], _S),
     "q4_k_quantize": ([_P, _I64, _I64, _P, _P, _P, _P, _P, _P], _S),
     "q4_k_dequantize": ([_P, _P, _P, _P, _P, _I64, _I64, _P, _P], _S),
     "q4_k_linear": ([_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P, _P, _P], _S),

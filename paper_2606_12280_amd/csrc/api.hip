@@ -4,6 +4,8 @@
 #include "../../include/w8a8.h"
 
 #include <hip/hip_runtime.h>
+
+#include <cmath>
 #include <stdint.h>
 #include <stdio.h>
 #include <string.h>
@@ -156,6 +158,24 @@ w8a8_status w8a8_quant_act(const uint16_t *X, const float *inv_lambda, int64_t M
     W8A8_TRY(check_alias({{Xq, M * K}, {x_scale, 4 * M}}, {{X, 2 * M * K}, {inv_lambda, 4 * K}}));
     return hip_status(
         w8a8::launch_smooth_quant_rows(X, inv_lambda, M, K, Xq, x_scale, as_stream(stream)));
+}
+
+w8a8_status w8a8_adaln_quant_act(const uint16_t *X, const uint16_t *shift, const uint16_t *scale,
+                                 const float *inv_lambda, int64_t M, int64_t K, double eps,
+                                 int8_t *Xq, float *x_scale, w8a8_stream stream) {
+    if (X == nullptr || shift == nullptr || scale == nullptr || inv_lambda == nullptr ||
+        Xq == nullptr || x_scale == nullptr)
+        return W8A8_ERR_NULL;
+    W8A8_TRY(check_rows(M, kMaxRows));
+    W8A8_TRY(check_k(K));
+    if (K > 8192 || !(eps >= 0.0) || !std::isfinite(eps)) return W8A8_ERR_UNSUPPORTED;
+    if (!aligned(X, 16) || !aligned(shift, 16) || !aligned(scale, 16) || !aligned(Xq, 16) ||
+        !aligned(inv_lambda, 16) || !aligned(x_scale, 4))
+        return W8A8_ERR_ALIGN;
+    W8A8_TRY(check_alias({{Xq, M * K}, {x_scale, 4 * M}},
+                         {{X, 2 * M * K}, {shift, 2 * K}, {scale, 2 * K}, {inv_lambda, 4 * K}}));
+    return hip_status(w8a8::launch_adaln_quant_act(X, shift, scale, inv_lambda, M, K, eps, Xq,
+                                                   x_scale, as_stream(stream)));
 }
 
 w8a8_status w8a8_linear(const int8_t *Xq, const float *x_scale, const int8_t *Wq,

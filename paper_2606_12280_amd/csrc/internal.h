@@ -37,6 +37,14 @@ hipError_t launch_q8_0_quantize(const uint16_t *W, int64_t N, int64_t K, int8_t 
 hipError_t launch_q8_0_dequantize(const int8_t *qs, const uint16_t *d, int64_t N, int64_t K,
                                   uint16_t *W, hipStream_t stream);
 
+// adaLN-modulated activation quantization: Xq, x_scale of
+// quant_act(bf16(LayerNorm(X) * (1 + scale) + shift), inv_lambda), the norm
+// in binary64 (64 | K, K <= 8192).
+hipError_t launch_adaln_quant_act(const uint16_t *X, const uint16_t *shift,
+                                  const uint16_t *scale, const float *inv_lambda, int64_t M,
+                                  int64_t K, double eps, int8_t *Xq, float *x_scale,
+                                  hipStream_t stream);
+
 // GGUF Q4_K (256 | K): W [N][K] bf16 -> codes qs [N][K/2] (two per byte,
 // even k low), 6-bit sub-block scales sc and offsets mn [N][K/32] (bytes),
 // binary16 super-block scales d and dmin [N][K/256]; and back to

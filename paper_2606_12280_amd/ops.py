@@ -133,6 +133,26 @@ def w8a8_quant_act(X: torch.Tensor, inv_lambda: torch.Tensor, Xq=None, x_scale=N
     return Xq, x_scale
 
 
+def w8a8_adaln_quant_act(X: torch.Tensor, shift: torch.Tensor, scale: torch.Tensor,
+                         inv_lambda: torch.Tensor, eps: float = 1e-6, Xq=None, x_scale=None):
+    """adaLN modulation (LayerNorm(X) * (1 + scale) + shift, rounded to bf16)
+    fused with smooth + per-token quantize -> (Xq int8 [M, K], x_scale fp32 [M])."""
+    _need(X, "X", torch.bfloat16, 2)
+    M, K = X.shape
+    dev = X.device
+    for name, t in (("shift", shift), ("scale", scale)):
+        _need(t, name, torch.bfloat16, 1, dev)
+    _need(inv_lambda, "inv_lambda", torch.float32, 1, dev)
+    Xq = _out(Xq, (M, K), torch.int8, dev, "Xq")
+    x_scale = _out(x_scale, (M,), torch.float32, dev, "x_scale")
+    lib = load()
+    with torch.cuda.device(dev):
+        check("w8a8_adaln_quant_act",
+              lib.w8a8_adaln_quant_act(_ptr(X), _ptr(shift), _ptr(scale), _ptr(inv_lambda), M, K,
+                                       float(eps), _ptr(Xq), _ptr(x_scale), _stream(dev)))
+    return Xq, x_scale
+
+
 def w8a8_linear(Xq: torch.Tensor, x_scale: torch.Tensor, Wq: torch.Tensor,
                 w_scale: torch.Tensor, bias: torch.Tensor | None = None,
                 out: torch.Tensor | None = None) -> torch.Tensor:

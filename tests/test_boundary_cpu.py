@@ -175,6 +175,22 @@ def test_q4_k_validation(lib):
     assert f(A, B, C, D, E, F, None, 0, 8, 256, G, 0x7F0700000000, None) == SHAPE
 
 
+def test_adaln_validation(lib):
+    f = lib.w8a8_adaln_quant_act
+    assert f(None, B, C, D, 4, 64, 1e-6, E, E + 4096, None) == NULL
+    assert f(A, B, None, D, 4, 64, 1e-6, E, E + 4096, None) == NULL
+    assert f(A, B, C, D, 0, 64, 1e-6, E, E + 4096, None) == SHAPE
+    assert f(A, B, C, D, 4, 96, 1e-6, E, E + 4096, None) == UNSUP          # K % 64 != 0
+    assert f(A, B, C, D, 4, 8256, 1e-6, E, E + 65536, None) == UNSUP       # K > 8192
+    assert f(A, B, C, D, 4, 64, -1e-6, E, E + 4096, None) == UNSUP
+    assert f(A, B, C, D, 4, 64, float("nan"), E, E + 4096, None) == UNSUP
+    assert f(A, B, C, D, 4, 64, float("inf"), E, E + 4096, None) == UNSUP
+    assert f(A, B + 2, C, D, 4, 64, 1e-6, E, E + 4096, None) == ALIGN      # shift
+    assert f(A, B, C, D, 4, 64, 1e-6, E, E + 2, None) == ALIGN             # x_scale
+    assert f(A, B, C, D, 4, 64, 1e-6, A, E + 4096, None) == ALIAS          # Xq over X
+    assert f(A, B, C, D, 4, 64, 1e-6, E, C + 64, None) == ALIAS            # x_scale in scale
+
+
 def test_binding_rejects_host_tensors():
     X = torch.zeros(4, 64, dtype=torch.bfloat16)
     il = torch.ones(64)

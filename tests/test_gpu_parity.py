@@ -569,3 +569,55 @@ def test_q4_k_full_size_ffn_up():
     Y = host_bits(ops.q4_k_linear(dev_bf16(X), q, dev_bf16(c["bias"])))
     rows = np.random.default_rng(163).choice(M, 24, replace=False)
     check_bf16_output(Y[rows], X[rows], oracle.q4_k_dequantize(ref, N, K), c["bias"])
+
+
+# --------------------------------------------------------------------------
+# adaLN modulation fused into the activation quantization (Section 2: the
+# modulation is generated at run time)
+# --------------------------------------------------------------------------
+
+def _adaln_inputs(seed, M, K):
+    rng = np.random.default_rng(seed)
+    X = rng.normal(0, 1, (M, K)).astype(np.float32)
+    X[:, rng.choice(K, max(1, K // 100), replace=False)] *= 20      # outlier channels
+    X[M // 2:] += rng.normal(0, 3, (M - M // 2, 1)).astype(np.float32)
+    shift = rng.normal(0, 0.05, K).astype(np.float32)
+    scale = rng.normal(0, 0.1, K).astype(np.float32)
+    il = rng.uniform(0.25, 4.0, K).astype(np.float32)
+    return synth.to_bf16_bits(X), synth.to_bf16_bits(shift), synth.to_bf16_bits(scale), il
+
+
+def _check_adaln(X, shift, scale, il, M, K, eps=1e-6):
+    Xq_ref, xs_ref = oracle.adaln_quant_act(X, shift, scale, il, M, K, eps)
+    Xq, xs = ops.w8a8_adaln_quant_act(dev_bf16(X), dev_bf16(shift), dev_bf16(scale), dev(il), eps)
+    assert np.array_equal(host(xs).view(np.uint32), xs_ref.view(np.uint32))
+    assert np.array_equal(host(Xq), Xq_ref)
+
+
+@pytest.mark.parametrize("M,K", [(1, 64), (5, 256), (33, 1088), (300, 2112), (257, 4096),
+                                 (64, 8192)])
+def test_adaln_quant_act_bit_exact(M, K):
+    _check_adaln(*_adaln_inputs([180, M, K], M, K), M, K)
+
+
+def test_adaln_quant_act_special_rows():
+    """Constant rows (the norm is 0, so they code bf16(shift)), all-zero rows
+    with zero shift (scale 0, zero codes), scale = -1 on some columns, a row
+    with a large offset, and eps = 0."""
+    M, K = 8, 512
+    X, shift, scale, il = _adaln_inputs(181, M, K)
+    X[0] = X[0, 5]
+    X[1] = 0
+    scale[:64] = 0xBF80                                        # -1
+    Xf = bf16_to_f64(X).reshape(M, K).astype(np.float32)
+    Xf[2] += 1000.0
+    X = synth.to_bf16_bits(Xf)
+    _check_adaln(X, shift, scale, il, M, K)
+    _check_adaln(X, np.zeros(K, np.uint16), scale, il, M, K)
+    _check_adaln(X, shift, scale, il, M, K, eps=0.0)
+
+
+def test_adaln_quant_act_full_size():
+    """The FFN-up / QKV input of a DiT block, 4608 x 4096, whole tensor."""
+    M, K = 4608, 4096
+    _check_adaln(*_adaln_inputs(182, M, K), M, K)

@@ -394,17 +394,27 @@ def cpu_baseline(workload: str, target_s: float = 10.0):
         oracle.w8a8_linear(Xq, xs, Wq, ws, c["bias"], rows, N, K)
         return time.perf_counter() - t
 
-    probe = 16
-    dt = run(probe)
-    rows = int(min(M, max(probe, probe * target_s / max(dt, 1e-6))))
-    rows = max(probe, rows // 16 * 16)
-    dt = run(rows)
-    tops = 2.0 * rows * N * K / dt / 1e12
+    # Size the sample from a small probe, then once more from a mid-sized
+    # run (a 16-row probe overstates the per-row time on many cores); if the
+    # whole linear takes less than target_s, time it repeatedly (at most 3x).
+    rows, dt = 16, run(16)
+    for _ in range(2):
+        if rows >= M or dt >= 0.8 * target_s:
+            break
+        rows = int(min(M, max(16, rows * target_s / max(dt, 1e-6))))
+        rows = max(16, rows // 16 * 16)
+        dt = run(rows)
+    reps = 1
+    while rows >= M and dt < target_s and reps < 3:
+        dt += run(rows)
+        reps += 1
+    tops = 2.0 * rows * N * K * reps / dt / 1e12
+    what = f"{rows} of {M} token rows" if reps == 1 else f"{reps} runs of all {M} token rows"
     return {"value": round(tops, 6), "unit": "TOPS", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"{rows} of {M} token rows of the {M}x{K}->{N} linear: smoothing + "
-                      f"per-token quant + int32 GEMM + bf16 epilogue (weights prepared "
-                      f"outside the timing), {dt:.1f} s"}
+            "sample": f"{what} of the {M}x{K}->{N} linear: smoothing + per-token quant + "
+                      f"int32 GEMM + bf16 epilogue (weights prepared outside the timing), "
+                      f"{dt:.1f} s"}
 
 
 # --------------------------------------------------------------------------

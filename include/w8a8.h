@@ -52,7 +52,7 @@ typedef enum w8a8_status {
     W8A8_ERR_SHAPE = 2,       /* a size is out of range */
     W8A8_ERR_ALIGN = 3,       /* a pointer is not aligned as required */
     W8A8_ERR_ALIAS = 4,       /* an output overlaps an input or another output */
-    W8A8_ERR_UNSUPPORTED = 5, /* a valid request this build does not handle
+    W8A8_ERR_UNSUPPORTED = 5, /* a valid request this library does not handle
                                  (K not a multiple of 64, K > 65536, alpha
                                  outside (0, 1)) */
     W8A8_ERR_HIP = 6          /* the HIP runtime reported an error */

@@ -62,8 +62,10 @@ __device__ __forceinline__ void widen8(const uint4 &x, float (&v)[8]) {
 
 // bf16 bits of a binary32 value, round to nearest even (v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t bf16_pair(float a, float b) {
-    return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(a))) |
-           static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(b))) << 16;
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    // one v_cvt_pk_bf16_f32 (round to nearest even), a in the low half
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2));
 }
 
 // Nearest bf16 to a finite binary64 value in one rounding, given f, its

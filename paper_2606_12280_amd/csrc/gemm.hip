@@ -69,8 +69,13 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, ui
                                              kBufferWord3);
 }
 
-__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-    return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));  // v_cvt_pk_bf16_f32 (RNE)
+// Two values to bf16 in one v_cvt_pk_bf16_f32 (round to nearest even), a in
+// the low half. Converting them one at a time costs two conversions plus a
+// shift and an or.
+__device__ __forceinline__ uint32_t f32x2_to_bf16x2(float a, float b) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2));
 }
 
 // s_waitcnt with only vmcnt constrained (gfx9 encoding: vmcnt[3:0] in bits
@@ -302,22 +307,23 @@ struct Epi {
                             }
                         }
                     } else {
-                        uint32_t h[4];
+                        float y[4];
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
                             const float a = static_cast<float>(acc[i][j][4 * g + e]);
                             const uint32_t bw = b_[i][g][e >> 1];
                             const float b =
                                 __uint_as_float((e & 1) ? (bw & 0xffff0000u) : (bw << 16));
-                            float y;
                             if constexpr (EPI == kDequantBf16)
-                                y = __builtin_fmaf(a, xs_[j] * ws_[i][g][e], b);
+                                y[e] = __builtin_fmaf(a, xs_[j] * ws_[i][g][e], b);
                             else
-                                y = a + b;
-                            h[e] = f32_to_bf16_bits(y);
+                                y[e] = a + b;
                         }
+                        const uint32_t p01 = f32x2_to_bf16x2(y[0], y[1]);
+                        const uint32_t p23 = f32x2_to_bf16x2(y[2], y[3]);
+                        const uint32_t h[4] = {p01 & 0xffffu, p01 >> 16, p23 & 0xffffu, p23 >> 16};
                         if (N_VEC && n + 3 < N) {
-                            const v2u v = {h[0] | h[1] << 16, h[2] | h[3] << 16};
+                            const v2u v = {p01, p23};
                             __builtin_amdgcn_raw_buffer_store_b64(v, ry, (row_off + n) * 2u, 0, 0);
                         } else {
 #pragma unroll
@@ -356,23 +362,21 @@ struct Epi {
             for (int i = 0; i < TI; ++i)
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
-                    uint32_t h[4];
+                    float y[4];
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const float a = static_cast<float>(acc[i][j][4 * g + e]);
                         const uint32_t bw = b_[i][g][e >> 1];
                         const float b = __uint_as_float((e & 1) ? (bw & 0xffff0000u) : (bw << 16));
-                        float y;
                         if constexpr (EPI == kDequantBf16)
-                            y = __builtin_fmaf(a, xs_[j] * ws_[i][g][e], b);
+                            y[e] = __builtin_fmaf(a, xs_[j] * ws_[i][g][e], b);
                         else
-                            y = a + b;
-                        h[e] = f32_to_bf16_bits(y);
+                            y[e] = a + b;
                     }
                     const int t = 32 * j + frow;
                     const int c = 32 * i + 8 * g + 4 * fhalf;
                     *reinterpret_cast<v2u *>(stage + t * kRowStride + c * 2) =
-                        v2u{h[0] | h[1] << 16, h[2] | h[3] << 16};
+                        v2u{f32x2_to_bf16x2(y[0], y[1]), f32x2_to_bf16x2(y[2], y[3])};
                 }
         constexpr int CPR = 64 * TI / 16;  // 16-byte chunks per row
         constexpr int ROUNDS = 32 * TJ * CPR / 64;

@@ -26,6 +26,7 @@
 #include <stdint.h>
 
 #include "internal.h"
+#include "wave_reduce.h"
 
 namespace w8a8 {
 namespace {
@@ -83,17 +84,8 @@ __device__ __forceinline__ uint32_t bf16_bits_past_midpoint(double d, float f) {
     return fabs(d) > fabs(static_cast<double>(f)) ? t + 1 : t;
 }
 
-__device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-    return v;
-}
-
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
-    return v;
-}
+__device__ __forceinline__ double wave_sum(double v) { return lanes::sum(v); }
+__device__ __forceinline__ float wave_max(float v) { return lanes::max(v); }
 
 __device__ __forceinline__ uint32_t code(float v, float r) {
     float c = rintf(v * r);

@@ -22,6 +22,7 @@
 #include <stdint.h>
 
 #include "internal.h"
+#include "wave_reduce.h"
 
 namespace w8a8 {
 namespace {
@@ -31,11 +32,7 @@ constexpr float kTinyAbsmax = 0x1p-96f;  // rows below quantize to zero
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
-    return v;
-}
+__device__ __forceinline__ float wave_max(float v) { return lanes::max(v); }
 
 // One code: clamp(rint(v * r), -127, 127) packed into the low byte.
 __device__ __forceinline__ uint32_t code(float v, float r) {

@@ -274,13 +274,14 @@ hipError_t launch_smooth_quant_rows(const uint16_t *src, const float *mul, int64
                                     int64_t K, int8_t *out, float *scale,
                                     hipStream_t stream) {
     // A group covers 512 * G * CH columns; take the smallest that holds K.
-    // Up to K = 32768 a group has at most 8 waves and walks two rows (the
-    // second one prefetched); the K = 65536 group of 16 waves has no register
-    // room for a prefetched row and walks one.
+    // Up to K = 32768 a group has at most 8 waves and walks two rows (each
+    // next one prefetched); at K = 4096 three (4608 x 4096: 11.96 against
+    // 12.91 us for two, in one job). The K = 65536 group of 16 waves has no
+    // register room for a prefetched row and walks one.
     if (K <= 512) return launch_rows<1, 1, 2, 4>(src, mul, R, K, out, scale, stream);
     if (K <= 1024) return launch_rows<2, 1, 2, 4>(src, mul, R, K, out, scale, stream);
     if (K <= 2048) return launch_rows<4, 1, 2, 4>(src, mul, R, K, out, scale, stream);
-    if (K <= 4096) return launch_rows<4, 2, 2, 4>(src, mul, R, K, out, scale, stream);
+    if (K <= 4096) return launch_rows<4, 2, 3, 4>(src, mul, R, K, out, scale, stream);
     if (K <= 8192) return launch_rows<8, 2, 2, 8>(src, mul, R, K, out, scale, stream);
     if (K <= 16384) return launch_rows<8, 4, 2, 8>(src, mul, R, K, out, scale, stream);
     if (K <= 32768) return launch_rows<8, 8, 2, 8>(src, mul, R, K, out, scale, stream);

@@ -621,3 +621,44 @@ def test_adaln_quant_act_full_size():
     """The FFN-up / QKV input of a DiT block, 4608 x 4096, whole tensor."""
     M, K = 4608, 4096
     _check_adaln(*_adaln_inputs(182, M, K), M, K)
+
+
+# --------------------------------------------------------------------------
+# GGUF linears without a bias, with one token, and through the router
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("fmt", ["q8_0", "q4_k"])
+@pytest.mark.parametrize("M,N", [(1, 65), (3, 1)])
+def test_gguf_linear_without_bias_small(fmt, M, N):
+    K = 512
+    c = synth.linear_case([190, M, N, K], M, N, K)
+    W = dev_bf16(c["W"].reshape(N, K))
+    X = c["X"].reshape(M, K)
+    if fmt == "q8_0":
+        qs_ref, d_ref = oracle.q8_0_quantize(c["W"], N, K)
+        Wd = oracle.q8_0_dequantize(qs_ref, d_ref, N, K)
+        qs, d = ops.q8_0_quantize(W)
+        Y = host_bits(ops.q8_0_linear(dev_bf16(X), qs, d, None))
+    else:
+        ref = oracle.q4_k_quantize(c["W"], N, K)
+        Wd = oracle.q4_k_dequantize(ref, N, K)
+        Y = host_bits(ops.q4_k_linear(dev_bf16(X), ops.q4_k_quantize(W), None))
+    check_bf16_output(Y, X, Wd, None)
+
+
+def test_router_runs_gguf_layers_like_the_entry_points():
+    """layer.route on Q8_0 and Q4_K layers (decode into the shared workspace,
+    then the bf16 linear) gives the entry points' outputs bit for bit."""
+    from paper_2606_12280_amd import layer
+    M, N, K = 96, 320, 768
+    c = synth.linear_case([191, M, N, K], M, N, K, act="gelu")
+    X, W, b = dev_bf16(c["X"].reshape(M, K)), dev_bf16(c["W"].reshape(N, K)), dev_bf16(c["bias"])
+    ws = layer.Workspace(DEV)
+    l8 = layer.prepare_q8_0(W, b)
+    l4 = layer.prepare_q4_k(W, b)
+    assert l8.weight_only and l4.weight_only and not l8.protected
+    assert l4.nbytes() < l8.nbytes() < 2 * N * K
+    y8 = host_bits(layer.route(l8, X, ws=ws))
+    y4 = host_bits(layer.route(l4, X, ws=ws))
+    assert np.array_equal(y8, host_bits(ops.q8_0_linear(X, l8.q8_qs, l8.q8_d, b)))
+    assert np.array_equal(y4, host_bits(ops.q4_k_linear(X, l4.q4k, b)))

@@ -33,13 +33,13 @@ SIGNATURES = {
     "w8a8_smooth_factors": ([_P, _P, _I64, _I64, ctypes.c_double, _P, _P], _S),
     "w8a8_prepare_weight": ([_P, _P, _I64, _I64, _P, _P, _P, _P], _S),
     "w8a8_quant_act": ([_P, _P, _I64, _I64, _P, _P, _P], _S),
+    "w8a8_adaln_quant_act": ([_P, _P, _P, _P, _I64, _I64, ctypes.c_double, _P, _P, _P], _S),
     "w8a8_linear": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P, _P], _S),
     "w8a8_gemm_i32": ([_P, _P, _I64, _I64, _I64, _P, _P], _S),
     "bf16_linear": ([_P, _P, _P, _I64, _I64, _I64, _P, _P], _S),
     "q8_0_quantize": ([_P, _I64, _I64, _P, _P, _P], _S),
     "q8_0_dequantize": ([_P, _P, _I64, _I64, _P, _P], _S),
     "q8_0_linear": ([_P, _P, _P, _P, _I64, _I64, _I64, _P, _P, _P], _S),
-    "w8a8_adaln_quant_act": ([_P, _P, _P, _P, _I64, _I64, ctypes.c_double, _P, _P, _P], _S),
     "q4_k_quantize": ([_P, _I64, _I64, _P, _P, _P, _P, _P, _P], _S),
     "q4_k_dequantize": ([_P, _P, _P, _P, _P, _I64, _I64, _P, _P], _S),
     "q4_k_linear": ([_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P, _P, _P], _S),

@@ -662,3 +662,38 @@ def test_router_runs_gguf_layers_like_the_entry_points():
     y4 = host_bits(layer.route(l4, X, ws=ws))
     assert np.array_equal(y8, host_bits(ops.q8_0_linear(X, l8.q8_qs, l8.q8_d, b)))
     assert np.array_equal(y4, host_bits(ops.q4_k_linear(X, l4.q4k, b)))
+
+
+# --------------------------------------------------------------------------
+# A seeded sweep of shapes: every tile configuration the dispatcher can pick
+# (by round fill and by K % 128), ragged M and N, K from 64 to 4160 bytes.
+# --------------------------------------------------------------------------
+
+def _sweep_shapes(n, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        M = int(rng.choice([rng.integers(1, 65), rng.integers(65, 700), rng.integers(2000, 4700)]))
+        N = int(rng.choice([rng.integers(1, 65), rng.integers(65, 1200), rng.integers(4000, 13000)]))
+        K = 64 * int(rng.integers(1, 66))
+        if M * N * K > 6e9:                     # keep the oracle's share to seconds
+            K = 64 * max(1, int(6e9 / (M * N * 64)))
+        out.append((M, N, K))
+    return out
+
+
+@pytest.mark.parametrize("M,N,K", _sweep_shapes(24, 195))
+def test_w8a8_linear_shape_sweep(M, N, K):
+    """int32 accumulators bit-exact, and the bf16 output within the
+    epilogue's tolerance, on the shapes of a seeded sweep."""
+    A = synth.rand_i8([196, M, K], (M, K))
+    B = synth.rand_i8([197, N, K], (N, K))
+    ref = oracle.gemm_i32(A, B, M, N, K)
+    Ad, Bd = dev(A), dev(B)
+    assert np.array_equal(host(ops.w8a8_gemm_i32(Ad, Bd)), ref)
+    rng = np.random.default_rng([198, M, N, K])
+    xs = rng.uniform(1e-3, 1e-1, M).astype(np.float32)
+    ws = rng.uniform(1e-4, 1e-2, N).astype(np.float32)
+    b = synth.rand_bf16([199, N], (N,), 0.5)
+    Y = host_bits(ops.w8a8_linear(Ad, dev(xs), Bd, dev(ws), dev_bf16(b)))
+    check_w8a8_output(Y, oracle.epilogue(ref, xs, ws, b, M, N), ref, xs, ws, b)

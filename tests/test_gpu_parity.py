@@ -697,3 +697,27 @@ def test_w8a8_linear_shape_sweep(M, N, K):
     b = synth.rand_bf16([199, N], (N,), 0.5)
     Y = host_bits(ops.w8a8_linear(Ad, dev(xs), Bd, dev(ws), dev_bf16(b)))
     check_w8a8_output(Y, oracle.epilogue(ref, xs, ws, b, M, N), ref, xs, ws, b)
+
+
+def _quant_sweep(n, seed):
+    rng = np.random.default_rng(seed)
+    return [(int(rng.integers(1, 3000)), 64 * int(rng.integers(1, 257))) for _ in range(n)]
+
+
+@pytest.mark.parametrize("M,K", _quant_sweep(16, 200))
+def test_quant_act_shape_sweep(M, K):
+    """Codes and scales bit-exact on a seeded sweep of (M, K), every row-group
+    configuration of the quant kernel up to K = 16384."""
+    c = synth.linear_case([201, M, K], M, 8, K, act="outlier")
+    lam = np.random.default_rng([202, K]).uniform(0.25, 4.0, K).astype(np.float32)
+    Xq, xs, Xq_ref, xs_ref = _quant_case(c["X"], lam, M, K)
+    assert np.array_equal(xs.view(np.uint32), xs_ref.view(np.uint32))
+    assert np.array_equal(Xq, Xq_ref)
+
+
+@pytest.mark.parametrize("M,N,K", _sweep_shapes(10, 203))
+def test_bf16_linear_shape_sweep(M, N, K):
+    c = synth.linear_case([204, M, N, K], M, N, K)
+    Y = host_bits(ops.bf16_linear(dev_bf16(c["X"]), dev_bf16(c["W"]), dev_bf16(c["bias"])))
+    rows = np.random.default_rng([205, M]).choice(M, min(M, 64), replace=False)
+    check_bf16_output(Y[rows], c["X"].reshape(M, K)[rows], c["W"].reshape(N, K), c["bias"])

@@ -275,15 +275,16 @@ hipError_t launch_smooth_quant_rows(const uint16_t *src, const float *mul, int64
                                     hipStream_t stream) {
     // A group covers 512 * G * CH columns; take the smallest that holds K.
     // Up to K = 32768 a group has at most 8 waves and walks two rows (each
-    // next one prefetched); at K = 4096 three (4608 x 4096: 11.96 against
-    // 12.91 us for two, in one job). The K = 65536 group of 16 waves has no
-    // register room for a prefetched row and walks one.
+    // next one prefetched); at K = 4096 and 16384 three (4608 x 4096: 11.96
+    // against 12.91 us for two; 4608 x 16384: 40.6 against 41.0-42.6 us; in
+    // one job each). The K = 65536 group of 16 waves has no register room
+    // for a prefetched row and walks one.
     if (K <= 512) return launch_rows<1, 1, 2, 4>(src, mul, R, K, out, scale, stream);
     if (K <= 1024) return launch_rows<2, 1, 2, 4>(src, mul, R, K, out, scale, stream);
     if (K <= 2048) return launch_rows<4, 1, 2, 4>(src, mul, R, K, out, scale, stream);
     if (K <= 4096) return launch_rows<4, 2, 3, 4>(src, mul, R, K, out, scale, stream);
     if (K <= 8192) return launch_rows<8, 2, 2, 8>(src, mul, R, K, out, scale, stream);
-    if (K <= 16384) return launch_rows<8, 4, 2, 8>(src, mul, R, K, out, scale, stream);
+    if (K <= 16384) return launch_rows<8, 4, 3, 8>(src, mul, R, K, out, scale, stream);
     if (K <= 32768) return launch_rows<8, 8, 2, 8>(src, mul, R, K, out, scale, stream);
     return launch_rows<16, 8, 1, 16>(src, mul, R, K, out, scale, stream);  // K <= 65536
 }

@@ -184,6 +184,15 @@ w8a8_status bf16_linear(const uint16_t *X, const uint16_t *W,
                         const uint16_t *bias, int64_t M, int64_t N, int64_t K,
                         uint16_t *Y, w8a8_stream stream);
 
+/* Diagnostic, host only (launches nothing, needs no GPU): the GEMM
+ * configuration that w8a8_linear and w8a8_gemm_i32 (bf16 == 0) or
+ * bf16_linear (bf16 != 0) launch for an M x N x K problem: the output tile
+ * of one workgroup, tile_m tokens x tile_n channels, and its threads.
+ * The same shape checks as those entry points (W8A8_ERR_SHAPE,
+ * W8A8_ERR_UNSUPPORTED); NULL outputs give W8A8_ERR_NULL. */
+w8a8_status w8a8_gemm_config(int64_t M, int64_t N, int64_t K, int bf16,
+                             int32_t *tile_m, int32_t *tile_n, int32_t *threads);
+
 /* ---------------------------------------------------------------------- */
 /* GGUF Q8_0 weight-only (Section 3, "GGUF k-quants": 8.5 bits per weight, */
 /* round to nearest). A row of W [N][K] is cut into blocks of 32           */

@@ -37,6 +37,7 @@ SIGNATURES = {
     "w8a8_linear": ([_P, _P, _P, _P, _P, _I64, _I64, _I64, _P, _P], _S),
     "w8a8_gemm_i32": ([_P, _P, _I64, _I64, _I64, _P, _P], _S),
     "bf16_linear": ([_P, _P, _P, _I64, _I64, _I64, _P, _P], _S),
+    "w8a8_gemm_config": ([_I64, _I64, _I64, ctypes.c_int, _P, _P, _P], _S),
     "q8_0_quantize": ([_P, _I64, _I64, _P, _P, _P], _S),
     "q8_0_dequantize": ([_P, _P, _I64, _I64, _P, _P], _S),
     "q8_0_linear": ([_P, _P, _P, _P, _I64, _I64, _I64, _P, _P, _P], _S),

@@ -227,6 +227,21 @@ w8a8_status bf16_linear(const uint16_t *X, const uint16_t *W, const uint16_t *bi
     return hip_status(w8a8::launch_gemm_bf16(X, W, bias, M, N, K, Y, as_stream(stream)));
 }
 
+w8a8_status w8a8_gemm_config(int64_t M, int64_t N, int64_t K, int bf16, int32_t *tile_m,
+                             int32_t *tile_n, int32_t *threads) {
+    if (tile_m == nullptr || tile_n == nullptr || threads == nullptr) return W8A8_ERR_NULL;
+    W8A8_TRY(check_rows(M, kMaxRows));
+    W8A8_TRY(check_rows(N, kMaxN));
+    if (M * N > kMaxMN) return W8A8_ERR_SHAPE;
+    W8A8_TRY(check_k(K));
+    int bm = 0, bn = 0, nt = 0;
+    w8a8::gemm_config(M, N, bf16 ? 2 * K : K, &bm, &bn, &nt);
+    *tile_m = bm;
+    *tile_n = bn;
+    *threads = nt;
+    return W8A8_OK;
+}
+
 w8a8_status q8_0_quantize(const uint16_t *W, int64_t N, int64_t K, int8_t *qs, uint16_t *d,
                           w8a8_stream stream) {
     if (W == nullptr || qs == nullptr || d == nullptr) return W8A8_ERR_NULL;

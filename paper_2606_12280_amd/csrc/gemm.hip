@@ -406,6 +406,71 @@ struct Epi {
             }
         }
     }
+
+    // store_rows one 32-token slice at a time, for workgroups whose LDS
+    // cannot stage every wave's whole tile: `stage` holds kSliceBytes.
+    static constexpr int kSliceBytes = 32 * kRowStride;
+
+    template <class Acc>
+    __device__ __forceinline__ void store_slices(const Acc (&acc)[TI][TJ], int8_t *stage,
+                                                 void *Yout, int m0, int rows_x, int mbase,
+                                                 int nbase, int N, int frow, int fhalf,
+                                                 int lane) const {
+        static_assert(EPI != kStoreI32, "row stores are for the bf16 epilogues");
+        constexpr int CPR = 64 * TI / 16;  // 16-byte chunks per row
+        constexpr int ROUNDS = 32 * CPR / 64;
+        static_assert(32 * CPR % 64 == 0, "whole store rounds");
+        const __amdgpu_buffer_rsrc_t ry =
+            make_rsrc(static_cast<int8_t *>(Yout) + static_cast<int64_t>(m0) * N * 2,
+                      static_cast<uint32_t>(rows_x) * N * 2u);
+        const bool vec8 = (N & 7) == 0;
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) {
+            // A wave's LDS accesses execute in order: the reads of slice j - 1
+            // below are done before these writes replace it.
+#pragma unroll
+            for (int i = 0; i < TI; ++i)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    float y[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float a = static_cast<float>(acc[i][j][4 * g + e]);
+                        const uint32_t bw = b_[i][g][e >> 1];
+                        const float b =
+                            __uint_as_float((e & 1) ? (bw & 0xffff0000u) : (bw << 16));
+                        if constexpr (EPI == kDequantBf16)
+                            y[e] = __builtin_fmaf(a, xs_[j] * ws_[i][g][e], b);
+                        else
+                            y[e] = a + b;
+                    }
+                    const int c = 32 * i + 8 * g + 4 * fhalf;
+                    *reinterpret_cast<v2u *>(stage + frow * kRowStride + c * 2) =
+                        v2u{f32x2_to_bf16x2(y[0], y[1]), f32x2_to_bf16x2(y[2], y[3])};
+                }
+#pragma unroll
+            for (int r = 0; r < ROUNDS; ++r) {
+                const int id = r * 64 + lane;
+                const int row = id / CPR;
+                const int c = id % CPR;
+                const v4i v = *reinterpret_cast<const v4i *>(stage + row * kRowStride + c * 16);
+                const int n = nbase + 8 * c;
+                const uint32_t base = static_cast<uint32_t>(mbase + 32 * j + row) * N;
+                if (vec8 && n + 8 <= N) {
+                    __builtin_amdgcn_raw_buffer_store_b128(v, ry, (base + n) * 2u, 0, 0);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const uint32_t off = n + e < N ? (base + n + e) * 2u : kOutOfRange;
+                        __builtin_amdgcn_raw_buffer_store_b16(
+                            static_cast<uint16_t>(static_cast<uint32_t>(v[e >> 1]) >>
+                                                  (16 * (e & 1))),
+                            ry, off, 0, 0);
+                    }
+                }
+            }
+        }
+    }
 };
 
 // MFMA side of one wave: fragment reads from an LDS slot and the MFMAs of a
@@ -549,6 +614,83 @@ struct Mma2 {
     }
 };
 
+// MFMA side of one wave of gemm_2s_kernel with three or more waves per SIMD:
+// fragments read one MFMA step ahead into two register buffers. The other
+// waves of the SIMD cover an LDS read's latency, and the 168 registers a
+// wave has at three waves per SIMD leave no room for four buffers.
+template <class Op, int BK, int TI, int TJ, int SWZ>
+struct Mma1 {
+    static constexpr int CPR = BK / 16;
+    static constexpr int KSTEPS = BK / 32;
+    static_assert(KSTEPS == 4, "four MFMA steps per K tile");
+    typename Op::Acc acc[TI][TJ];
+    v4i wf[2][TI];
+    v4i xf[2][TJ];
+    int x_row, w_row, fhalf, fkey;
+
+    __device__ __forceinline__ void init(int lane, int mbase, int nbase) {
+        const int frow = lane & 31;
+        fhalf = lane >> 5;
+        fkey = (frow >> SWZ) & (CPR - 1);
+        x_row = (mbase + frow) * BK;
+        w_row = (nbase + frow) * BK;
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+            for (int j = 0; j < TJ; ++j) acc[i][j] = typename Op::Acc{};
+    }
+    // Fragments of MFMA step s (0..3) of a K tile into buffer s % 2.
+    template <int S>
+    __device__ __forceinline__ void load(const int8_t *xslot, const int8_t *wslot) {
+        const int chunk = (2 * S + fhalf) ^ fkey;
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+            wf[S & 1][i] = *reinterpret_cast<const v4i *>(wslot + w_row + i * 32 * BK + chunk * 16);
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+            xf[S & 1][j] = *reinterpret_cast<const v4i *>(xslot + x_row + j * 32 * BK + chunk * 16);
+    }
+    template <int S>
+    __device__ __forceinline__ void step() {
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+            for (int j = 0; j < TJ; ++j)
+                acc[i][j] = Op::mma(wf[S & 1][i], xf[S & 1][j], acc[i][j]);
+    }
+    // One K tile. On entry buffer 0 holds its step 0. Steps 0..2 read the
+    // next step; then `boundary()`; then, unless LAST, step 3 reads step 0
+    // of the next tile from (nxslot, nwslot) and LOADS loads (`issue(i)`)
+    // go out during it.
+    template <bool LAST, int LOADS, class Boundary, class Issue>
+    __device__ __forceinline__ void tile(const int8_t *xslot, const int8_t *wslot,
+                                         const int8_t *nxslot, const int8_t *nwslot,
+                                         Boundary &&boundary, Issue &&issue) {
+        load<1>(xslot, wslot);
+        step<0>();
+        interleave_from<0, TI * TJ, TI + TJ, 0>();
+        sched_fence();
+        load<2>(xslot, wslot);
+        step<1>();
+        interleave_from<0, TI * TJ, TI + TJ, 0>();
+        sched_fence();
+        load<3>(xslot, wslot);
+        step<2>();
+        interleave_from<0, TI * TJ, TI + TJ, 0>();
+        sched_fence();
+        if constexpr (!LAST) {
+            boundary();
+            sched_fence();
+#pragma unroll
+            for (int i = 0; i < LOADS; ++i) issue(i);
+            load<0>(nxslot, nwslot);
+        }
+        step<3>();
+        interleave_from<0, TI * TJ, LAST ? 0 : TI + TJ, LOADS>();
+        sched_fence();
+    }
+};
+
 // Lane l of 1 KiB DMA block `blk` of a BK-wide tile writes LDS bytes
 // [blk*1024 + 16 l, +16) = row blk*(1024/BK) + l / CPR, physical chunk
 // l % CPR, which holds logical chunk (l % CPR) ^ swizzle(row). Returns the
@@ -674,17 +816,20 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_kernel(
 }
 
 // --------------------------------------------------------------------------
-// gemm_2s_kernel: every wave loads and multiplies, two-slot rings. Made for
-// large tiles (192 x 256: 27% fewer bytes per MFMA than 256 x 128) whose
-// accumulators leave no registers for separate producer waves. One barrier
-// per K tile, placed before the tile's third MFMA step (fragments are read
-// two steps ahead, so by then every read of the tile has been issued):
+// gemm_2s_kernel: four loading waves, two-slot rings. Made for large tiles
+// (192 x 256: 27% fewer bytes per MFMA than 256 x 128; 288 x 256 with 12
+// waves: 19% fewer than 192 x 256) whose accumulators leave no registers
+// for separate producer waves. One barrier per K tile, placed once every
+// fragment read of the tile has been issued: before its third MFMA step
+// when fragments are read two steps ahead (8 waves), before its fourth when
+// one step ahead (12 waves):
 //   barrier #kt+1: every wave has finished reading the slots of tile kt and
 //   its own loads of tile kt+1 have landed.
 // Right after it each wave issues its share of tile kt+2 into the slots
 // just freed, so a tile's loads have most of a K tile of MFMAs to land in.
 // The epilogue operands are staged in LDS by wave 0 before barrier #0; the
-// output rows go out through LDS (store_rows), staged in the ring.
+// output rows go out through LDS (store_rows / store_slices), staged in the
+// ring.
 // --------------------------------------------------------------------------
 template <class Op, int BM, int BN, int WAVES_M, int WAVES_N, int SWZ, int GROUP_M, int EPI,
           bool N_VEC, bool HAS_BIAS>
@@ -701,10 +846,10 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_2s_kernel(
     constexpr int NBX = BM * BK / 1024;
     constexpr int NBW = BN * BK / 1024;
     // Waves 0..NI-1 load; a workgroup's waves go round-robin to the 4 SIMDs,
-    // so each SIMD has one loading wave and one that only multiplies (whose
-    // MFMAs keep going while a load instruction waits to issue).
-    constexpr int NI = NW / 2;
-    static_assert(NI == 4, "one loading wave per SIMD");
+    // so each SIMD has one loading wave and one or two that only multiply
+    // (whose MFMAs keep going while a load instruction waits to issue).
+    constexpr int NI = 4;
+    static_assert(NW == 8 || NW == 12, "two or three waves per SIMD");
     constexpr int LX = NBX / NI;  // 1 KiB DMA blocks per loading wave and K tile, X
     constexpr int LW = NBW / NI;  // ... W
     constexpr int XSLOT = BM * BK;
@@ -716,8 +861,11 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_2s_kernel(
 
     using EpiT = Epi<TI, TJ, EPI, N_VEC, HAS_BIAS>;
     // The ring; after the last K tile the same bytes stage the waves' output
-    // rows. Then the epilogue operands.
-    constexpr int BODY = RING > NW * EpiT::kStageBytes ? RING : NW * EpiT::kStageBytes;
+    // rows (whole wave tiles if they fit, else 32-token slices). Then the
+    // epilogue operands.
+    constexpr bool SLICED = NW * EpiT::kStageBytes > RING;
+    constexpr int STAGE_BYTES = SLICED ? EpiT::kSliceBytes : EpiT::kStageBytes;
+    constexpr int BODY = RING > NW * STAGE_BYTES ? RING : NW * STAGE_BYTES;
     static_assert(BODY + 4 * BM + 6 * BN <= 160 * 1024, "LDS");
 
     __shared__ __attribute__((aligned(1024))) int8_t smem[BODY + 4 * BM + 6 * BN];
@@ -762,8 +910,14 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_2s_kernel(
             dma16(rx, xslot(kt) + (iw + (i - LW) * NI) * 1024, off_x[i - LW] + kt * BK);
     };
 
-    Mma2<Op, BK, TI, TJ, SWZ> mma;
-    prefer_agpr_mfma();
+    // Fragments two MFMA steps ahead at two waves per SIMD, one at three.
+    constexpr bool AHEAD2 = NW == 8;
+    std::conditional_t<AHEAD2, Mma2<Op, BK, TI, TJ, SWZ>, Mma1<Op, BK, TI, TJ, SWZ>> mma;
+    // Accumulators in AGPRs at two waves per SIMD. At three, a wave has 168
+    // registers, which the compiler splits evenly between VGPRs and AGPRs
+    // once a kernel uses AGPRs: 96 accumulators in 84 AGPRs spill. In the
+    // VGPR form of the MFMAs everything fits in 165 VGPRs.
+    if constexpr (AHEAD2) prefer_agpr_mfma();
     mma.init(lane, mbase, nbase);
 
 #pragma unroll
@@ -779,7 +933,7 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_2s_kernel(
         for (int i = 0; i < LW + LX; ++i) issue_one(1, i);
     }
     mma.template load<0>(xslot(0), wslot(0));
-    mma.template load<1>(xslot(0), wslot(0));
+    if constexpr (AHEAD2) mma.template load<1>(xslot(0), wslot(0));
 
     // Tile kt's loads went out at barrier #kt-1 (tiles 0 and 1 in the
     // prologue). Branch-free loops keep the compiler's own waits exact.
@@ -807,8 +961,12 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_2s_kernel(
         epi.load_lds(ep_xs, ep_ws, ep_b, mbase, nbase, lane & 31, lane >> 5);
         wait_lgkmcnt0();
         barrier();  // every wave is done with the ring
-        epi.store_rows(mma.acc, smem + wave * EpiT::kStageBytes, Yout, m0, rows_x, mbase,
-                       n0 + nbase, N, lane & 31, lane >> 5, lane);
+        if constexpr (SLICED)
+            epi.store_slices(mma.acc, smem + wave * STAGE_BYTES, Yout, m0, rows_x, mbase,
+                             n0 + nbase, N, lane & 31, lane >> 5, lane);
+        else
+            epi.store_rows(mma.acc, smem + wave * STAGE_BYTES, Yout, m0, rows_x, mbase,
+                           n0 + nbase, N, lane & 31, lane >> 5, lane);
     }
 }
 
@@ -1028,34 +1186,64 @@ struct TwoSlot {
     }
 };
 
-// Fraction of the slots of ceil(tiles / 256) full rounds of the 256 CUs
-// (one workgroup per CU) that the tiles of an M x N output fill.
-double round_fill(int M, int N, int BM, int BN) {
-    const int64_t tiles = static_cast<int64_t>((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    const int64_t rounds = (tiles + 255) / 256;
-    return static_cast<double>(tiles) / static_cast<double>(rounds * 256);
-}
-
-// Default configurations (measured on the DiT shapes, M = 4608).
-//  - K a multiple of 128 bytes (every DiT shape):
-//    * 192 x 256 tiles (tokens x channels), every wave loading and
-//      multiplying, when their tiles fill the rounds of the 256 CUs to at
-//      least 85% (N = 16384: 6 full rounds; N = 12288: 4.5);
-//    * otherwise warp-specialized, 4 consumer and 4 producer waves, 3-slot
-//      ring; 192 x 128 tiles (waves of 96 x 64) or 256 x 128 (128 x 64),
-//      whichever fills the rounds better (N = 4096: 192 x 128, 3 full rounds).
+// Default configurations.
+//  - K a multiple of 128 bytes (every DiT shape): the candidate that
+//    minimizes the estimated time, rounds of the 256 CUs (one workgroup per
+//    CU) x tile area / rate, where rate is the throughput per output
+//    element at full rounds, measured on the DiT shapes relative to the
+//    288 x 256 tiles. Ties go to the earlier candidate.
+//    * 288 x 256 tiles (tokens x channels), two-slot, 12 waves of 96 x 64:
+//      at M = 4608 = 16 x 288 every DiT shape fills whole rounds (N = 16384:
+//      4, N = 12288: 3, N = 4096: 1);
+//    * 192 x 256, two-slot, 8 waves of 96 x 64;
+//    * 192 x 128 and 256 x 128, warp-specialized (4 consumer waves of 96 x
+//      64 or 128 x 64, 4 producer waves, 3-slot ring): the small tiles for
+//      outputs of fewer than a round of large tiles.
 //    All use 128-byte K tiles (full cache lines per row) and the swizzle key
-//    (row >> 1) & 7, groups of 4 tile rows.
+//    (row >> 1) & 7.
 //  - otherwise: every wave loads, 192 x 256 tiles, 4 waves of 192 x 64,
 //    4-slot ring of 64-byte K tiles (BK = 64 divides K), key (row >> 2) & 3.
+struct TileChoice {
+    int bm, bn, threads;
+    double rate;
+};
+constexpr TileChoice kTiles[] = {
+    {288, 256, 768, 1.0},
+    {192, 256, 512, 0.94},
+    {192, 128, 512, 0.86},
+    {256, 128, 512, 0.86},
+};
+constexpr int kTileChoices = sizeof(kTiles) / sizeof(kTiles[0]);
+
+int pick_tiles(int M, int N) {
+    int best = 0;
+    double best_t = 0.0;
+    for (int c = 0; c < kTileChoices; ++c) {
+        const TileChoice &t = kTiles[c];
+        const int64_t tiles = static_cast<int64_t>((M + t.bm - 1) / t.bm) * ((N + t.bn - 1) / t.bn);
+        const int64_t rounds = (tiles + 255) / 256;
+        const double est = static_cast<double>(rounds) * t.bm * t.bn / t.rate;
+        if (c == 0 || est < best_t) {
+            best = c;
+            best_t = est;
+        }
+    }
+    return best;
+}
+
 template <class Op, int EPI>
 hipError_t launch_default(const GemmArgs &a) {
     if (a.Kb % 128 == 0) {
-        if (round_fill(a.M, a.N, 192, 256) >= 0.85)
+        switch (pick_tiles(a.M, a.N)) {
+        case 0:
+            return TwoSlot<Op, 288, 256, 3, 4, 1, 8, EPI>::launch(a);
+        case 1:
             return TwoSlot<Op, 192, 256, 2, 4, 1, 4, EPI>::launch(a);
-        if (round_fill(a.M, a.N, 192, 128) > round_fill(a.M, a.N, 256, 128) + 1e-9)
+        case 2:
             return Specialized<Op, 192, 128, 128, 2, 2, 4, 3, 1, 4, EPI>::launch(a);
-        return Specialized<Op, 256, 128, 128, 2, 2, 4, 3, 1, 4, EPI>::launch(a);
+        default:
+            return Specialized<Op, 256, 128, 128, 2, 2, 4, 3, 1, 4, EPI>::launch(a);
+        }
     }
     return Uniform<Op, 192, 256, 64, 1, 4, 4, 2, 4, EPI>::launch(a);
 }
@@ -1089,6 +1277,19 @@ hipError_t launch_gemm_bf16(const uint16_t *A, const uint16_t *B, const uint16_t
                Y,
                stream};
     return launch_default<Bf16Op, kBiasBf16>(a);
+}
+
+void gemm_config(int64_t M, int64_t N, int64_t Kb, int *tile_m, int *tile_n, int *threads) {
+    if (Kb % 128 == 0) {
+        const TileChoice &t = kTiles[pick_tiles(static_cast<int>(M), static_cast<int>(N))];
+        *tile_m = t.bm;
+        *tile_n = t.bn;
+        *threads = t.threads;
+    } else {
+        *tile_m = 192;
+        *tile_n = 256;
+        *threads = 256;
+    }
 }
 
 }  // namespace w8a8

@@ -76,4 +76,8 @@ hipError_t launch_gemm_bf16(const uint16_t *A, const uint16_t *B,
                             const uint16_t *bias, int64_t M, int64_t N,
                             int64_t K, uint16_t *Y, hipStream_t stream);
 
+// The tile (tokens x channels) and threads per workgroup of the GEMM the
+// two launchers above run for M x N with K bytes per row (host only).
+void gemm_config(int64_t M, int64_t N, int64_t Kb, int *tile_m, int *tile_n, int *threads);
+
 }  // namespace w8a8

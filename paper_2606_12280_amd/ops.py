@@ -7,6 +7,8 @@ the library, and raises W8A8Error on a non-zero status. Every arithmetic step
 runs in the library's HIP kernels. bf16 tensors are torch.bfloat16."""
 from __future__ import annotations
 
+import ctypes
+
 import torch
 
 from ._lib import MOMENTS_WORK_BYTES, check, load
@@ -209,6 +211,15 @@ def bf16_linear(X: torch.Tensor, W: torch.Tensor, bias: torch.Tensor | None = No
         check("bf16_linear",
               lib.bf16_linear(_ptr(X), _ptr(W), _ptr(bias), M, N, K, _ptr(Y), _stream(X.device)))
     return Y
+
+
+def w8a8_gemm_config(M: int, N: int, K: int, bf16: bool = False) -> tuple[int, int, int]:
+    """(tile_m, tile_n, threads) of the GEMM that w8a8_linear / w8a8_gemm_i32
+    (bf16=False) or bf16_linear (bf16=True) launch for M x N x K. Host only."""
+    tm, tn, nt = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    check("w8a8_gemm_config", load().w8a8_gemm_config(M, N, K, int(bool(bf16)), ctypes.byref(tm),
+                                                      ctypes.byref(tn), ctypes.byref(nt)))
+    return tm.value, tn.value, nt.value
 
 
 # --------------------------------------------------------------------------

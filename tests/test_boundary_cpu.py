@@ -93,6 +93,33 @@ def test_linear_validation(lib):
     assert h(A, B, None, 4, 8, 0, C, None) == SHAPE
 
 
+def test_gemm_config_picks_tiles_by_rounds(lib):
+    """The host-side tile choice: the estimated time (rounds of the 256 CUs x
+    tile area / measured rate) of each candidate, computed here by hand."""
+    cfg = ops.w8a8_gemm_config
+    T288, T192, S192, S256, U = (288, 256, 768), (192, 256, 512), (192, 128, 512), \
+        (256, 128, 512), (192, 256, 256)
+    # every DiT linear at M = 4608 = 16 x 288 fills whole rounds of 288 x 256
+    for N, K in [(16384, 4096), (4096, 16384), (12288, 4096), (4096, 4096)]:
+        assert cfg(4608, N, K) == T288 and cfg(4608, N, K, bf16=True) == T288
+    # N = 12290: 784 large tiles take 4 rounds, 1176 of 192 x 256 take 5
+    # (5 x 49152 / 0.94 < 4 x 73728)
+    assert cfg(4545, 12290, 384) == T192
+    # fewer than a round of tiles: the smallest tile
+    assert cfg(64, 512, 256) == S192 and cfg(200, 4096, 512) == S192
+    # M = 1000: 384 tiles of 192 x 128 take 2 rounds, 256 of 256 x 128 one
+    assert cfg(1000, 8190, 256) == S256
+    # K not a multiple of 128 bytes: the uniform 64-byte K tile kernel ...
+    assert cfg(513, 384, 4160) == U and cfg(1, 1, 64) == U
+    # ... unless bf16 doubles the bytes per row
+    assert cfg(513, 384, 4160, bf16=True) == S192
+    out = ctypes.c_int32()
+    f = lib.w8a8_gemm_config
+    assert f(4, 8, 64, 0, None, ctypes.byref(out), ctypes.byref(out)) == NULL
+    assert f(0, 8, 64, 0, ctypes.byref(out), ctypes.byref(out), ctypes.byref(out)) == SHAPE
+    assert f(4, 8, 96, 0, ctypes.byref(out), ctypes.byref(out), ctypes.byref(out)) == UNSUP
+
+
 def test_calibration_validation(lib):
     f = lib.w8a8_smooth_factors
     assert f(A, B, 8, 64, 0.5, None, None) == NULL

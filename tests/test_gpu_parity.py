@@ -207,11 +207,46 @@ def test_gemm_i32_bit_exact(M, N, K):
     assert np.array_equal(C, ref)
 
 
-# Shapes large enough to select the 192 x 256 tiles (at least 85% of the
-# 256 CUs' rounds filled), with ragged M and N (N odd: element stores at the
-# edge) and 1, 2, 3 and 5 K tiles of 128 bytes.
+# Shapes large enough to select the two-slot kernels (288 x 256 tiles, and
+# 192 x 256 for the third), with ragged M and N (N odd: element stores at
+# the edge) and 1, 2, 3 and 5 K tiles of 128 bytes.
 LARGE_RAGGED = [(4571, 16376, 128), (4600, 16375, 256), (4545, 12290, 384),
                 (4608, 16384, 640)]
+
+# One ragged shape per GEMM configuration, with the (tile_m, tile_n,
+# threads) the library reports for it.
+CONFIG_SHAPES = [
+    ((4571, 16376, 128), (288, 256, 768)),
+    ((4545, 12290, 384), (192, 256, 512)),
+    ((250, 1000, 256), (192, 128, 512)),
+    ((1000, 8190, 256), (256, 128, 512)),
+    ((513, 384, 4160), (192, 256, 256)),
+]
+
+
+@pytest.mark.parametrize("shape,config", CONFIG_SHAPES)
+def test_every_gemm_configuration(shape, config):
+    """Each kernel configuration on a shape ragged in M and N: int32
+    accumulators bit-exact, the dequantizing epilogue without a bias within
+    tolerance, and bf16_linear within its bound on sampled rows (its rows
+    have twice the bytes, so its configuration can differ)."""
+    M, N, K = shape
+    assert ops.w8a8_gemm_config(M, N, K) == config
+    A = synth.rand_i8([116, M, K], (M, K))
+    B = synth.rand_i8([117, N, K], (N, K))
+    ref = oracle.gemm_i32(A, B, M, N, K)
+    Ad, Bd = dev(A), dev(B)
+    assert np.array_equal(host(ops.w8a8_gemm_i32(Ad, Bd)), ref)
+    rng = np.random.default_rng([118, M, N, K])
+    xs = rng.uniform(1e-3, 1e-1, M).astype(np.float32)
+    ws = rng.uniform(1e-4, 1e-2, N).astype(np.float32)
+    zero = np.zeros(N, np.uint16)
+    Y = host_bits(ops.w8a8_linear(Ad, dev(xs), Bd, dev(ws), None))
+    check_w8a8_output(Y, oracle.epilogue(ref, xs, ws, zero, M, N), ref, xs, ws, zero)
+    c = synth.linear_case([119, M, N, K], M, N, K)
+    Yb = host_bits(ops.bf16_linear(dev_bf16(c["X"]), dev_bf16(c["W"]), dev_bf16(c["bias"])))
+    rows = np.sort(np.concatenate([[0, M - 1], rng.choice(M, min(M, 40), replace=False)]))
+    check_bf16_output(Yb[rows], c["X"].reshape(M, K)[rows], c["W"].reshape(N, K), c["bias"])
 
 
 @pytest.mark.parametrize("M,N,K", LARGE_RAGGED)

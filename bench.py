@@ -444,20 +444,29 @@ def counter_traffic(workload: str):
 COPY_BYTES = 512 << 20
 
 
-def counter_run(layers, dev, reps: int = 3):
+def counter_run(layers, dev, reps: int = 3, codes: str = "workload"):
+    """codes="uniform" replaces the workload's int8 codes (X and W) by
+    uniform random ones in [-127, 127], to compare the clock the GPU holds
+    under the two (same launches, same scales)."""
     lin = max((x for x in layers if not x.lay.protected), key=lambda x: x.ops)
     ws = L.Workspace(dev)
     Xq, xs = ws.get(lin.M, lin.lay.K)
     ops.w8a8_quant_act(lin.xs[0], lin.lay.inv_lambda, Xq=Xq, x_scale=xs)
+    Wq = lin.lay.Wq
+    if codes == "uniform":
+        g = torch.Generator(device=dev)
+        g.manual_seed(7)
+        Xq.copy_(torch.randint(-127, 128, Xq.shape, generator=g, device=dev, dtype=torch.int8))
+        Wq = torch.randint(-127, 128, Wq.shape, generator=g, device=dev, dtype=torch.int8)
     src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
     dst = torch.empty_like(src)
     torch.cuda.synchronize()
     for _ in range(reps):
-        ops.w8a8_linear(Xq, xs, lin.lay.Wq, lin.lay.w_scale, lin.lay.bias, out=lin.Y)
+        ops.w8a8_linear(Xq, xs, Wq, lin.lay.w_scale, lin.lay.bias, out=lin.Y)
         torch.cuda.synchronize()
         torch.neg(src, out=dst)
         torch.cuda.synchronize()
-    log(f"counter run: {reps} x w8a8_linear {lin.M}x{lin.lay.K}->{lin.lay.N}, "
+    log(f"counter run: {reps} x w8a8_linear {lin.M}x{lin.lay.K}->{lin.lay.N} ({codes} codes), "
         f"{reps} x neg over {COPY_BYTES} bytes")
     return lin
 
@@ -539,6 +548,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--counter-run", action="store_true",
                     help="only the short launch sequence the counter passes profile")
+    ap.add_argument("--counter-codes", choices=["workload", "uniform"], default="workload",
+                    help="int8 codes of the counter run: the workload's, or uniform random")
     ap.add_argument("--counters-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 counter runs into profiles/ (no GPU)")
     args = ap.parse_args()
@@ -566,7 +577,7 @@ def main():
     log(f"workload {args.workload}: {len(layers)} linears prepared in "
         f"{time.perf_counter() - t_build:.1f} s")
     if args.counter_run:
-        counter_run(layers, dev)
+        counter_run(layers, dev, codes=args.counter_codes)
         return
 
     # per-kernel durations inside the timed steps (events between kernels)

@@ -29,15 +29,18 @@
 //   epilogue: y = float(acc) * (x_scale[m] * w_scale[n]) + bias[n] with one
 //     fma, four channels packed into 8 bytes of bf16 per store.
 //
-// Two kernels share this skeleton:
-//   gemm_kernel     every wave loads and multiplies (used when the K tile is
-//                   64 bytes, i.e. K not a multiple of 128 bytes);
+// Three kernels share this skeleton:
+//   gemm_2s_kernel  large tiles (288 x 256 with 12 waves, 192 x 256 with 8)
+//                   in two-slot rings; four of the waves also issue the tile
+//                   loads. The default wherever its tiles fill the CUs;
 //   gemm_ws_kernel  warp-specialized: NPROD producer waves only issue the
 //                   tile loads, the WAVES_M x WAVES_N consumer waves only read
 //                   fragments and run MFMAs. With one wave doing both, the
 //                   in-order issue stalls the MFMA stream whenever the load
 //                   path pushes back; split across waves that share a SIMD,
-//                   loads and MFMAs proceed side by side.
+//                   loads and MFMAs proceed side by side. Small outputs;
+//   gemm_kernel     every wave loads and multiplies (used when the K tile is
+//                   64 bytes, i.e. K not a multiple of 128 bytes).
 //
 // Launch order is XCD-aware: workgroups are dispatched round-robin over the
 // 8 XCDs, so block id b runs on XCD b % 8. Each XCD is given a contiguous

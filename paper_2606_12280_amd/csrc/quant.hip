@@ -192,36 +192,42 @@ __global__ void zero_kernel(float *__restrict__ dst, int64_t K) {
     if (k < K) dst[k] = 0.0f;
 }
 
-// Column absmax: a workgroup covers 64 chunks of 8 columns (512 columns) of a
-// strip of rows; its kColWaves waves take interleaved rows (wave w: r0 + w,
-// r0 + w + kColWaves, ...), each lane 16 bytes of a row with 4 rows in
-// flight, so that every wave load is a contiguous 1 KiB. The waves' maxima
-// combine in LDS and one integer atomic max per column leaves the workgroup
-// (the bit patterns of non-negative floats order like the floats). Strips
-// are sized for about kColBlocks workgroups; atomics on one address
-// serialize, so a column sees at most about kColBlocks / (K / 512) of them.
-constexpr int64_t kColBlocks = 512;
+// Column absmax: a workgroup covers 8 CPW columns (16 CPW bytes of every
+// row) of a strip of rows. Lane l of wave w reads the 8 columns of chunk
+// l % CPW in row (64 / CPW) w + l / CPW of every step of 16 (64 / CPW) rows,
+// so each wave load is 64 / CPW row segments of 16 CPW bytes, with
+// kColUnroll steps in flight. Lanes holding the same chunk combine with lane
+// shuffles, the waves in LDS, and one integer atomic max per column leaves
+// the workgroup (the bit patterns of non-negative floats order like the
+// floats). Strips are sized for about kColTarget workgroups, so a column
+// sees about kColTarget / (K / (8 CPW)) atomics: atomics on one address
+// serialize at the memory side.
+constexpr int64_t kColTarget = 512;
 constexpr int kColWaves = 16;
 constexpr int kColUnroll = 4;
 
+template <int CPW>
 __global__ __launch_bounds__(kColWaves * 64) void col_absmax_kernel(
     const uint16_t *__restrict__ src, int64_t R, int64_t K, int64_t strip,
     float *__restrict__ colmax) {
-    __shared__ float red[kColWaves][64][9];
+    static_assert(CPW >= 8 && CPW <= 64 && (CPW & (CPW - 1)) == 0, "chunks per segment");
+    constexpr int RPL = 64 / CPW;              // rows per wave load
+    constexpr int STEP = kColWaves * RPL;      // rows per workgroup step
+    __shared__ float red[kColWaves][CPW][9];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int64_t j = static_cast<int64_t>(blockIdx.x) * 64 + lane;  // chunk of 8 columns
-    const bool ok = j * 8 < K;
+    const int chunk = lane % CPW;
+    const int64_t c0 = static_cast<int64_t>(blockIdx.x) * (8 * CPW) + chunk * 8;
     const int64_t r0 = static_cast<int64_t>(blockIdx.y) * strip;
     const int64_t r1 = r0 + strip < R ? r0 + strip : R;
     float m[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int64_t r = r0 + wave; r < r1; r += kColWaves * kColUnroll) {
+    for (int64_t r = r0 + wave * RPL + lane / CPW; r < r1; r += STEP * kColUnroll) {
         uint4 x[kColUnroll];
 #pragma unroll
         for (int u = 0; u < kColUnroll; ++u) {
-            const int64_t ru = r + kColWaves * u;
-            x[u] = (ok && ru < r1) ? reinterpret_cast<const uint4 *>(src + ru * K)[j]
-                                   : make_uint4(0u, 0u, 0u, 0u);
+            const int64_t ru = r + STEP * u;
+            x[u] = ru < r1 ? *reinterpret_cast<const uint4 *>(src + ru * K + c0)
+                           : make_uint4(0u, 0u, 0u, 0u);
         }
 #pragma unroll
         for (int u = 0; u < kColUnroll; ++u) {
@@ -235,16 +241,23 @@ __global__ __launch_bounds__(kColWaves * 64) void col_absmax_kernel(
             m[7] = fmaxf(m[7], fabsf(bf16_hi(x[u].w)));
         }
     }
+    // lanes l, l ^ CPW, l ^ 2 CPW, ... hold the same chunk
 #pragma unroll
-    for (int e = 0; e < 8; ++e) red[wave][lane][e] = m[e];
+    for (int d = CPW; d < 64; d <<= 1)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) m[e] = fmaxf(m[e], __shfl_xor(m[e], d, 64));
+    if (lane < CPW) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) red[wave][lane][e] = m[e];
+    }
     __syncthreads();
-    if (wave != 0 || !ok) return;
-    unsigned int *dst = reinterpret_cast<unsigned int *>(colmax) + j * 8;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        float v = red[0][lane][e];
-        for (int w = 1; w < kColWaves; ++w) v = fmaxf(v, red[w][lane][e]);
-        atomicMax(dst + e, __float_as_uint(v));
+    for (int t = threadIdx.x; t < 8 * CPW; t += kColWaves * 64) {
+        const int ch = t >> 3;
+        const int e = t & 7;
+        float v = red[0][ch][e];
+        for (int w = 1; w < kColWaves; ++w) v = fmaxf(v, red[w][ch][e]);
+        atomicMax(reinterpret_cast<unsigned int *>(colmax) + blockIdx.x * (8 * CPW) + t,
+                  __float_as_uint(v));
     }
 }
 
@@ -300,19 +313,30 @@ hipError_t launch_zero_f32(float *dst, int64_t K, hipStream_t stream) {
     return hipGetLastError();
 }
 
-hipError_t launch_col_absmax(const uint16_t *src, int64_t R, int64_t K, float *colmax,
-                             hipStream_t stream) {
-    const int64_t gx = (K / 8 + 63) / 64;
-    int64_t strips = (kColBlocks + gx - 1) / gx;
-    const int64_t max_strips = (R + kColWaves - 1) / kColWaves;  // a row per wave at least
+template <int CPW>
+hipError_t launch_col_absmax_cpw(const uint16_t *src, int64_t R, int64_t K, float *colmax,
+                                 hipStream_t stream) {
+    const int64_t gx = K / (8 * CPW);
+    const int64_t step = kColWaves * (64 / CPW);
+    int64_t strips = (kColTarget + gx - 1) / gx;
+    const int64_t max_strips = (R + step - 1) / step;  // a step of rows at least
     if (strips > max_strips) strips = max_strips;
-    if (strips > 65535) strips = 65535;
     if (strips < 1) strips = 1;
     const int64_t strip = (R + strips - 1) / strips;
     const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>((R + strip - 1) / strip));
-    hipLaunchKernelGGL(col_absmax_kernel, grid, dim3(kColWaves * 64), 0, stream, src, R, K,
+    hipLaunchKernelGGL(col_absmax_kernel<CPW>, grid, dim3(kColWaves * 64), 0, stream, src, R, K,
                        strip, colmax);
     return hipGetLastError();
+}
+
+hipError_t launch_col_absmax(const uint16_t *src, int64_t R, int64_t K, float *colmax,
+                             hipStream_t stream) {
+    // 512-byte row segments where K allows (4608 x 4096: 8.4 us against 9.9
+    // for 128-byte and 8.4 for 1 KiB segments; 4608 x 16384: 25.7 against
+    // 31.3 and 27.2 us; in one job). The entry point guarantees 64 | K.
+    if (K % 256 == 0) return launch_col_absmax_cpw<32>(src, R, K, colmax, stream);
+    if (K % 128 == 0) return launch_col_absmax_cpw<16>(src, R, K, colmax, stream);
+    return launch_col_absmax_cpw<8>(src, R, K, colmax, stream);
 }
 
 hipError_t launch_lambda_from_stats(const float *s, float *lam, int64_t K, double alpha,

@@ -84,7 +84,8 @@ def test_prepare_weight_bit_exact(N, K):
     assert np.array_equal(host(Wq), Wq_ref)
 
 
-@pytest.mark.parametrize("M,K", [(64, 256), (4608, 4096), (1000, 16384), (3, 64)])
+@pytest.mark.parametrize("M,K", [(64, 256), (4608, 4096), (1000, 16384), (3, 64), (77, 384),
+                                 (300, 1088)])
 def test_act_absmax_bit_exact_and_accumulates(M, K):
     X1 = synth.rand_bf16([104, M, K], (M, K), 2.0)
     X2 = synth.rand_bf16([105, M, K], (7, K), 5.0)

@@ -1218,12 +1218,15 @@ constexpr TileChoice kTiles[] = {
 };
 constexpr int kTileChoices = sizeof(kTiles) / sizeof(kTiles[0]);
 
+// A candidate whose grid would reach 2^32 work-items is skipped; the first
+// never does within the entry points' limit M N <= 2^38.
 int pick_tiles(int M, int N) {
     int best = 0;
     double best_t = 0.0;
     for (int c = 0; c < kTileChoices; ++c) {
         const TileChoice &t = kTiles[c];
         const int64_t tiles = static_cast<int64_t>((M + t.bm - 1) / t.bm) * ((N + t.bn - 1) / t.bn);
+        if (c > 0 && tiles * t.threads >= (INT64_C(1) << 32)) continue;
         const int64_t rounds = (tiles + 255) / 256;
         const double est = static_cast<double>(rounds) * t.bm * t.bn / t.rate;
         if (c == 0 || est < best_t) {

@@ -113,6 +113,13 @@ def test_gemm_config_picks_tiles_by_rounds(lib):
     assert cfg(513, 384, 4160) == U and cfg(1, 1, 64) == U
     # ... unless bf16 doubles the bytes per row
     assert cfg(513, 384, 4160, bf16=True) == S192
+    # at the size limit (M N <= 2^38) every grid stays below 2^32 work-items
+    for M, N in [(1 << 22, 1 << 16), (1 << 18, 1 << 20), ((1 << 22) - 1, 65535), (1, 1 << 20),
+                 (1 << 22, 1), (300000, 916000)]:
+        for bf16 in (False, True):
+            for K in (64, 128):
+                tm, tn, nt = cfg(M, N, K, bf16=bf16)
+                assert -(-M // tm) * -(-N // tn) * nt < 1 << 32, (M, N, K, bf16)
     out = ctypes.c_int32()
     f = lib.w8a8_gemm_config
     assert f(4, 8, 64, 0, None, ctypes.byref(out), ctypes.byref(out)) == NULL

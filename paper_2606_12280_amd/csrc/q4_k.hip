@@ -27,6 +27,11 @@
 namespace w8a8 {
 namespace {
 
+// The thread's unit under grid_for().
+__device__ __forceinline__ int64_t unit_index() {
+    return (static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x) * 256 + threadIdx.x;
+}
+
 constexpr int kSub = 32;
 constexpr int kSubs = 8;  // sub-blocks per super-block
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -65,7 +70,7 @@ __global__ __launch_bounds__(256) void q4_k_quantize_kernel(
     const uint16_t *__restrict__ W, int64_t subs, uint8_t *__restrict__ qs,
     uint8_t *__restrict__ sc, uint8_t *__restrict__ mn, uint16_t *__restrict__ d,
     uint16_t *__restrict__ dmin) {
-    const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t j = unit_index();
     // subs is a multiple of 8 and groups of 8 lanes are aligned, so a
     // super-block's lanes are either all in range or all out.
     if (j >= subs) return;
@@ -122,7 +127,7 @@ __global__ __launch_bounds__(256) void q4_k_dequantize_kernel(
     const uint32_t *__restrict__ qs, const uint8_t *__restrict__ sc,
     const uint8_t *__restrict__ mn, const uint16_t *__restrict__ d,
     const uint16_t *__restrict__ dmin, int64_t octets, u32x4 *__restrict__ W) {
-    const int64_t t = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t t = unit_index();
     if (t >= octets) return;
     const int64_t j = t >> 2;  // sub-block (4 octets each)
     const int64_t g = t >> 5;  // super-block (32 octets each)
@@ -139,14 +144,20 @@ __global__ __launch_bounds__(256) void q4_k_dequantize_kernel(
     __builtin_nontemporal_store(u32x4{out[0], out[1], out[2], out[3]}, W + t);
 }
 
-unsigned grid_for(int64_t n) { return static_cast<unsigned>((n + 255) / 256); }
+// Blocks of 256 threads for n units as a 2-D grid whose x extent stays at
+// most 2^20 blocks, so that no dimension reaches 2^32 work-items.
+dim3 grid_for(int64_t n) {
+    const int64_t b = n > 0 ? (n + 255) / 256 : 1;
+    const int64_t x = b < (INT64_C(1) << 20) ? b : (INT64_C(1) << 20);
+    return dim3(static_cast<unsigned>(x), static_cast<unsigned>((b + x - 1) / x));
+}
 
 }  // namespace
 
 hipError_t launch_q4_k_quantize(const uint16_t *W, int64_t N, int64_t K, uint8_t *qs, uint8_t *sc,
                                 uint8_t *mn, uint16_t *d, uint16_t *dmin, hipStream_t stream) {
     const int64_t subs = N * (K / kSub);
-    hipLaunchKernelGGL(q4_k_quantize_kernel, dim3(grid_for(subs)), dim3(256), 0, stream, W, subs,
+    hipLaunchKernelGGL(q4_k_quantize_kernel, grid_for(subs), dim3(256), 0, stream, W, subs,
                        qs, sc, mn, d, dmin);
     return hipGetLastError();
 }
@@ -155,7 +166,7 @@ hipError_t launch_q4_k_dequantize(const uint8_t *qs, const uint8_t *sc, const ui
                                   const uint16_t *d, const uint16_t *dmin, int64_t N, int64_t K,
                                   uint16_t *W, hipStream_t stream) {
     const int64_t octets = N * K / 8;
-    hipLaunchKernelGGL(q4_k_dequantize_kernel, dim3(grid_for(octets)), dim3(256), 0, stream,
+    hipLaunchKernelGGL(q4_k_dequantize_kernel, grid_for(octets), dim3(256), 0, stream,
                        reinterpret_cast<const uint32_t *>(qs), sc, mn, d, dmin, octets,
                        reinterpret_cast<u32x4 *>(W));
     return hipGetLastError();

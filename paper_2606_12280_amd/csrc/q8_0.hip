@@ -18,6 +18,11 @@
 namespace w8a8 {
 namespace {
 
+// The thread's unit under grid_for().
+__device__ __forceinline__ int64_t unit_index() {
+    return (static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x) * 256 + threadIdx.x;
+}
+
 constexpr int kBlock = 32;
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -48,7 +53,7 @@ __global__ __launch_bounds__(256) void q8_0_quantize_kernel(const uint16_t *__re
                                                             int64_t blocks,
                                                             int8_t *__restrict__ qs,
                                                             uint16_t *__restrict__ d) {
-    const int64_t b = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t b = unit_index();
     if (b >= blocks) return;
     const uint4 *src = reinterpret_cast<const uint4 *>(W + b * kBlock);
     float v[kBlock];
@@ -88,7 +93,7 @@ __global__ __launch_bounds__(256) void q8_0_dequantize_kernel(const u32x2 *__res
                                                               const uint16_t *__restrict__ d,
                                                               int64_t octets,
                                                               u32x4 *__restrict__ W) {
-    const int64_t t = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t t = unit_index();
     if (t >= octets) return;
     const float ds = static_cast<float>(__builtin_bit_cast(_Float16, d[t >> 2]));
     const u32x2 q = __builtin_nontemporal_load(qs + t);
@@ -106,14 +111,20 @@ __global__ __launch_bounds__(256) void q8_0_dequantize_kernel(const u32x2 *__res
     __builtin_nontemporal_store(u32x4{out[0], out[1], out[2], out[3]}, W + t);
 }
 
-unsigned grid_for(int64_t n) { return static_cast<unsigned>((n + 255) / 256); }
+// Blocks of 256 threads for n units as a 2-D grid whose x extent stays at
+// most 2^20 blocks, so that no dimension reaches 2^32 work-items.
+dim3 grid_for(int64_t n) {
+    const int64_t b = n > 0 ? (n + 255) / 256 : 1;
+    const int64_t x = b < (INT64_C(1) << 20) ? b : (INT64_C(1) << 20);
+    return dim3(static_cast<unsigned>(x), static_cast<unsigned>((b + x - 1) / x));
+}
 
 }  // namespace
 
 hipError_t launch_q8_0_quantize(const uint16_t *W, int64_t N, int64_t K, int8_t *qs,
                                 uint16_t *d, hipStream_t stream) {
     const int64_t blocks = N * (K / kBlock);
-    hipLaunchKernelGGL(q8_0_quantize_kernel, dim3(grid_for(blocks)), dim3(256), 0, stream, W,
+    hipLaunchKernelGGL(q8_0_quantize_kernel, grid_for(blocks), dim3(256), 0, stream, W,
                        blocks, qs, d);
     return hipGetLastError();
 }
@@ -121,7 +132,7 @@ hipError_t launch_q8_0_quantize(const uint16_t *W, int64_t N, int64_t K, int8_t 
 hipError_t launch_q8_0_dequantize(const int8_t *qs, const uint16_t *d, int64_t N, int64_t K,
                                   uint16_t *W, hipStream_t stream) {
     const int64_t octets = N * K / 8;
-    hipLaunchKernelGGL(q8_0_dequantize_kernel, dim3(grid_for(octets)), dim3(256), 0, stream,
+    hipLaunchKernelGGL(q8_0_dequantize_kernel, grid_for(octets), dim3(256), 0, stream,
                        reinterpret_cast<const u32x2 *>(qs), d, octets,
                        reinterpret_cast<u32x4 *>(W));
     return hipGetLastError();

@@ -565,6 +565,39 @@ def test_q4_k_planes_and_decode_bit_exact(N, K):
     assert np.array_equal(host_bits(ops.q4_k_dequantize(q)), oracle.q4_k_dequantize(ref, N, K))
 
 
+@pytest.mark.parametrize("fmt", ["q8_0", "q4_k"])
+def test_gguf_decode_past_2_28_workgroups(fmt):
+    """A 32832 x 65536 weight: N K / 8 decode threads need more than 2^20
+    workgroups of 256, so the decode grid takes its second dimension (the
+    last 64 rows). The weight is a 64-row block tiled 513 times; the first
+    and last copies are checked against the oracle's decode of the block."""
+    R0, K = 64, 65536
+    N = 513 * R0
+    assert N * K // 8 > (1 << 28)
+    blk = _q8_case([170, R0, K], R0, K) if fmt == "q8_0" else _q4k_case([171, R0, K], R0, K)
+    Wd = dev_bf16(blk).repeat(N // R0, 1)
+    if fmt == "q8_0":
+        qs_ref, d_ref = oracle.q8_0_quantize(blk, R0, K)
+        ref = oracle.q8_0_dequantize(qs_ref, d_ref, R0, K)
+        qs, d = ops.q8_0_quantize(Wd)
+        del Wd
+        out = ops.q8_0_dequantize(qs, d)
+        assert np.array_equal(host(qs[-R0:]), qs_ref)
+        del qs, d
+    else:
+        ref_planes = oracle.q4_k_quantize(blk, R0, K)
+        ref = oracle.q4_k_dequantize(ref_planes, R0, K)
+        q = ops.q4_k_quantize(Wd)
+        del Wd
+        out = ops.q4_k_dequantize(q)
+        assert np.array_equal(host(q.qs[-R0:]), ref_planes["qs"])
+        del q
+    assert np.array_equal(host_bits(out[:R0]), ref)
+    assert np.array_equal(host_bits(out[-R0:]), ref)
+    del out
+    torch.cuda.empty_cache()
+
+
 def test_q4_k_decode_of_arbitrary_planes():
     """Decoding planes the encoder would not produce (every code, 6-bit
     value and a wide range of binary16 scales) matches the oracle."""

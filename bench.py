@@ -41,7 +41,6 @@ PEAK_INT8_TOPS = 5000.0    # MI355X dense INT8 MFMA
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
 GEMM_SOURCES = ["paper_2606_12280_amd/csrc/gemm.hip"]
-QUANT_SOURCES = ["paper_2606_12280_amd/csrc/quant.hip"]
 
 
 def log(*a):

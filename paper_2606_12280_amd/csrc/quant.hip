@@ -175,6 +175,9 @@ hipError_t launch_rows(const uint16_t *src, const float *mul, int64_t R, int64_t
     constexpr int SLOTS = WPB / G;
     const int64_t groups = (R + RPW - 1) / RPW;
     const int64_t blocks = (groups + SLOTS - 1) / SLOTS;
+    // A grid of 2^32 work-items or more cannot be launched. Only R = 2^22
+    // rows with K > 32768 get there, 512 GB of bf16, more than the GPU holds.
+    if (blocks * WPB * 64 >= (INT64_C(1) << 32)) return hipErrorInvalidValue;
     hipLaunchKernelGGL((smooth_quant_rows_kernel<G, CH, RPW, WPB>),
                        dim3(static_cast<unsigned>(blocks)), dim3(WPB * 64), 0, stream, src, mul,
                        R, K, out, scale);

@@ -275,9 +275,11 @@ def test_w8a8_linear_large_ragged(M, N, K, with_bias):
     check_w8a8_output(host_bits(Y), Yref, acc, xs, ws, b)
 
 
-def test_gemm_i32_extremes():
-    """All +-127 codes at K = 16384: |acc| = 127^2 K, the largest sum."""
-    M, N, K = 64, 96, 16384
+@pytest.mark.parametrize("K", [16384, 65536])
+def test_gemm_i32_extremes(K):
+    """All +-127 codes: |acc| = 127^2 K, the largest sum (1.06e9 at the
+    largest K the entry points accept, inside int32)."""
+    M, N = 64, 96
     A = np.full((M, K), 127, np.int8)
     A[1::2] = -127
     B = np.full((N, K), -127, np.int8)

@@ -91,13 +91,13 @@ w8a8_status w8a8_act_absmax(const uint16_t *X, int64_t M, int64_t K,
  *   stats[0] = max |x|, stats[1] = mean, stats[2] = sqrt(m2) (population
  *   standard deviation), stats[3] = m4 / m2^2 (Pearson kurtosis, 3 for a
  *   Gaussian; 0 when m2 == 0).
- * Two passes over X (mean first, then the central sums); a fixed grid and
- * fixed reduction order, so equal inputs give equal bits. work: device
+ * One pass over X: central moments of groups of entries, merged pairwise in
+ * a fixed grid and a fixed order, so equal inputs give equal bits. work: device
  * scratch of W8A8_MOMENTS_WORK_BYTES bytes owned by the caller, 8-byte
  * aligned, overwritten; calls that share it must be ordered on one stream.
  * stats: device, 4 doubles, 8-byte aligned. Same M and K limits as the other
  * calls (K % 64 == 0). */
-#define W8A8_MOMENTS_WORK_BYTES ((2 * 1024 + 2) * 8)
+#define W8A8_MOMENTS_WORK_BYTES (6 * 1024 * 8)
 w8a8_status w8a8_act_moments(const uint16_t *X, int64_t M, int64_t K, void *work,
                              double *stats, w8a8_stream stream);
 

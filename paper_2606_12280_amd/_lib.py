@@ -22,7 +22,7 @@ _S = ctypes.c_int
 
 # name -> (argtypes, restype), in the order of include/w8a8.h
 # W8A8_MOMENTS_WORK_BYTES of the header: scratch of w8a8_act_moments.
-MOMENTS_WORK_BYTES = (2 * 1024 + 2) * 8
+MOMENTS_WORK_BYTES = 6 * 1024 * 8
 
 SIGNATURES = {
     "w8a8_abi_version": ([], ctypes.c_int),

@@ -104,7 +104,7 @@ w8a8_status w8a8_act_absmax(const uint16_t *X, int64_t M, int64_t K, float *absm
 
 w8a8_status w8a8_act_moments(const uint16_t *X, int64_t M, int64_t K, void *work,
                              double *stats, w8a8_stream stream) {
-    static_assert(W8A8_MOMENTS_WORK_BYTES == (2 * w8a8::kMomentBlocks + 2) * 8,
+    static_assert(W8A8_MOMENTS_WORK_BYTES == 6 * w8a8::kMomentBlocks * 8,
                   "workspace size");
     if (X == nullptr || work == nullptr || stats == nullptr) return W8A8_ERR_NULL;
     W8A8_TRY(check_rows(M, kMaxRows));

@@ -25,7 +25,8 @@ hipError_t launch_col_absmax(const uint16_t *src, int64_t R, int64_t K,
 
 // Fragility statistics of the n bf16 entries of X (8 | n): stats[0..3] =
 // max |x|, mean, population std, Pearson kurtosis (binary64). work holds
-// 2 * kMomentBlocks + 2 doubles of partials.
+// 6 * kMomentBlocks doubles: each workgroup's count, mean, central sums of
+// the second to fourth powers and max |x|.
 constexpr int kMomentBlocks = 1024;
 hipError_t launch_act_moments(const uint16_t *X, int64_t n, double *work, double *stats,
                               hipStream_t stream);

@@ -2,16 +2,18 @@
 // fragility profiling and protection"): max |x|, mean, population standard
 // deviation and Pearson kurtosis m4 / m2^2 over all entries of X, in binary64.
 //
-// Two passes over X: the sum and max |x|, then the central sums of the second
-// and fourth powers around the mean (the mean is never folded into raw power
-// sums, which would cancel). Both passes use a fixed grid of kMomentBlocks
-// workgroups walking X in 16-byte chunks with a fixed stride; each workgroup
-// reduces in a fixed order and writes its partials to the caller's workspace,
-// and a single workgroup adds those in order. Every call on the same input
-// therefore returns the same bits. The passes are HBM-bound. The first pass
-// reads X with ordinary loads, so that an X of up to ~200 MB (every DiT
-// linear input) is still in the 256 MB last-level cache for the second,
-// which reads it nontemporally. Each thread keeps 4 chunk loads in flight.
+// One pass over X. A fixed grid of kMomentBlocks workgroups walks X in
+// 16-byte chunks (8 entries) with a fixed stride; each thread takes its
+// chunks kUnroll at a time (the loads first). For such a group of up to 32
+// entries it computes the group's own mean and central sums of the second,
+// third and fourth powers around it, from registers, and merges them into
+// its running state with the pairwise update for central moments (Chan,
+// Golub and LeVeque for the second; Pebay, 2008, for the third and fourth).
+// Sums are never taken of raw powers, which would cancel. The threads'
+// states merge in a fixed tree in LDS and each workgroup writes its state to
+// the caller's workspace; one workgroup then merges the kMomentBlocks states
+// in a fixed tree. Every call on the same input therefore returns the same
+// bits, and X is read once, nontemporally.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -22,7 +24,8 @@ namespace w8a8 {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kFinalThreads = 1024;
+constexpr int kUnroll = 4;      // chunk loads in flight per thread
+constexpr int kStateWords = 6;  // n, mean, M2, M3, M4, max |x| (binary64 each)
 
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
@@ -34,143 +37,159 @@ __device__ __forceinline__ uint4 load_stream(const uint4 *p) {
 __device__ __forceinline__ float lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// Sum over a workgroup of NT threads, in a fixed order: butterfly within each
-// wave, then the wave totals in wave order by thread 0 (valid there only).
-template <int NT>
-__device__ __forceinline__ double group_sum(double v, double *red) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-    const int wave = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) red[wave] = v;
-    __syncthreads();
-    double t = 0.0;
-    if (threadIdx.x == 0)
-        for (int w = 0; w < NT / 64; ++w) t += red[w];
-    __syncthreads();
-    return t;
+// Count, mean and central sums M_j = sum (x - mean)^j of a set of entries.
+struct Moments {
+    double n, mean, m2, m3, m4;
+};
+
+// The moments of the union of two disjoint sets from theirs.
+__device__ __forceinline__ Moments merge(const Moments &a, const Moments &b) {
+    if (b.n == 0.0) return a;
+    if (a.n == 0.0) return b;
+    const double n = a.n + b.n;
+    const double delta = b.mean - a.mean;
+    const double dn = delta / n;
+    const double dn2 = dn * dn;
+    const double ab = a.n * b.n;
+    Moments r;
+    r.n = n;
+    r.mean = a.mean + b.n * dn;
+    r.m2 = a.m2 + b.m2 + delta * dn * ab;
+    r.m3 = a.m3 + b.m3 + delta * dn2 * ab * (a.n - b.n) + 3.0 * dn * (a.n * b.m2 - b.n * a.m2);
+    r.m4 = a.m4 + b.m4 + delta * dn2 * dn * ab * (a.n * a.n - ab + b.n * b.n) +
+           6.0 * dn2 * (a.n * a.n * b.m2 + b.n * b.n * a.m2) + 4.0 * dn * (a.n * b.m3 - b.n * a.m3);
+    return r;
 }
 
-template <int NT>
-__device__ __forceinline__ float group_max(float v, float *red) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
-    const int wave = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) red[wave] = v;
-    __syncthreads();
-    float t = 0.0f;
-    if (threadIdx.x == 0)
-        for (int w = 0; w < NT / 64; ++w) t = fmaxf(t, red[w]);
-    __syncthreads();
-    return t;
+__device__ __forceinline__ void put(double *s, int i, const Moments &m) {
+    s[5 * i] = m.n;
+    s[5 * i + 1] = m.mean;
+    s[5 * i + 2] = m.m2;
+    s[5 * i + 3] = m.m3;
+    s[5 * i + 4] = m.m4;
 }
 
-constexpr int kUnroll = 4;  // chunk loads in flight per thread
+__device__ __forceinline__ Moments get(const double *s, int i) {
+    return Moments{s[5 * i], s[5 * i + 1], s[5 * i + 2], s[5 * i + 3], s[5 * i + 4]};
+}
 
-// Chunks of thread `tid` of the grid: tid, tid + stride, ... in groups of
-// kUnroll (loads first, then the arithmetic in chunk order). Chunks past
-// the end read as zero and are skipped by `valid`.
-template <bool STREAM, class F>
-__device__ __forceinline__ void for_chunks(const uint4 *__restrict__ X, int64_t chunks, F &&f) {
+// Merges the NT threads' states (and maxima) of a workgroup in a fixed tree:
+// at each level thread t < h takes thread t + h's state. Valid in thread 0.
+// (Lane shuffles instead of LDS for the levels inside a wave measured
+// slower: every lane of a wave then runs each level's merge.)
+template <int NT>
+__device__ __forceinline__ Moments group_merge(Moments m, float &mx, double *s, float *smx) {
+    put(s, threadIdx.x, m);
+    smx[threadIdx.x] = mx;
+    __syncthreads();
+#pragma unroll 1
+    for (int h = NT / 2; h > 0; h >>= 1) {
+        if (static_cast<int>(threadIdx.x) < h) {
+            m = merge(m, get(s, threadIdx.x + h));
+            mx = fmaxf(mx, smx[threadIdx.x + h]);
+            put(s, threadIdx.x, m);
+            smx[threadIdx.x] = mx;
+        }
+        __syncthreads();
+    }
+    return m;
+}
+
+// The 8 entries of a chunk, widened (exactly).
+__device__ __forceinline__ void widen8(const uint4 &x, float (&v)[8]) {
+    v[0] = lo(x.x);
+    v[1] = hi(x.x);
+    v[2] = lo(x.y);
+    v[3] = hi(x.y);
+    v[4] = lo(x.z);
+    v[5] = hi(x.z);
+    v[6] = lo(x.w);
+    v[7] = hi(x.w);
+}
+
+// Pass over X: thread t of the grid takes chunks t, t + stride, ... in
+// groups of kUnroll; workgroup b writes its merged state and max |x| to
+// part[kStateWords b ...].
+__global__ __launch_bounds__(kThreads) void moments_pass_kernel(const uint4 *__restrict__ X,
+                                                                int64_t chunks,
+                                                                double *__restrict__ part) {
+    __shared__ double s[5 * kThreads];
+    __shared__ float smx[kThreads];
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
+    Moments st{0.0, 0.0, 0.0, 0.0, 0.0};
+    float mx = 0.0f;
     for (int64_t c0 = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; c0 < chunks;
          c0 += kUnroll * stride) {
         uint4 x[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             const int64_t c = c0 + u * stride;
-            x[u] = c < chunks ? (STREAM ? load_stream(X + c) : X[c]) : make_uint4(0u, 0u, 0u, 0u);
+            x[u] = c < chunks ? load_stream(X + c) : make_uint4(0u, 0u, 0u, 0u);
         }
+        int valid = 0;
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
-            if (c0 + u * stride < chunks) f(x[u]);
-    }
-}
-
-// Pass 1: part[2 b] = sum of x, part[2 b + 1] = max |x| over workgroup b's chunks.
-__global__ __launch_bounds__(kThreads) void moments_sum_kernel(const uint4 *__restrict__ X,
-                                                               int64_t chunks,
-                                                               double *__restrict__ part) {
-    __shared__ double red[kThreads / 64];
-    __shared__ float redf[kThreads / 64];
-    double s = 0.0;
-    float m = 0.0f;
-    for_chunks<false>(X, chunks, [&](const uint4 &x) {
-        const float v[8] = {lo(x.x), hi(x.x), lo(x.y), hi(x.y), lo(x.z), hi(x.z), lo(x.w), hi(x.w)};
+        for (int u = 0; u < kUnroll; ++u) valid += c0 + u * stride < chunks ? 1 : 0;
+        // the group's mean (its entries are exact in binary64; 8 valid ones
+        // per chunk, and zero-filled chunks add nothing to the sum)
+        double dv[kUnroll][8];
+        double sum = 0.0;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            s += static_cast<double>(v[e]);
-            m = fmaxf(m, fabsf(v[e]));
+        for (int u = 0; u < kUnroll; ++u) {
+            float v[8];
+            widen8(x[u], v);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                dv[u][e] = static_cast<double>(v[e]);
+                sum += dv[u][e];
+                mx = fmaxf(mx, fabsf(v[e]));
+            }
         }
-    });
-    s = group_sum<kThreads>(s, red);
-    m = group_max<kThreads>(m, redf);
-    if (threadIdx.x == 0) {
-        part[2 * blockIdx.x] = s;
-        part[2 * blockIdx.x + 1] = static_cast<double>(m);
-    }
-}
-
-// mm[0] = mean = (sum of the partial sums) / n, mm[1] = max |x|.
-__global__ __launch_bounds__(kFinalThreads) void moments_mean_kernel(
-    const double *__restrict__ part, int blocks, double n, double *__restrict__ mm) {
-    __shared__ double red[kFinalThreads / 64];
-    __shared__ float redf[kFinalThreads / 64];
-    double s = 0.0;
-    float m = 0.0f;
-    for (int b = threadIdx.x; b < blocks; b += kFinalThreads) {
-        s += part[2 * b];
-        m = fmaxf(m, static_cast<float>(part[2 * b + 1]));
-    }
-    s = group_sum<kFinalThreads>(s, red);
-    m = group_max<kFinalThreads>(m, redf);
-    if (threadIdx.x == 0) {
-        mm[0] = s / n;
-        mm[1] = static_cast<double>(m);
-    }
-}
-
-// Pass 2: part[2 b] = sum of (x - mean)^2, part[2 b + 1] = sum of (x - mean)^4.
-__global__ __launch_bounds__(kThreads) void moments_central_kernel(
-    const uint4 *__restrict__ X, int64_t chunks, const double *__restrict__ mm,
-    double *__restrict__ part) {
-    __shared__ double red[kThreads / 64];
-    const double mean = mm[0];
-    double s2 = 0.0, s4 = 0.0;
-    for_chunks<true>(X, chunks, [&](const uint4 &x) {
-        const float v[8] = {lo(x.x), hi(x.x), lo(x.y), hi(x.y), lo(x.z), hi(x.z), lo(x.w), hi(x.w)};
+        const double cnt = 8.0 * valid;
+        const double gm = valid == kUnroll ? sum * (1.0 / (8.0 * kUnroll)) : sum / cnt;
+        // central sums around it; the third and fourth powers accumulate
+        // with fused multiply-adds (one rounding each)
+        double g2 = 0.0, g3 = 0.0, g4 = 0.0;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const double d = static_cast<double>(v[e]) - mean;
-            const double d2 = d * d;
-            s2 += d2;
-            s4 += d2 * d2;
+        for (int u = 0; u < kUnroll; ++u) {
+            if (u >= valid) break;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const double d = dv[u][e] - gm;
+                const double d2 = d * d;
+                g2 += d2;
+                g3 = __builtin_fma(d2, d, g3);
+                g4 = __builtin_fma(d2, d2, g4);
+            }
         }
-    });
-    s2 = group_sum<kThreads>(s2, red);
-    s4 = group_sum<kThreads>(s4, red);
+        st = merge(st, Moments{cnt, gm, g2, g3, g4});
+    }
+    st = group_merge<kThreads>(st, mx, s, smx);
     if (threadIdx.x == 0) {
-        part[2 * blockIdx.x] = s2;
-        part[2 * blockIdx.x + 1] = s4;
+        double *o = part + kStateWords * blockIdx.x;
+        o[0] = st.n;
+        o[1] = st.mean;
+        o[2] = st.m2;
+        o[3] = st.m3;
+        o[4] = st.m4;
+        o[5] = static_cast<double>(mx);
     }
 }
 
-// stats = [max |x|, mean, sqrt(m2), m4 / m2^2 (0 when m2 == 0)].
-__global__ __launch_bounds__(kFinalThreads) void moments_final_kernel(
-    const double *__restrict__ part, int blocks, double n, const double *__restrict__ mm,
-    double *__restrict__ stats) {
-    __shared__ double red[kFinalThreads / 64];
-    double s2 = 0.0, s4 = 0.0;
-    for (int b = threadIdx.x; b < blocks; b += kFinalThreads) {
-        s2 += part[2 * b];
-        s4 += part[2 * b + 1];
-    }
-    s2 = group_sum<kFinalThreads>(s2, red);
-    s4 = group_sum<kFinalThreads>(s4, red);
+// stats = [max |x|, mean, sqrt(m2), m4 / m2^2 (0 when m2 == 0)] from the
+// kMomentBlocks workgroup states, merged in a fixed tree.
+__global__ __launch_bounds__(kMomentBlocks) void moments_final_kernel(
+    const double *__restrict__ part, double *__restrict__ stats) {
+    __shared__ double s[5 * kMomentBlocks];
+    __shared__ float smx[kMomentBlocks];
+    const double *p = part + kStateWords * threadIdx.x;
+    Moments m{p[0], p[1], p[2], p[3], p[4]};
+    float mx = static_cast<float>(p[5]);
+    m = group_merge<kMomentBlocks>(m, mx, s, smx);
     if (threadIdx.x == 0) {
-        const double m2 = s2 / n;
-        const double m4 = s4 / n;
-        stats[0] = mm[1];
-        stats[1] = mm[0];
+        const double m2 = m.m2 / m.n;
+        const double m4 = m.m4 / m.n;
+        stats[0] = static_cast<double>(mx);
+        stats[1] = m.mean;
         stats[2] = sqrt(m2);
         stats[3] = m2 > 0.0 ? m4 / (m2 * m2) : 0.0;
     }
@@ -181,18 +200,10 @@ __global__ __launch_bounds__(kFinalThreads) void moments_final_kernel(
 hipError_t launch_act_moments(const uint16_t *X, int64_t n, double *work, double *stats,
                               hipStream_t stream) {
     const int64_t chunks = n / 8;  // the entry point guarantees 8 | n
-    const uint4 *x4 = reinterpret_cast<const uint4 *>(X);
-    double *part = work;
-    double *mm = work + 2 * kMomentBlocks;
-    const double dn = static_cast<double>(n);
-    hipLaunchKernelGGL(moments_sum_kernel, dim3(kMomentBlocks), dim3(kThreads), 0, stream, x4,
-                       chunks, part);
-    hipLaunchKernelGGL(moments_mean_kernel, dim3(1), dim3(kFinalThreads), 0, stream, part,
-                       kMomentBlocks, dn, mm);
-    hipLaunchKernelGGL(moments_central_kernel, dim3(kMomentBlocks), dim3(kThreads), 0, stream,
-                       x4, chunks, mm, part);
-    hipLaunchKernelGGL(moments_final_kernel, dim3(1), dim3(kFinalThreads), 0, stream, part,
-                       kMomentBlocks, dn, mm, stats);
+    hipLaunchKernelGGL(moments_pass_kernel, dim3(kMomentBlocks), dim3(kThreads), 0, stream,
+                       reinterpret_cast<const uint4 *>(X), chunks, work);
+    hipLaunchKernelGGL(moments_final_kernel, dim3(1), dim3(kMomentBlocks), 0, stream, work,
+                       stats);
     return hipGetLastError();
 }
 

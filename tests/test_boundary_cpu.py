@@ -154,7 +154,8 @@ def test_moments_validation(lib):
     assert f(A, 8, 64, A + 512, C, None) == ALIAS     # workspace inside X (1 KiB)
     assert f(A, 8, 64, B, B + 1024, None) == ALIAS    # stats inside the workspace
     assert f(A, 8, 64, B, A, None) == ALIAS
-    assert _lib.MOMENTS_WORK_BYTES == (2 * 1024 + 2) * 8
+    expr = re.search(r"#define W8A8_MOMENTS_WORK_BYTES \(([^\n]*)\)\n", open(HEADER).read())
+    assert expr and _lib.MOMENTS_WORK_BYTES == eval(expr.group(1), {}) == 6 * 1024 * 8
 
 
 def test_q8_0_validation(lib):

@@ -6,7 +6,9 @@
 //   mean = sum_k x_k / K,  var = sum_k (x_k - mean)^2 / K,
 //   rstd = 1 / sqrt(var + eps),
 //   h_k = bf16(((x_k - mean) * rstd) * (1 + scale_k) + shift_k)
-// in binary64 (h is the bf16 tensor the unfused model would hold), then the
+// in binary64 (h is the bf16 tensor the unfused model would hold; the
+// squares accumulate and the modulation applies with fused multiply-adds,
+// which moves a binary64 result by at most an ulp of it), then the
 // W8A8 activation step on h exactly as w8a8_quant_act does it: binary32
 // v_k = float(h_k) * inv_lambda_k, absmax, scale absmax / 127, codes
 // clamp(rint(v_k * RN(127 / absmax)), -127, 127). h never leaves registers:
@@ -182,7 +184,7 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const double d = static_cast<double>(v[e]) - mean;
-                q += d * d;
+                q = __builtin_fma(d, d, q);
             }
         }
         q = wave_sum(q);
@@ -205,7 +207,7 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const double n = (static_cast<double>(v[e]) - mean) * rstd;
-                const double t = n * one_sc[c][e] + shd[c][e];
+                const double t = __builtin_fma(n, one_sc[c][e], shd[c][e]);
                 f[e] = static_cast<float>(t);
                 mid |= bf16_midpoint(f[e]);
             }
@@ -217,7 +219,7 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
                 for (int e = 0; e < 8; ++e) {
                     if (!bf16_midpoint(f[e])) continue;
                     const double n = (static_cast<double>(v[e]) - mean) * rstd;
-                    const double t = n * one_sc[c][e] + shd[c][e];
+                    const double t = __builtin_fma(n, one_sc[c][e], shd[c][e]);
                     const uint32_t h = bf16_bits_past_midpoint(t, f[e]);
                     const int sh = 16 * (e & 1);
                     w[e >> 1] = (w[e >> 1] & ~(0xffffu << sh)) | (h << sh);

@@ -24,7 +24,8 @@
  *     nothing is enqueued. A failed launch returns W8A8_ERR_HIP. Faults in
  *     the kernels surface at the caller's next synchronization.
  *   - Sizes: 1 <= M <= 2^22 rows (tokens; also N for the weight-side row
- *     kernels); GEMM outputs 1 <= N <= 2^20 and M * N <= 2^38;
+ *     kernels; fewer than 2^22 when K > 32768, W8A8_ERR_SHAPE otherwise);
+ *     GEMM outputs 1 <= N <= 2^20 and M * N <= 2^38;
  *     64 <= K <= 65536 with K % 64 == 0 (the int32 sum is then exact:
  *     127^2 * K < 2^31). Ragged M and N need no padding. Matrix pointers
  *     and lambda / inv_lambda must be 16-byte aligned; scales 4-byte and

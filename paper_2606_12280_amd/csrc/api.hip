@@ -53,6 +53,12 @@ w8a8_status check_k(int64_t K) {
     return W8A8_OK;
 }
 
+// The row kernels give a row of K > 32768 a workgroup of 1024 threads; 2^22
+// such rows (512 GB of bf16) would make a grid of 2^32 work-items.
+w8a8_status check_row_grid(int64_t rows, int64_t K) {
+    return K > 32768 && rows >= kMaxRows ? W8A8_ERR_SHAPE : W8A8_OK;
+}
+
 w8a8_status check_rows(int64_t R, int64_t max_rows) {
     return (R < 1 || R > max_rows) ? W8A8_ERR_SHAPE : W8A8_OK;
 }
@@ -137,6 +143,7 @@ w8a8_status w8a8_prepare_weight(const uint16_t *W, const float *lambda, int64_t 
         return W8A8_ERR_NULL;
     W8A8_TRY(check_rows(N, kMaxRows));
     W8A8_TRY(check_k(K));
+    W8A8_TRY(check_row_grid(N, K));
     if (!aligned(W, 16) || !aligned(Wq, 16) || !aligned(lambda, 16) || !aligned(w_scale, 4) ||
         !aligned(inv_lambda, 4))
         return W8A8_ERR_ALIGN;
@@ -153,6 +160,7 @@ w8a8_status w8a8_quant_act(const uint16_t *X, const float *inv_lambda, int64_t M
         return W8A8_ERR_NULL;
     W8A8_TRY(check_rows(M, kMaxRows));
     W8A8_TRY(check_k(K));
+    W8A8_TRY(check_row_grid(M, K));
     if (!aligned(X, 16) || !aligned(Xq, 16) || !aligned(inv_lambda, 16) || !aligned(x_scale, 4))
         return W8A8_ERR_ALIGN;
     W8A8_TRY(check_alias({{Xq, M * K}, {x_scale, 4 * M}}, {{X, 2 * M * K}, {inv_lambda, 4 * K}}));

@@ -60,6 +60,7 @@ def test_quant_act_validation(lib):
     assert f(A, B, 4, 0, C, D, None) == SHAPE
     assert f(A, B, 4, 100, C, D, None) == UNSUP
     assert f(A, B, 4, 65536 + 64, C, D, None) == UNSUP
+    assert f(A, B, 1 << 22, 32768 + 64, C, D, None) == SHAPE  # a 2^32 work-item grid
     assert f(A + 8, B, 4, 64, C, D, None) == ALIGN
     assert f(A, B + 4, 4, 64, C, D, None) == ALIGN
     assert f(A, B, 4, 64, C + 1, D, None) == ALIGN

@@ -373,7 +373,7 @@ def test_bf16_linear_small_integers_exact(M, N, K):
 
 
 @pytest.mark.parametrize("M,N,K", [(64, 512, 256), (300, 520, 1088), (65, 128, 16384),
-                                   (4571, 16376, 192)])
+                                   (4571, 16376, 192), (33, 70, 65536)])
 def test_bf16_linear_random(M, N, K):
     c = synth.linear_case([114, M, N, K], M, N, K, act="gelu")
     Y = host_bits(ops.bf16_linear(dev_bf16(c["X"]), dev_bf16(c["W"]), dev_bf16(c["bias"])))

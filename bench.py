@@ -14,7 +14,9 @@ paths), dit_block (the four linears of a block, both CFG branches), backbone
 Prints one JSON line. ``value`` is the step's throughput in TOPS
 (2 M N K per step divided by the step time). ``roofline`` covers the dominant
 kernel (the INT8 GEMM). ``cpu_baseline`` is the CPU oracle timed on a bounded
-sample of the same workload on this host.
+sample of the same workload on this host. ``eager_torch`` times the dominant
+layer run the way the paper runs it, as eager Torch ops with torch._int_mm for
+the GEMM, on the same GPU.
 """
 from __future__ import annotations
 
@@ -345,6 +347,59 @@ def absmax_isolated(lin: Linear, dev, reps: int = 30, rounds: int = 5):
     return float(np.median(per)), float(per.min()), float(per.max())
 
 
+def eager_torch(lin: Linear, dev, reps: int = 20, rounds: int = 5):
+    """The same layer as the paper runs it: eager Torch ops, one pass each
+    (smoothing, per-token absmax, scale, round and clamp, INT8 GEMM by
+    torch._int_mm, dequantization and bias), on this GPU. Timing context
+    only; it is no part of the library. Returns (median us per layer, median
+    us of the _int_mm alone, mean |difference| to the fused path's output
+    over mean |output|)."""
+    lay = lin.lay
+    X = lin.xs[0]
+    Wt = lay.Wq.t()
+    inv = lay.inv_lambda
+    ws_ = lay.w_scale
+    b = lay.bias.float() if lay.bias is not None else None
+
+    def step():
+        xs_ = X.float() * inv
+        s = xs_.abs().amax(dim=1, keepdim=True) / 127.0
+        q = torch.clamp(torch.round(xs_ / s), -127, 127).to(torch.int8)
+        y = torch._int_mm(q, Wt).float() * s * ws_
+        if b is not None:
+            y = y + b
+        return y.bfloat16(), q
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        per = []
+        for _ in range(rounds):
+            a = torch.cuda.Event(enable_timing=True)
+            e = torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(reps):
+                fn()
+            e.record()
+            torch.cuda.synchronize()
+            per.append(a.elapsed_time(e) * 1e3 / reps)
+        return float(np.median(per))
+
+    y, q = step()
+    ours = torch.empty_like(y)
+    Xq = torch.empty(lin.M, lay.K, dtype=torch.int8, device=dev)
+    xsc = torch.empty(lin.M, dtype=torch.float32, device=dev)
+    lin.quant(X, Xq, xsc)
+    ops.w8a8_linear(Xq, xsc, lay.Wq, lay.w_scale, lay.bias, out=ours)
+    torch.cuda.synchronize()
+    diff = float((y.float() - ours.float()).abs().mean() / ours.float().abs().mean())
+    us = timed(step)
+    us_mm = timed(lambda: torch._int_mm(q, Wt))
+    del y, q, ours, Xq
+    return us, us_mm, diff
+
+
 def quant_bytes(M, K) -> int:
     """Algorithmic bytes of one quant launch: read X (bf16) and inv_lambda,
     write Xq (int8) and x_scale."""
@@ -544,6 +599,8 @@ def main():
                              "q4_k_ffn_up", "adaln_ffn_up"])
     ap.add_argument("--pool", type=int, default=4, help="distinct inputs rotated over steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-eager", action="store_true",
+                    help="skip timing the eager Torch pipeline beside the fused path")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--counter-run", action="store_true",
                     help="only the short launch sequence the counter passes profile")
@@ -669,6 +726,17 @@ def main():
                     "traffic": counter_traffic(args.workload),
                     "ops_per_launch": lin.ops, "avg_launch_us": round(float(gemm_us[dom]), 2)}
 
+    eager = None
+    if dom is not None and not args.no_eager and layers[dom].mod is None:
+        lin = layers[dom]
+        fused = float(quant_us[dom] + gemm_us[dom])
+        us, us_mm, diff = eager_torch(lin, dev)
+        eager = {"kind": "the layer as eager Torch ops (smoothing, absmax, round, clamp, "
+                         "torch._int_mm, dequantization, bias), one pass each",
+                 "shape": [lin.M, lin.lay.K, lin.lay.N], "us": round(us, 2),
+                 "int_mm_us": round(us_mm, 2), "fused_us": round(fused, 2),
+                 "speedup": round(us / fused, 3), "mean_abs_diff_rel": round(diff, 6)}
+
     cpu = None
     if not args.no_cpu_baseline and args.workload in ("ffn_up", "ffn_down"):
         log("timing the CPU oracle on a bounded sample ...")
@@ -691,7 +759,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if gg and not w8 else "int8",
         "data": "synthetic", "config": cfg, "roofline": roofline, "cpu_baseline": cpu,
-        "kernels": kernels, "ms_per_step_with_kernel_events": round(step_ms_ev, 4),
+        "eager_torch": eager, "kernels": kernels, "ms_per_step_with_kernel_events": round(step_ms_ev, 4),
         "host_wall_ms_per_step": round(wall_ms, 4),
         "device": {"name": props.name, "arch": getattr(props, "gcnArchName", ""),
                    "cus": props.multi_processor_count},

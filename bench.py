@@ -13,7 +13,8 @@ paths), dit_block (the four linears of a block, both CFG branches), backbone
 
 Prints one JSON line. ``value`` is the step's throughput in TOPS
 (2 M N K per step divided by the step time). ``roofline`` covers the dominant
-kernel (the INT8 GEMM). ``cpu_baseline`` is the CPU oracle timed on a bounded
+kernel (the INT8 GEMM); its ``clock`` holds the XCD clocks read while that
+kernel runs back to back and the fraction of the peak at that clock. ``cpu_baseline`` is the CPU oracle timed on a bounded
 sample of the same workload on this host. ``eager_torch`` times the dominant
 layer run the way the paper runs it, as eager Torch ops with torch._int_mm for
 the GEMM, on the same GPU.
@@ -42,6 +43,7 @@ METRIC = "W8A8 linear TOPS (% INT8 MFMA peak) + act-quant GB/s at DiT FFN shapes
 PEAK_INT8_TOPS = 5000.0    # MI355X dense INT8 MFMA
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
+PEAK_CLOCK_MHZ = 2400.0    # the engine clock the MFMA peaks are quoted at
 GEMM_SOURCES = ["paper_2606_12280_amd/csrc/gemm.hip"]
 
 
@@ -400,6 +402,75 @@ def eager_torch(lin: Linear, dev, reps: int = 20, rounds: int = 5):
     return us, us_mm, diff
 
 
+def _amdsmi_handle(amdsmi, dev):
+    """The amdsmi handle of torch device `dev` (matched by PCI address)."""
+    props = torch.cuda.get_device_properties(dev)
+    want = (getattr(props, "pci_domain_id", None), getattr(props, "pci_bus_id", None),
+            getattr(props, "pci_device_id", None))
+    handles = amdsmi.amdsmi_get_processor_handles()
+    for h in handles:
+        try:
+            bdf = amdsmi.amdsmi_get_gpu_device_bdf(h)  # "dddd:bb:dd.f"
+            dom, bus, rest = bdf.split(":")
+            if (int(dom, 16), int(bus, 16), int(rest.split(".")[0], 16)) == want:
+                return h
+        except Exception:
+            continue
+    return handles[0] if len(handles) == 1 else None
+
+
+def clock_under_load(lin: Linear, dev, seconds: float = 3.0):
+    """The graphics clock of each XCD while `lin`'s INT8 GEMM runs back to
+    back, read in-process from the GPU metrics table through amdsmi (no
+    child process). The first second is left out while the clock settles.
+    None where amdsmi or the metric is missing."""
+    try:
+        import amdsmi
+        amdsmi.amdsmi_init()
+    except Exception:
+        return None
+    try:
+        h = _amdsmi_handle(amdsmi, dev)
+        if h is None:
+            return None
+        Xq = torch.empty(lin.M, lin.lay.K, dtype=torch.int8, device=dev)
+        xsc = torch.empty(lin.M, dtype=torch.float32, device=dev)
+        lin.quant(lin.xs[0], Xq, xsc)
+        per = max(1, int(10e-3 / max(lin.ops / 2.5e15, 1e-6)))  # about 10 ms of launches
+        samples = []
+        t0 = time.perf_counter()
+        last = 0.0
+        while time.perf_counter() - t0 < seconds:
+            for _ in range(per):
+                ops.w8a8_linear(Xq, xsc, lin.lay.Wq, lin.lay.w_scale, lin.lay.bias, out=lin.Y)
+            torch.cuda.synchronize()
+            now = time.perf_counter() - t0
+            if now > 1.0 and now - last > 0.05:
+                last = now
+                clks = amdsmi.amdsmi_get_gpu_metrics_info(h).get("current_gfxclks")
+                if isinstance(clks, (list, tuple)):
+                    clks = [int(c) for c in clks if isinstance(c, (int, float)) and 0 < c < 10000]
+                    if clks:
+                        samples.append(clks)
+        del Xq, xsc
+        if not samples or len({len(c) for c in samples}) != 1:
+            return None
+        a = np.array(samples, dtype=np.float64)
+        per_xcd = a.mean(axis=0)
+        return {"source": "amdsmi GPU metrics (current_gfxclks), sampled in-process during "
+                          f"{seconds:.0f} s of back-to-back launches of this kernel",
+                "mhz_per_xcd": [round(float(v)) for v in per_xcd],
+                "mhz_mean": round(float(per_xcd.mean()), 1),
+                "mhz_min": round(float(per_xcd.min()), 1), "samples": len(samples)}
+    except Exception:
+        return None
+    finally:
+        try:
+            amdsmi.amdsmi_shut_down()
+        except Exception:
+            pass
+
+
 def quant_bytes(M, K) -> int:
     """Algorithmic bytes of one quant launch: read X (bf16) and inv_lambda,
     write Xq (int8) and x_scale."""
@@ -599,6 +670,8 @@ def main():
                              "q4_k_ffn_up", "adaln_ffn_up"])
     ap.add_argument("--pool", type=int, default=4, help="distinct inputs rotated over steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-clock", action="store_true",
+                    help="skip reading the XCD clocks under load (amdsmi)")
     ap.add_argument("--no-eager", action="store_true",
                     help="skip timing the eager Torch pipeline beside the fused path")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -725,6 +798,12 @@ def main():
                     "frac": round(ach / PEAK_INT8_TOPS, 4),
                     "traffic": counter_traffic(args.workload),
                     "ops_per_launch": lin.ops, "avg_launch_us": round(float(gemm_us[dom]), 2)}
+        clk = None if args.no_clock else clock_under_load(lin, dev)
+        if clk is not None:
+            clk["peak_clock_mhz"] = PEAK_CLOCK_MHZ
+            clk["frac_at_measured_clock"] = round(
+                ach / (PEAK_INT8_TOPS * clk["mhz_mean"] / PEAK_CLOCK_MHZ), 4)
+        roofline["clock"] = clk
 
     eager = None
     if dom is not None and not args.no_eager and layers[dom].mod is None:

@@ -513,10 +513,14 @@ def cpu_baseline(workload: str, target_s: float = 10.0):
     Wq, ws, il = oracle.prepare_weight(c["W"], lam, N, K)   # offline, not timed
     X = c["X"].reshape(M, K)
 
+    tq = [0.0]   # time in the quant step, summed over the timed runs
+
     def run(rows):
         t = time.perf_counter()
         Xq, xs = oracle.quant_act(X[:rows], il, rows, K)
+        t1 = time.perf_counter()
         oracle.w8a8_linear(Xq, xs, Wq, ws, c["bias"], rows, N, K)
+        tq[0] = t1 - t
         return time.perf_counter() - t
 
     # Size the sample from a small probe, then once more from a mid-sized
@@ -530,13 +534,17 @@ def cpu_baseline(workload: str, target_s: float = 10.0):
         rows = max(16, rows // 16 * 16)
         dt = run(rows)
     reps = 1
+    q = tq[0]
     while rows >= M and dt < target_s and reps < 3:
         dt += run(rows)
+        q += tq[0]
         reps += 1
     tops = 2.0 * rows * N * K * reps / dt / 1e12
     what = f"{rows} of {M} token rows" if reps == 1 else f"{reps} runs of all {M} token rows"
     return {"value": round(tops, 6), "unit": "TOPS", "cores": oracle.num_threads(),
             "kind": "oracle",
+            "quant_GB_s": round((3 * rows * K + 4 * rows) * reps / q / 1e9, 3),
+            "gemm_epilogue_TOPS": round(2.0 * rows * N * K * reps / (dt - q) / 1e12, 6),
             "sample": f"{what} of the {M}x{K}->{N} linear: smoothing + per-token quant + "
                       f"int32 GEMM + bf16 epilogue (weights prepared outside the timing), "
                       f"{dt:.1f} s"}

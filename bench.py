@@ -17,7 +17,8 @@ kernel (the INT8 GEMM); its ``clock`` holds the XCD clocks read while that
 kernel runs back to back and the fraction of the peak at that clock. ``cpu_baseline`` is the CPU oracle timed on a bounded
 sample of the same workload on this host. ``eager_torch`` times the dominant
 layer run the way the paper runs it, as eager Torch ops with torch._int_mm for
-the GEMM, on the same GPU.
+the GEMM, on the same GPU. ``accuracy`` (FFN workloads) gives the W8A8 and
+bf16 paths' error against X W^T + b in binary64.
 """
 from __future__ import annotations
 
@@ -75,6 +76,7 @@ class Linear:
         self.M = xs[0].shape[0]
         self.Y = torch.empty(self.M, lay.N, dtype=torch.bfloat16, device=xs[0].device)
         self.mod = None   # (shift, scale) bf16 [K]: the input is adaLN-modulated first
+        self.case = None  # the host case the layer and xs[0] were made from, if any
 
     def quant(self, X, Xq, xs):
         """The activation step of this layer (fused with adaLN if modulated)."""
@@ -118,7 +120,9 @@ def host_case_linear(name, case, dev, pool: int, protected: bool, seed_base) -> 
         else:
             x = synth.outlier_activations(rng, M, K, int(round(0.01 * K)), 20.0)
         xs.append(to_dev_bf16(synth.to_bf16_bits(x), dev))
-    return Linear(name, lay, xs)
+    lin = Linear(name, lay, xs)
+    lin.case = case
+    return lin
 
 
 def device_linear(name, M, N, K, dev, gen: torch.Generator, protected: bool, x_pool) -> Linear:
@@ -402,6 +406,42 @@ def eager_torch(lin: Linear, dev, reps: int = 20, rounds: int = 5):
     return us, us_mm, diff
 
 
+def accuracy_report(layers, dev):
+    """Error of the W8A8 and bf16 paths of the workload's layer against
+    X W^T + b in binary64 (numpy on the host, from the same seeded case):
+    relative Frobenius norm and largest absolute difference of the bf16
+    output. Where the workload has no protected copy, the bf16 path runs on
+    the case's weights for comparison."""
+    lin = next(l for l in layers if l.case is not None and not l.lay.protected)
+    c = lin.case
+    M, N, K = c["M"], c["N"], c["K"]
+    X = synth.bf16_bits_to_f32(c["X"]).reshape(M, K).astype(np.float64)
+    W = synth.bf16_bits_to_f32(c["W"]).reshape(N, K).astype(np.float64)
+    b = synth.bf16_bits_to_f32(c["bias"]).astype(np.float64)
+    ref = X @ W.T + b
+    del X, W
+    nref = float(np.linalg.norm(ref))
+
+    def err(Y):
+        d = Y.float().cpu().numpy().astype(np.float64) - ref
+        return {"rel_frobenius": float(f"{np.linalg.norm(d) / nref:.4g}"),
+                "max_abs": float(f"{np.abs(d).max():.4g}")}
+
+    out = {"shape": [M, K, N], "reference": "X W^T + b in binary64 (numpy, host)",
+           "max_abs_reference": float(f"{np.abs(ref).max():.4g}")}
+    Xq = torch.empty(M, K, dtype=torch.int8, device=dev)
+    xsc = torch.empty(M, dtype=torch.float32, device=dev)
+    lin.quant(lin.xs[0], Xq, xsc)
+    Y = ops.w8a8_linear(Xq, xsc, lin.lay.Wq, lin.lay.w_scale, lin.lay.bias)
+    out["w8a8"] = err(Y)
+    prot = next((l for l in layers if l.lay.protected and l.case is c), None)
+    Wd = prot.lay.W if prot is not None else to_dev_bf16(c["W"].reshape(N, K), dev)
+    Y = ops.bf16_linear(lin.xs[0], Wd, lin.lay.bias)
+    out["bf16"] = err(Y)
+    del Y, Xq, Wd
+    return out
+
+
 def _amdsmi_handle(amdsmi, dev):
     """The amdsmi handle of torch device `dev` (matched by PCI address)."""
     props = torch.cuda.get_device_properties(dev)
@@ -678,6 +718,8 @@ def main():
                              "q4_k_ffn_up", "adaln_ffn_up"])
     ap.add_argument("--pool", type=int, default=4, help="distinct inputs rotated over steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-accuracy", action="store_true",
+                    help="skip the error report against a binary64 product")
     ap.add_argument("--no-clock", action="store_true",
                     help="skip reading the XCD clocks under load (amdsmi)")
     ap.add_argument("--no-eager", action="store_true",
@@ -824,6 +866,11 @@ def main():
                  "int_mm_us": round(us_mm, 2), "fused_us": round(fused, 2),
                  "speedup": round(us / fused, 3), "mean_abs_diff_rel": round(diff, 6)}
 
+    accuracy = None
+    if not args.no_accuracy and args.workload in ("ffn_up", "ffn_down"):
+        log("error against a binary64 product on the host ...")
+        accuracy = accuracy_report(layers, dev)
+
     cpu = None
     if not args.no_cpu_baseline and args.workload in ("ffn_up", "ffn_down"):
         log("timing the CPU oracle on a bounded sample ...")
@@ -846,7 +893,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if gg and not w8 else "int8",
         "data": "synthetic", "config": cfg, "roofline": roofline, "cpu_baseline": cpu,
-        "eager_torch": eager, "kernels": kernels, "ms_per_step_with_kernel_events": round(step_ms_ev, 4),
+        "eager_torch": eager, "accuracy": accuracy, "kernels": kernels, "ms_per_step_with_kernel_events": round(step_ms_ev, 4),
         "host_wall_ms_per_step": round(wall_ms, 4),
         "device": {"name": props.name, "arch": getattr(props, "gcnArchName", ""),
                    "cus": props.multi_processor_count},

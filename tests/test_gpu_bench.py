@@ -1,0 +1,53 @@
+"""bench.py on the GPU, run in this process with few steps: the JSON line
+carries the fields its contract names (metric, value, roofline with the
+clocks under load, the eager Torch comparison, the error report), and the
+W8A8 and bf16 paths' errors against X W^T + b in binary64 on the FFN-up case
+stay within what the recipe and the bf16 output rounding allow."""
+from __future__ import annotations
+
+import json
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+pytestmark = pytest.mark.gpu
+
+
+def test_bench_json_line(capsys, monkeypatch):
+    sys.path.insert(0, ROOT)
+    import bench
+
+    print("bench.py --steps 3 --warmup 1 --pool 1 --no-cpu-baseline", flush=True)
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--steps", "3", "--warmup", "1", "--pool", "1",
+                                      "--no-cpu-baseline"])
+    capsys.readouterr()
+    bench.main()
+    line = capsys.readouterr().out.strip().splitlines()[-1]
+    d = json.loads(line)
+    assert d["metric"] == bench.METRIC and d["unit"] == "TOPS" and d["n_gpus"] == 1
+    assert d["steps"] == 3 and d["warmup"] == 1 and d["higher_is_better"] is True
+    assert d["value"] > 0 and d["ms_per_step"] > 0 and d["dtype"] == "int8"
+    assert d["config"]["workload"].startswith("DiT FFN up-projection 4608x4096->16384")
+    r = d["roofline"]
+    assert r["bound"] == "mfma" and r["unit"] == "TOP/s" and r["peak"] == 5000.0
+    assert r["ops_per_launch"] == 2 * 4608 * 4096 * 16384
+    assert r["achieved"] == pytest.approx(r["ops_per_launch"] / r["avg_launch_us"] / 1e6, rel=1e-3)
+    assert 0 < r["frac"] < 1
+    clk = r["clock"]
+    if clk is not None:  # amdsmi present
+        assert len(clk["mhz_per_xcd"]) == 8 and 100 < clk["mhz_mean"] <= 2400
+        assert r["frac"] < clk["frac_at_measured_clock"] < 1
+    e = d["eager_torch"]
+    assert e["shape"] == [4608, 4096, 16384] and e["us"] > 0 and e["fused_us"] > 0
+    assert e["mean_abs_diff_rel"] < 1e-3
+    a = d["accuracy"]
+    assert a["shape"] == [4608, 4096, 16384]
+    # bf16 output rounding alone: at most half an ulp, 2^-8 relative; its rms
+    # over many outputs is near 2^-8 / sqrt(3)
+    assert a["bf16"]["rel_frobenius"] < 2.0 ** -8
+    # per-token and per-channel 8-bit grids with outlier channels smoothed
+    assert a["bf16"]["rel_frobenius"] < a["w8a8"]["rel_frobenius"] < 0.05
+    assert d["cpu_baseline"] is None

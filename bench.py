@@ -260,14 +260,16 @@ def measure(layers, steps: int, warmup: int, dev, per_kernel: bool, warm_ms: flo
     total_ms = t0.elapsed_time(t1)
     quant_us = np.zeros(len(layers))
     gemm_us = np.zeros(len(layers))
+    gemm_each = np.zeros((steps, len(layers)))
     if ev:
         for s in range(steps):
             for li in range(len(layers)):
                 a, b, c = ev[s][li]
                 quant_us[li] += a.elapsed_time(b) * 1e3
-                gemm_us[li] += b.elapsed_time(c) * 1e3
+                gemm_each[s, li] = b.elapsed_time(c) * 1e3
         quant_us /= steps
-        gemm_us /= steps
+        gemm_us = gemm_each.mean(axis=0)
+    measure.gemm_each = gemm_each  # per-step GEMM times of the last call, us
     return total_ms / steps, wall / steps * 1e3, quant_us, gemm_us
 
 
@@ -761,6 +763,7 @@ def main():
 
     # per-kernel durations inside the timed steps (events between kernels)
     step_ms_ev, _, quant_us, gemm_us = measure(layers, args.steps, args.warmup, dev, True)
+    gemm_each = measure.gemm_each
     # the step time proper, without per-kernel events
     step_ms, wall_ms, _, _ = measure(layers, args.steps, args.warmup, dev, False)
     total_ops = sum(lin.ops for lin in layers)
@@ -847,7 +850,9 @@ def main():
                     "achieved": round(ach, 1), "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                     "frac": round(ach / PEAK_INT8_TOPS, 4),
                     "traffic": counter_traffic(args.workload),
-                    "ops_per_launch": lin.ops, "avg_launch_us": round(float(gemm_us[dom]), 2)}
+                    "ops_per_launch": lin.ops, "avg_launch_us": round(float(gemm_us[dom]), 2),
+                    "launch_us_p10_p50_p90": [round(float(v), 2) for v in
+                                              np.percentile(gemm_each[:, dom], [10, 50, 90])]}
         clk = None if args.no_clock else clock_under_load(lin, dev)
         if clk is not None:
             clk["peak_clock_mhz"] = PEAK_CLOCK_MHZ

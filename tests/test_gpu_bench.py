@@ -36,6 +36,8 @@ def test_bench_json_line(capsys, monkeypatch):
     assert r["ops_per_launch"] == 2 * 4608 * 4096 * 16384
     assert r["achieved"] == pytest.approx(r["ops_per_launch"] / r["avg_launch_us"] / 1e6, rel=1e-3)
     assert 0 < r["frac"] < 1
+    p10, p50, p90 = r["launch_us_p10_p50_p90"]
+    assert 0 < p10 <= p50 <= p90
     clk = r["clock"]
     if clk is not None:  # amdsmi present
         assert len(clk["mhz_per_xcd"]) == 8 and 100 < clk["mhz_mean"] <= 2400

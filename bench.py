@@ -480,6 +480,7 @@ def clock_under_load(lin: Linear, dev, seconds: float = 3.0):
         lin.quant(lin.xs[0], Xq, xsc)
         per = max(1, int(10e-3 / max(lin.ops / 2.5e15, 1e-6)))  # about 10 ms of launches
         samples = []
+        uclk = []
         t0 = time.perf_counter()
         last = 0.0
         while time.perf_counter() - t0 < seconds:
@@ -489,7 +490,11 @@ def clock_under_load(lin: Linear, dev, seconds: float = 3.0):
             now = time.perf_counter() - t0
             if now > 1.0 and now - last > 0.05:
                 last = now
-                clks = amdsmi.amdsmi_get_gpu_metrics_info(h).get("current_gfxclks")
+                met = amdsmi.amdsmi_get_gpu_metrics_info(h)
+                clks = met.get("current_gfxclks")
+                u = met.get("current_uclk")
+                if isinstance(u, (int, float)) and 0 < u < 100000:
+                    uclk.append(float(u))
                 if isinstance(clks, (list, tuple)):
                     clks = [int(c) for c in clks if isinstance(c, (int, float)) and 0 < c < 10000]
                     if clks:
@@ -503,7 +508,8 @@ def clock_under_load(lin: Linear, dev, seconds: float = 3.0):
                           f"{seconds:.0f} s of back-to-back launches of this kernel",
                 "mhz_per_xcd": [round(float(v)) for v in per_xcd],
                 "mhz_mean": round(float(per_xcd.mean()), 1),
-                "mhz_min": round(float(per_xcd.min()), 1), "samples": len(samples)}
+                "mhz_min": round(float(per_xcd.min()), 1), "samples": len(samples),
+                "memory_clock_mhz": round(float(np.mean(uclk)), 1) if uclk else None}
     except Exception:
         return None
     finally:

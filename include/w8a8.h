@@ -25,6 +25,11 @@
  *     the kernels surface at the caller's next synchronization.
  *   - Sizes: 1 <= M <= 2^22 rows (tokens; also N for the weight-side row
  *     kernels; fewer than 2^22 when K > 32768, W8A8_ERR_SHAPE otherwise);
+ *     an empty token batch, M = 0, is accepted by every entry point that
+ *     takes tokens except w8a8_act_moments (no statistics of no entries):
+ *     the other arguments are validated as usual, buffers sized by M may
+ *     then be NULL, W8A8_OK is returned and nothing is enqueued (q8_0_linear
+ *     and q4_k_linear then leave `work` untouched);
  *     GEMM outputs 1 <= N <= 2^20 and M * N <= 2^38;
  *     64 <= K <= 65536 with K % 64 == 0 (the int32 sum is then exact:
  *     127^2 * K < 2^31). Ragged M and N need no padding. Matrix pointers

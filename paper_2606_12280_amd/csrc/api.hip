@@ -63,6 +63,15 @@ w8a8_status check_rows(int64_t R, int64_t max_rows) {
     return (R < 1 || R > max_rows) ? W8A8_ERR_SHAPE : W8A8_OK;
 }
 
+// Token counts may be 0: an empty batch is validated like any other and
+// then enqueues nothing.
+w8a8_status check_tokens(int64_t M) {
+    return (M < 0 || M > kMaxRows) ? W8A8_ERR_SHAPE : W8A8_OK;
+}
+
+// A buffer sized by the token count may be NULL when that count is 0.
+bool missing(const void *p, int64_t M) { return p == nullptr && M > 0; }
+
 w8a8_status hip_status(hipError_t e) {
     if (e == hipSuccess) return W8A8_OK;
     snprintf(g_last_hip_error, sizeof g_last_hip_error, "%s", hipGetErrorName(e));
@@ -100,11 +109,12 @@ const char *w8a8_last_hip_error(void) { return g_last_hip_error; }
 
 w8a8_status w8a8_act_absmax(const uint16_t *X, int64_t M, int64_t K, float *absmax,
                             w8a8_stream stream) {
-    if (X == nullptr || absmax == nullptr) return W8A8_ERR_NULL;
-    W8A8_TRY(check_rows(M, kMaxRows));
+    if (missing(X, M) || absmax == nullptr) return W8A8_ERR_NULL;
+    W8A8_TRY(check_tokens(M));
     W8A8_TRY(check_k(K));
     if (!aligned(X, 16) || !aligned(absmax, 4)) return W8A8_ERR_ALIGN;
     W8A8_TRY(check_alias({{absmax, 4 * K}}, {{X, 2 * M * K}}));
+    if (M == 0) return W8A8_OK;  // the running maximum is unchanged
     return hip_status(w8a8::launch_col_absmax(X, M, K, absmax, as_stream(stream)));
 }
 
@@ -156,14 +166,15 @@ w8a8_status w8a8_prepare_weight(const uint16_t *W, const float *lambda, int64_t 
 
 w8a8_status w8a8_quant_act(const uint16_t *X, const float *inv_lambda, int64_t M, int64_t K,
                            int8_t *Xq, float *x_scale, w8a8_stream stream) {
-    if (X == nullptr || inv_lambda == nullptr || Xq == nullptr || x_scale == nullptr)
+    if (missing(X, M) || inv_lambda == nullptr || missing(Xq, M) || missing(x_scale, M))
         return W8A8_ERR_NULL;
-    W8A8_TRY(check_rows(M, kMaxRows));
+    W8A8_TRY(check_tokens(M));
     W8A8_TRY(check_k(K));
     W8A8_TRY(check_row_grid(M, K));
     if (!aligned(X, 16) || !aligned(Xq, 16) || !aligned(inv_lambda, 16) || !aligned(x_scale, 4))
         return W8A8_ERR_ALIGN;
     W8A8_TRY(check_alias({{Xq, M * K}, {x_scale, 4 * M}}, {{X, 2 * M * K}, {inv_lambda, 4 * K}}));
+    if (M == 0) return W8A8_OK;
     return hip_status(
         w8a8::launch_smooth_quant_rows(X, inv_lambda, M, K, Xq, x_scale, as_stream(stream)));
 }
@@ -171,10 +182,10 @@ w8a8_status w8a8_quant_act(const uint16_t *X, const float *inv_lambda, int64_t M
 w8a8_status w8a8_adaln_quant_act(const uint16_t *X, const uint16_t *shift, const uint16_t *scale,
                                  const float *inv_lambda, int64_t M, int64_t K, double eps,
                                  int8_t *Xq, float *x_scale, w8a8_stream stream) {
-    if (X == nullptr || shift == nullptr || scale == nullptr || inv_lambda == nullptr ||
-        Xq == nullptr || x_scale == nullptr)
+    if (missing(X, M) || shift == nullptr || scale == nullptr || inv_lambda == nullptr ||
+        missing(Xq, M) || missing(x_scale, M))
         return W8A8_ERR_NULL;
-    W8A8_TRY(check_rows(M, kMaxRows));
+    W8A8_TRY(check_tokens(M));
     W8A8_TRY(check_k(K));
     if (K > 8192 || !(eps >= 0.0) || !std::isfinite(eps)) return W8A8_ERR_UNSUPPORTED;
     if (!aligned(X, 16) || !aligned(shift, 16) || !aligned(scale, 16) || !aligned(Xq, 16) ||
@@ -182,6 +193,7 @@ w8a8_status w8a8_adaln_quant_act(const uint16_t *X, const uint16_t *shift, const
         return W8A8_ERR_ALIGN;
     W8A8_TRY(check_alias({{Xq, M * K}, {x_scale, 4 * M}},
                          {{X, 2 * M * K}, {shift, 2 * K}, {scale, 2 * K}, {inv_lambda, 4 * K}}));
+    if (M == 0) return W8A8_OK;
     return hip_status(w8a8::launch_adaln_quant_act(X, shift, scale, inv_lambda, M, K, eps, Xq,
                                                    x_scale, as_stream(stream)));
 }
@@ -189,10 +201,10 @@ w8a8_status w8a8_adaln_quant_act(const uint16_t *X, const uint16_t *shift, const
 w8a8_status w8a8_linear(const int8_t *Xq, const float *x_scale, const int8_t *Wq,
                         const float *w_scale, const uint16_t *bias, int64_t M, int64_t N,
                         int64_t K, uint16_t *Y, w8a8_stream stream) {
-    if (Xq == nullptr || x_scale == nullptr || Wq == nullptr || w_scale == nullptr ||
-        Y == nullptr)
+    if (missing(Xq, M) || missing(x_scale, M) || Wq == nullptr || w_scale == nullptr ||
+        missing(Y, M))
         return W8A8_ERR_NULL;
-    W8A8_TRY(check_rows(M, kMaxRows));
+    W8A8_TRY(check_tokens(M));
     W8A8_TRY(check_rows(N, kMaxN));
     if (M * N > kMaxMN) return W8A8_ERR_SHAPE;
     W8A8_TRY(check_k(K));
@@ -204,27 +216,29 @@ w8a8_status w8a8_linear(const int8_t *Xq, const float *x_scale, const int8_t *Wq
                                             {Wq, N * K},
                                             {w_scale, 4 * N},
                                             {bias, bias ? 2 * N : 0}}));
+    if (M == 0) return W8A8_OK;
     return hip_status(w8a8::launch_gemm_i8(Xq, Wq, x_scale, w_scale, bias, M, N, K, Y, nullptr,
                                            as_stream(stream)));
 }
 
 w8a8_status w8a8_gemm_i32(const int8_t *Xq, const int8_t *Wq, int64_t M, int64_t N, int64_t K,
                           int32_t *C, w8a8_stream stream) {
-    if (Xq == nullptr || Wq == nullptr || C == nullptr) return W8A8_ERR_NULL;
-    W8A8_TRY(check_rows(M, kMaxRows));
+    if (missing(Xq, M) || Wq == nullptr || missing(C, M)) return W8A8_ERR_NULL;
+    W8A8_TRY(check_tokens(M));
     W8A8_TRY(check_rows(N, kMaxN));
     if (M * N > kMaxMN) return W8A8_ERR_SHAPE;
     W8A8_TRY(check_k(K));
     if (!aligned(Xq, 16) || !aligned(Wq, 16) || !aligned(C, 16)) return W8A8_ERR_ALIGN;
     W8A8_TRY(check_alias({{C, 4 * M * N}}, {{Xq, M * K}, {Wq, N * K}}));
+    if (M == 0) return W8A8_OK;
     return hip_status(w8a8::launch_gemm_i8(Xq, Wq, nullptr, nullptr, nullptr, M, N, K, nullptr, C,
                                            as_stream(stream)));
 }
 
 w8a8_status bf16_linear(const uint16_t *X, const uint16_t *W, const uint16_t *bias, int64_t M,
                         int64_t N, int64_t K, uint16_t *Y, w8a8_stream stream) {
-    if (X == nullptr || W == nullptr || Y == nullptr) return W8A8_ERR_NULL;
-    W8A8_TRY(check_rows(M, kMaxRows));
+    if (missing(X, M) || W == nullptr || missing(Y, M)) return W8A8_ERR_NULL;
+    W8A8_TRY(check_tokens(M));
     W8A8_TRY(check_rows(N, kMaxN));
     if (M * N > kMaxMN) return W8A8_ERR_SHAPE;
     W8A8_TRY(check_k(K));
@@ -232,6 +246,7 @@ w8a8_status bf16_linear(const uint16_t *X, const uint16_t *W, const uint16_t *bi
         return W8A8_ERR_ALIGN;
     W8A8_TRY(check_alias({{Y, 2 * M * N}},
                          {{X, 2 * M * K}, {W, 2 * N * K}, {bias, bias ? 2 * N : 0}}));
+    if (M == 0) return W8A8_OK;
     return hip_status(w8a8::launch_gemm_bf16(X, W, bias, M, N, K, Y, as_stream(stream)));
 }
 
@@ -273,9 +288,9 @@ w8a8_status q8_0_dequantize(const int8_t *qs, const uint16_t *d, int64_t N, int6
 w8a8_status q8_0_linear(const uint16_t *X, const int8_t *qs, const uint16_t *d,
                         const uint16_t *bias, int64_t M, int64_t N, int64_t K, uint16_t *work,
                         uint16_t *Y, w8a8_stream stream) {
-    if (X == nullptr || qs == nullptr || d == nullptr || work == nullptr || Y == nullptr)
+    if (missing(X, M) || qs == nullptr || d == nullptr || work == nullptr || missing(Y, M))
         return W8A8_ERR_NULL;
-    W8A8_TRY(check_rows(M, kMaxRows));
+    W8A8_TRY(check_tokens(M));
     W8A8_TRY(check_rows(N, kMaxN));
     if (M * N > kMaxMN) return W8A8_ERR_SHAPE;
     W8A8_TRY(check_k(K));
@@ -285,6 +300,7 @@ w8a8_status q8_0_linear(const uint16_t *X, const int8_t *qs, const uint16_t *d,
     W8A8_TRY(check_alias({{work, 2 * N * K}, {Y, 2 * M * N}},
                          {{X, 2 * M * K}, {qs, N * K}, {d, N * (K / 32) * 2},
                           {bias, bias ? 2 * N : 0}}));
+    if (M == 0) return W8A8_OK;
     const hipStream_t s = as_stream(stream);
     W8A8_TRY(hip_status(w8a8::launch_q8_0_dequantize(qs, d, N, K, work, s)));
     return hip_status(w8a8::launch_gemm_bf16(X, work, bias, M, N, K, Y, s));
@@ -335,9 +351,9 @@ w8a8_status q4_k_linear(const uint16_t *X, const uint8_t *qs, const uint8_t *sc,
                         const uint8_t *mn, const uint16_t *d, const uint16_t *dmin,
                         const uint16_t *bias, int64_t M, int64_t N, int64_t K, uint16_t *work,
                         uint16_t *Y, w8a8_stream stream) {
-    if (X == nullptr || work == nullptr || Y == nullptr) return W8A8_ERR_NULL;
+    if (missing(X, M) || work == nullptr || missing(Y, M)) return W8A8_ERR_NULL;
     W8A8_TRY(check_q4_k_args(qs, sc, mn, d, dmin, N, K));
-    W8A8_TRY(check_rows(M, kMaxRows));
+    W8A8_TRY(check_tokens(M));
     W8A8_TRY(check_rows(N, kMaxN));
     if (M * N > kMaxMN) return W8A8_ERR_SHAPE;
     if (!aligned(X, 16) || !aligned(work, 16) || !aligned(Y, 16) || !aligned(bias, 2))
@@ -346,6 +362,7 @@ w8a8_status q4_k_linear(const uint16_t *X, const uint8_t *qs, const uint8_t *sc,
     W8A8_TRY(check_alias({{work, 2 * N * K}, {Y, 2 * M * N}},
                          {{X, 2 * M * K}, {qs, b.qs}, {sc, b.sub}, {mn, b.sub}, {d, b.super},
                           {dmin, b.super}, {bias, bias ? 2 * N : 0}}));
+    if (M == 0) return W8A8_OK;
     const hipStream_t s = as_stream(stream);
     W8A8_TRY(hip_status(w8a8::launch_q4_k_dequantize(qs, sc, mn, d, dmin, N, K, work, s)));
     return hip_status(w8a8::launch_gemm_bf16(X, work, bias, M, N, K, Y, s));

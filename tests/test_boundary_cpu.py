@@ -23,6 +23,8 @@ B = 0x7F0100000000
 C = 0x7F0200000000
 D = 0x7F0300000000
 E = 0x7F0400000000
+F = 0x7F0500000000
+G = 0x7F0600000000
 
 
 def declared_functions():
@@ -55,7 +57,7 @@ def test_version_and_status_strings(lib):
 def test_quant_act_validation(lib):
     f = lib.w8a8_quant_act
     assert f(None, B, 4, 64, C, D, None) == NULL
-    assert f(A, B, 0, 64, C, D, None) == SHAPE
+    assert f(A, B, -1, 64, C, D, None) == SHAPE
     assert f(A, B, (1 << 22) + 1, 64, C, D, None) == SHAPE
     assert f(A, B, 4, 0, C, D, None) == SHAPE
     assert f(A, B, 4, 100, C, D, None) == UNSUP
@@ -92,6 +94,34 @@ def test_linear_validation(lib):
     assert h(A, None, None, 4, 8, 64, C, None) == NULL
     assert h(A, B, None, 4, 8, 64, A, None) == ALIAS
     assert h(A, B, None, 4, 8, 0, C, None) == SHAPE
+
+
+def test_empty_token_batch_is_a_no_op(lib):
+    """M = 0 returns OK without touching the GPU (this process has none), with
+    NULL for every buffer sized by M; the other arguments are still checked,
+    and the moments of no entries stay an error."""
+    assert lib.w8a8_act_absmax(None, 0, 64, B, None) == OK
+    assert lib.w8a8_act_absmax(None, 0, 64, None, None) == NULL
+    assert lib.w8a8_act_absmax(None, 0, 96, B, None) == UNSUP
+    assert lib.w8a8_act_moments(A, 0, 64, B, C, None) == SHAPE
+    assert lib.w8a8_quant_act(None, B, 0, 64, None, None, None) == OK
+    assert lib.w8a8_quant_act(None, None, 0, 64, None, None, None) == NULL
+    assert lib.w8a8_quant_act(None, B + 4, 0, 64, None, None, None) == ALIGN
+    assert lib.w8a8_adaln_quant_act(None, B, C, D, 0, 64, 1e-6, None, None, None) == OK
+    assert lib.w8a8_adaln_quant_act(None, B, C, D, 0, 64, -1.0, None, None, None) == UNSUP
+    assert lib.w8a8_linear(None, None, C, D, None, 0, 8, 64, None, None) == OK
+    assert lib.w8a8_linear(None, None, None, D, None, 0, 8, 64, None, None) == NULL
+    assert lib.w8a8_linear(None, None, C, D, None, 0, 0, 64, None, None) == SHAPE
+    assert lib.w8a8_linear(None, None, C, D, None, 0, 8, 96, None, None) == UNSUP
+    assert lib.w8a8_linear(None, None, C, D, E, 0, 8, 64, None, None) == OK
+    assert lib.w8a8_gemm_i32(None, B, 0, 8, 64, None, None) == OK
+    assert lib.bf16_linear(None, B, None, 0, 8, 64, None, None) == OK
+    assert lib.bf16_linear(None, B, None, 0, 8, 0, None, None) == SHAPE
+    assert lib.q8_0_linear(None, B, C, None, 0, 8, 64, D, None, None) == OK
+    assert lib.q8_0_linear(None, B, C, None, 0, 8, 64, None, None, None) == NULL
+    assert lib.q4_k_linear(None, B, C, D, E, F, None, 0, 8, 256, G, None, None) == OK
+    assert lib.q4_k_linear(None, B, C, D, E, F, None, 0, 8, 128, G, None, None) == UNSUP
+    assert lib.w8a8_gemm_config(0, 8, 64, 0, None, None, None) == NULL
 
 
 def test_gemm_config_picks_tiles_by_rounds(lib):
@@ -183,8 +213,6 @@ def test_q8_0_validation(lib):
 
 
 def test_q4_k_validation(lib):
-    F = 0x7F0500000000
-    G = 0x7F0600000000
     q = lib.q4_k_quantize
     assert q(None, 8, 256, B, C, D, E, F, None) == NULL
     assert q(A, 8, 256, B, C, D, E, None, None) == NULL
@@ -208,14 +236,14 @@ def test_q4_k_validation(lib):
     assert f(A, B, C, D, E, F, None, 4, 8, 256, G, G, None) == ALIAS     # Y inside work
     assert f(A, B, C, D, E, F, None, 4, 8, 256, B, G, None) == ALIAS     # work over the codes
     assert f(A, B, C, D, E, F, None, 4, 8, 512 + 64, G, 0x7F0700000000, None) == UNSUP
-    assert f(A, B, C, D, E, F, None, 0, 8, 256, G, 0x7F0700000000, None) == SHAPE
+    assert f(A, B, C, D, E, F, None, -1, 8, 256, G, 0x7F0700000000, None) == SHAPE
 
 
 def test_adaln_validation(lib):
     f = lib.w8a8_adaln_quant_act
     assert f(None, B, C, D, 4, 64, 1e-6, E, E + 4096, None) == NULL
     assert f(A, B, None, D, 4, 64, 1e-6, E, E + 4096, None) == NULL
-    assert f(A, B, C, D, 0, 64, 1e-6, E, E + 4096, None) == SHAPE
+    assert f(A, B, C, D, -1, 64, 1e-6, E, E + 4096, None) == SHAPE
     assert f(A, B, C, D, 4, 96, 1e-6, E, E + 4096, None) == UNSUP          # K % 64 != 0
     assert f(A, B, C, D, 4, 8256, 1e-6, E, E + 65536, None) == UNSUP       # K > 8192
     assert f(A, B, C, D, 4, 64, -1e-6, E, E + 4096, None) == UNSUP

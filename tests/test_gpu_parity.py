@@ -735,6 +735,45 @@ def test_router_runs_gguf_layers_like_the_entry_points():
     assert np.array_equal(y4, host_bits(ops.q4_k_linear(X, l4.q4k, b)))
 
 
+def test_empty_token_batch():
+    """M = 0 (an empty batch, as a view with a live pointer and as a fresh
+    tensor with a NULL one) through every entry point that takes tokens and
+    through the router: [0, N] outputs, the running absmax unchanged, and the
+    next full call bit-identical to the same call made before."""
+    from paper_2606_12280_amd import layer
+    M, N, K = 64, 320, 512
+    c = synth.linear_case([197, M, N, K], M, N, K)
+    X, W, b = dev_bf16(c["X"].reshape(M, K)), dev_bf16(c["W"].reshape(N, K)), dev_bf16(c["bias"])
+    s = torch.zeros(K, dtype=torch.float32, device=DEV)
+    ops.w8a8_act_absmax(X, s)
+    lam = ops.w8a8_smooth_factors(s, W, 0.5)
+    lays = [layer.prepare_linear(W, b, lam, protected=False),
+            layer.prepare_linear(W, b, None, protected=True),
+            layer.prepare_q8_0(W, b), layer.prepare_q4_k(W, b)]
+    ws = layer.Workspace(DEV)
+    before = [host_bits(layer.route(lay, X, ws=ws)) for lay in lays]
+    shift = dev_bf16(synth.rand_bf16([198, 0], (K,), 0.05))
+    scale = dev_bf16(synth.rand_bf16([198, 1], (K,), 0.1))
+    ada_before = [host(t) for t in ops.w8a8_adaln_quant_act(X, shift, scale, lays[0].inv_lambda)]
+    s_before = host(s)
+    for X0 in (X[:0], torch.empty((0, K), dtype=torch.bfloat16, device=DEV)):
+        ops.w8a8_act_absmax(X0, s)
+        Xq0, xs0 = ops.w8a8_quant_act(X0, lays[0].inv_lambda)
+        assert tuple(Xq0.shape) == (0, K) and tuple(xs0.shape) == (0,)
+        assert tuple(ops.w8a8_linear(Xq0, xs0, lays[0].Wq, lays[0].w_scale, b).shape) == (0, N)
+        assert tuple(ops.w8a8_gemm_i32(Xq0, lays[0].Wq).shape) == (0, N)
+        assert tuple(ops.w8a8_adaln_quant_act(X0, shift, scale, lays[0].inv_lambda)[0].shape) == (0, K)
+        for lay in lays:
+            assert tuple(layer.route(lay, X0, ws=ws).shape) == (0, N)
+            assert tuple(layer.route(lay, X0).shape) == (0, N)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(s), s_before)
+    for lay, y in zip(lays, before):
+        assert np.array_equal(host_bits(layer.route(lay, X, ws=ws)), y)
+    ada_after = [host(t) for t in ops.w8a8_adaln_quant_act(X, shift, scale, lays[0].inv_lambda)]
+    assert all(np.array_equal(a, b_) for a, b_ in zip(ada_after, ada_before))
+
+
 # --------------------------------------------------------------------------
 # A seeded sweep of shapes: every tile configuration the dispatcher can pick
 # (by round fill and by K % 128), ragged M and N, K from 64 to 4160 bytes.

@@ -78,8 +78,8 @@ const char *w8a8_status_string(int status);
 const char *w8a8_last_hip_error(void);
 
 /* ---------------------------------------------------------------------- */
-/* Calibration (Section 3: per-channel activation scales come from a      */
-/* profiling pass; the smoothing equation).                               */
+/* Calibration (Section 3, "INT8 W8A8": the per-channel activation scales */
+/* are measured beforehand on calibration inputs; the smoothing equation).*/
 /* ---------------------------------------------------------------------- */
 
 /* Per-input-channel activation absmax, accumulated:

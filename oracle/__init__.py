@@ -111,8 +111,9 @@ def double_to_bf16(d: float) -> int:
 
 
 def act_absmax(X, M: int, K: int, s=None) -> np.ndarray:
-    """Calibration statistic s_j = max_t |X_tj| (Section 3, activation scales
-    from a profiling pass), accumulated into ``s`` if given."""
+    """Calibration statistic s_j = max_t |X_tj| (Section 3, "INT8 W8A8": the
+    activation scales are measured beforehand on calibration inputs),
+    accumulated into ``s`` if given."""
     X = _c(X, np.uint16)
     out = np.zeros(K, np.float32) if s is None else np.array(s, np.float32, copy=True)
     _load().oracle_act_absmax(_p(X), M, K, _p(out))

@@ -133,8 +133,9 @@ float oracle_bf16_to_float(uint16_t h) { return bf16_to_float(h); }
 uint16_t oracle_double_to_bf16(double d) { return double_to_bf16(d); }
 
 /* ------------------------------------------------------------------ */
-/* Calibration (Section 3: "activation scales come from a profiling     */
-/* pass"): per-input-channel absmax over tokens, and lambda.            */
+/* Calibration (Section 3, "INT8 W8A8": the per-channel activation      */
+/* scales are measured beforehand over calibration inputs): the         */
+/* per-input-channel absmax over tokens, and lambda.                    */
 /* ------------------------------------------------------------------ */
 
 /* s[k] = max(s[k], max_t |X[t][k]|). X is [M][K] bf16. The caller seeds s

@@ -43,6 +43,15 @@ def _need(t: torch.Tensor, name: str, dtype: torch.dtype, ndim: int, device=None
     return t
 
 
+def _need_vec(t: torch.Tensor, name: str, dtype: torch.dtype, n: int, device=None) -> torch.Tensor:
+    """A 1-D operand of exactly n entries: the C ABI takes no lengths, so a
+    shorter vector would be read past its end."""
+    _need(t, name, dtype, 1, device)
+    if t.numel() != n:
+        raise ValueError(f"{name} must have {n} entries, got {t.numel()}")
+    return t
+
+
 def _out(t, shape, dtype, device, name):
     if t is None:
         return torch.empty(shape, dtype=dtype, device=device)
@@ -56,9 +65,7 @@ def w8a8_act_absmax(X: torch.Tensor, absmax: torch.Tensor) -> torch.Tensor:
     """absmax[k] = max(absmax[k], max_t |X[t, k]|), in place (calibration)."""
     _need(X, "X", torch.bfloat16, 2)
     M, K = X.shape
-    _need(absmax, "absmax", torch.float32, 1, X.device)
-    if absmax.numel() != K:
-        raise ValueError("absmax must have K entries")
+    _need_vec(absmax, "absmax", torch.float32, K, X.device)
     lib = load()
     with torch.cuda.device(X.device):
         check("w8a8_act_absmax",
@@ -91,7 +98,7 @@ def w8a8_smooth_factors(act_absmax: torch.Tensor, W: torch.Tensor, alpha: float 
     """lambda_j = s_j^alpha / max_i |W_ij|^(1 - alpha) -> fp32 [K]."""
     _need(W, "W", torch.bfloat16, 2)
     N, K = W.shape
-    _need(act_absmax, "act_absmax", torch.float32, 1, W.device)
+    _need_vec(act_absmax, "act_absmax", torch.float32, K, W.device)
     lam = _out(out, (K,), torch.float32, W.device, "out")
     lib = load()
     with torch.cuda.device(W.device):
@@ -106,7 +113,7 @@ def w8a8_prepare_weight(W: torch.Tensor, lam: torch.Tensor, Wq=None, w_scale=Non
     """Offline weight side -> (Wq int8 [N, K], w_scale fp32 [N], inv_lambda fp32 [K])."""
     _need(W, "W", torch.bfloat16, 2)
     N, K = W.shape
-    _need(lam, "lambda", torch.float32, 1, W.device)
+    _need_vec(lam, "lambda", torch.float32, K, W.device)
     dev = W.device
     Wq = _out(Wq, (N, K), torch.int8, dev, "Wq")
     w_scale = _out(w_scale, (N,), torch.float32, dev, "w_scale")
@@ -123,7 +130,7 @@ def w8a8_quant_act(X: torch.Tensor, inv_lambda: torch.Tensor, Xq=None, x_scale=N
     """Smooth + per-token quantize -> (Xq int8 [M, K], x_scale fp32 [M])."""
     _need(X, "X", torch.bfloat16, 2)
     M, K = X.shape
-    _need(inv_lambda, "inv_lambda", torch.float32, 1, X.device)
+    _need_vec(inv_lambda, "inv_lambda", torch.float32, K, X.device)
     dev = X.device
     Xq = _out(Xq, (M, K), torch.int8, dev, "Xq")
     x_scale = _out(x_scale, (M,), torch.float32, dev, "x_scale")
@@ -143,8 +150,8 @@ def w8a8_adaln_quant_act(X: torch.Tensor, shift: torch.Tensor, scale: torch.Tens
     M, K = X.shape
     dev = X.device
     for name, t in (("shift", shift), ("scale", scale)):
-        _need(t, name, torch.bfloat16, 1, dev)
-    _need(inv_lambda, "inv_lambda", torch.float32, 1, dev)
+        _need_vec(t, name, torch.bfloat16, K, dev)
+    _need_vec(inv_lambda, "inv_lambda", torch.float32, K, dev)
     Xq = _out(Xq, (M, K), torch.int8, dev, "Xq")
     x_scale = _out(x_scale, (M,), torch.float32, dev, "x_scale")
     lib = load()
@@ -165,10 +172,10 @@ def w8a8_linear(Xq: torch.Tensor, x_scale: torch.Tensor, Wq: torch.Tensor,
     N = Wq.shape[0]
     if Wq.shape[1] != K:
         raise ValueError("Xq and Wq must share K")
-    _need(x_scale, "x_scale", torch.float32, 1, Xq.device)
-    _need(w_scale, "w_scale", torch.float32, 1, Xq.device)
+    _need_vec(x_scale, "x_scale", torch.float32, M, Xq.device)
+    _need_vec(w_scale, "w_scale", torch.float32, N, Xq.device)
     if bias is not None:
-        _need(bias, "bias", torch.bfloat16, 1, Xq.device)
+        _need_vec(bias, "bias", torch.bfloat16, N, Xq.device)
     Y = _out(out, (M, N), torch.bfloat16, Xq.device, "out")
     lib = load()
     with torch.cuda.device(Xq.device):
@@ -204,7 +211,7 @@ def bf16_linear(X: torch.Tensor, W: torch.Tensor, bias: torch.Tensor | None = No
     if W.shape[1] != K:
         raise ValueError("X and W must share K")
     if bias is not None:
-        _need(bias, "bias", torch.bfloat16, 1, X.device)
+        _need_vec(bias, "bias", torch.bfloat16, N, X.device)
     Y = _out(out, (M, N), torch.bfloat16, X.device, "out")
     lib = load()
     with torch.cuda.device(X.device):
@@ -273,7 +280,7 @@ def q8_0_linear(X: torch.Tensor, qs: torch.Tensor, d: torch.Tensor,
     if tuple(d.shape) != (N, K // Q8_0_BLOCK):
         raise ValueError("d must be [N, K/32]")
     if bias is not None:
-        _need(bias, "bias", torch.bfloat16, 1, X.device)
+        _need_vec(bias, "bias", torch.bfloat16, N, X.device)
     work = _out(work, (N, K), torch.bfloat16, X.device, "work")
     Y = _out(out, (M, N), torch.bfloat16, X.device, "out")
     lib = load()
@@ -363,7 +370,7 @@ def q4_k_linear(X: torch.Tensor, q: Q4K, bias: torch.Tensor | None = None,
     if Kq != K:
         raise ValueError(f"the weights are [{N}, {Kq}], X has K = {K}")
     if bias is not None:
-        _need(bias, "bias", torch.bfloat16, 1, X.device)
+        _need_vec(bias, "bias", torch.bfloat16, N, X.device)
     work = _out(work, (N, K), torch.bfloat16, X.device, "work")
     Y = _out(out, (M, N), torch.bfloat16, X.device, "out")
     lib = load()

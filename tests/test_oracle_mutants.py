@@ -78,6 +78,14 @@ MUTANTS = {
                                   "const double m = n * (1.0 + (double)bf16_to_float(shift[k]));\n            H[t * K + k] = double_to_bf16(m + (double)bf16_to_float(scale[k]));"),
     "adaln_uncentered_variance": ("const double c = (double)bf16_to_float(x[k]) - mean;", "const double c = (double)bf16_to_float(x[k]);"),
     "adaln_not_centered": ("const double n = ((double)bf16_to_float(x[k]) - mean) * rstd;", "const double n = (double)bf16_to_float(x[k]) * rstd;"),
+    "linear_drops_last_k": ("for (k = 0; k < K; ++k)\n                acc += (int32_t)Xq[t * K + k] * (int32_t)Wq[n * K + k];\n            y = (double)acc",
+                            "for (k = 0; k + 1 < K; ++k)\n                acc += (int32_t)Xq[t * K + k] * (int32_t)Wq[n * K + k];\n            y = (double)acc"),
+    "linear_drops_bias": ("double b = bias ? (double)bf16_to_float(bias[n]) : 0.0;\n            double y;",
+                          "double b = 0.0;\n            double y;"),
+    "linear_scale_index": ("y = (double)acc * ((double)x_scale[t] * (double)w_scale[n]) + b;",
+                           "y = (double)acc * ((double)x_scale[t] * (double)w_scale[t]) + b;"),
+    "linear_transposed_weight": ("acc += (int32_t)Xq[t * K + k] * (int32_t)Wq[n * K + k];\n            y = (double)acc",
+                                 "acc += (int32_t)Xq[t * K + k] * (int32_t)Wq[k * N + n];\n            y = (double)acc"),
     "moments_drops_last_row": ("    for (t = 0; t < M; ++t) {\n        s2 += r2[t];",
                                "    for (t = 0; t + 1 < M; ++t) {\n        s2 += r2[t];"),
 }
@@ -99,6 +107,7 @@ PINS = [
     pins.test_lossless_grid_reduces_to_plain_product,
     lambda: pins.test_w8a8_error_bound_vs_fp64("tiny"),
     pins.test_epilogue_against_exact_rationals,
+    pins.test_w8a8_linear_against_int64_and_exact_rationals,
     pins.test_bf16_linear_small_integers_exact,
     pins.test_bf16_linear_random_vs_numpy_fp64,
     pins.test_act_moments_against_exact_rationals,

@@ -268,6 +268,13 @@ def test_lossless_grid_reduces_to_plain_product():
     assert np.array_equal(r["Y"], want)
     assert np.array_equal(r["acc"].astype(np.float64) * r["x_scale"][:, None]
                           * r["w_scale"][None, :], X @ W.T)
+    # the fused per-row routine (the one the CPU baseline times) on the same
+    # lossless grid, with and without the bias
+    Yf = oracle.w8a8_linear(r["Xq"], r["x_scale"], r["Wq"], r["w_scale"], bb, M, N, K)
+    assert np.array_equal(Yf, want)
+    Y0 = oracle.w8a8_linear(r["Xq"], r["x_scale"], r["Wq"], r["w_scale"], None, M, N, K)
+    want0 = np.array([[round_bf16_exact(float(v)) for v in row] for row in X @ W.T], np.uint16)
+    assert np.array_equal(Y0, want0)
 
 
 @pytest.mark.parametrize("which", ["tiny", "gelu_small"])
@@ -319,6 +326,32 @@ def test_epilogue_against_exact_rationals():
     Y0 = oracle.epilogue(C, xs, ws, None, M, N)
     assert Y0[2, 3] == round_bf16_exact(Fraction(int(C[2, 3])) * Fraction(float(xs[2]))
                                         * Fraction(float(ws[3])))
+
+
+def test_w8a8_linear_against_int64_and_exact_rationals():
+    """The fused routine (int32 sum and epilogue per row, what the CPU
+    baseline times) against an int64 NumPy product and exact rational
+    epilogue arithmetic, on a ragged shape with codes reaching +-127 (catches
+    a dropped last k, a dropped bias, a wrong scale index or a transposed
+    operand)."""
+    rng = np.random.default_rng(31)
+    M, N, K = 7, 33, 320
+    Xq = rng.integers(-127, 128, (M, K)).astype(np.int8)
+    Wq = rng.integers(-127, 128, (N, K)).astype(np.int8)
+    Xq[:, -1] = 127                      # the last k carries weight in every sum
+    Wq[:, -1] = -127
+    C = Xq.astype(np.int64) @ Wq.astype(np.int64).T
+    xs = rng.uniform(1e-4, 1e-1, M).astype(np.float32)
+    ws = rng.uniform(1e-5, 1e-2, N).astype(np.float32)
+    b = synth.rand_bf16(10, (N,), 5.0)
+    bf = bf16_to_f64(b)
+    Y = oracle.w8a8_linear(Xq, xs, Wq, ws, b, M, N, K)
+    Y0 = oracle.w8a8_linear(Xq, xs, Wq, ws, None, M, N, K)
+    for t in range(M):
+        for n in range(N):
+            p = Fraction(int(C[t, n])) * Fraction(float(xs[t])) * Fraction(float(ws[n]))
+            assert Y[t, n] == round_bf16_exact(p + Fraction(float(bf[n]))), (t, n)
+            assert Y0[t, n] == round_bf16_exact(p), (t, n)
 
 
 def test_bf16_linear_small_integers_exact():

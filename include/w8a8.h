@@ -107,6 +107,35 @@ w8a8_status w8a8_act_absmax(const uint16_t *X, int64_t M, int64_t K,
 w8a8_status w8a8_act_moments(const uint16_t *X, int64_t M, int64_t K, void *work,
                              double *stats, w8a8_stream stream);
 
+/* Protection choice (Section 3, "Activation-fragility profiling and
+ * protection": the layers whose inputs are most fragile stay in bf16, N = 17
+ * of 211 per branch, and the ranking is checked for stability between the
+ * early and late halves of the trajectory). The paper gives no formula for
+ * the score; a layer's score here is its input kurtosis averaged over the
+ * profiled steps. These three are HOST functions: every pointer is host
+ * memory, nothing is launched and no GPU is needed. Inputs must be finite,
+ * else W8A8_ERR_UNSUPPORTED; at most 2^20 layers and 2^20 steps.
+ *
+ * Scores: kurtosis [layers][steps] binary64 (row-major, e.g. stats[3] of
+ * w8a8_act_moments per layer and step) -> scores [layers], the sum over
+ * steps step_begin <= s < step_end in step order divided by the number of
+ * those steps (0 <= step_begin < step_end <= steps). */
+w8a8_status w8a8_fragility_scores(const double *kurtosis, int64_t layers,
+                                  int64_t steps, int64_t step_begin,
+                                  int64_t step_end, double *scores);
+
+/* The n most fragile layers: indices [n] of the n highest of scores
+ * [layers], highest first, equal scores in increasing layer index
+ * (0 <= n <= layers; indices may be NULL when n == 0). */
+w8a8_status w8a8_select_protected(const double *scores, int64_t layers,
+                                  int64_t n, int32_t *indices);
+
+/* Spearman rank correlation of a [n] and b [n] (n >= 2): the Pearson
+ * correlation of their 1-based ranks, equal values sharing the mean of their
+ * positions. A constant vector has no ranking: W8A8_ERR_UNSUPPORTED. */
+w8a8_status w8a8_rank_correlation(const double *a, const double *b, int64_t n,
+                                  double *rho);
+
 /* SmoothQuant factors (Section 3, the smoothing equation):
  *   lambda[j] = act_absmax[j]^alpha / (max_i |W[i][j]|)^(1 - alpha),
  * computed in binary64 (sqrt(s)/sqrt(m) when alpha == 0.5, else

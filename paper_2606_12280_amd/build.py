@@ -12,7 +12,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libw8a8.so")
-SOURCES = ["api.hip", "quant.hip", "gemm.hip", "stats.hip", "q8_0.hip", "q4_k.hip", "adaln.hip"]
+SOURCES = ["api.hip", "quant.hip", "gemm.hip", "stats.hip", "q8_0.hip", "q4_k.hip", "adaln.hip",
+           "protect.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

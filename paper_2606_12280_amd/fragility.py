@@ -7,17 +7,32 @@ highest-scoring layers are kept in bf16 (no activation quantization), the
 rest run W8A8. The ranking's stability over the trajectory is checked with
 the Spearman rank correlation of scores from early and late steps.
 
-Selection and ranking are host logic over a few hundred numbers.
+Argument marshalling only: the scores, the selection and the rank
+correlation are the library's host calls w8a8_fragility_scores,
+w8a8_select_protected and w8a8_rank_correlation (include/w8a8.h).
 """
 from __future__ import annotations
+
+import ctypes
 
 import numpy as np
 import torch
 
 from . import ops
-from ._lib import MOMENTS_WORK_BYTES
+from ._lib import MOMENTS_WORK_BYTES, check, load
 
 MAX_ABS, MEAN, STD, KURTOSIS = range(4)
+
+
+def _host_f64(a, name: str, ndim: int) -> np.ndarray:
+    v = np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+    if v.ndim != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions, got shape {v.shape}")
+    return v
+
+
+def _dp(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
 
 
 class Profile:
@@ -37,41 +52,43 @@ class Profile:
         return self.stats.cpu().numpy()
 
     def scores(self, steps: slice = slice(None)) -> np.ndarray:
-        """Fragility score per layer over the given steps."""
-        return fragility_scores(self.table()[:, steps, KURTOSIS])
+        """Fragility score per layer over a contiguous range of steps."""
+        n_steps = self.stats.shape[1]
+        begin, end, stride = steps.indices(n_steps)
+        if stride != 1:
+            raise ValueError("steps must be a contiguous range")
+        return fragility_scores(self.table()[:, :, KURTOSIS], begin, end)
 
 
-def fragility_scores(kurtosis) -> np.ndarray:
-    """Mean kurtosis over steps; kurtosis is [layers, steps]."""
-    k = np.asarray(kurtosis, dtype=np.float64)
-    return k.mean(axis=1)
+def fragility_scores(kurtosis, step_begin: int = 0, step_end: int | None = None) -> np.ndarray:
+    """Mean kurtosis over steps [step_begin, step_end) of kurtosis [layers, steps]."""
+    k = _host_f64(kurtosis, "kurtosis", 2)
+    layers, steps = k.shape
+    end = steps if step_end is None else step_end
+    out = np.empty(layers, dtype=np.float64)
+    check("w8a8_fragility_scores",
+          load().w8a8_fragility_scores(_dp(k), layers, steps, step_begin, end, _dp(out)))
+    return out
 
 
 def select_protected(scores, n: int) -> list[int]:
     """The n most fragile layers, most fragile first (equal scores: lower
-    layer index first)."""
-    s = np.asarray(scores, dtype=np.float64)
-    order = np.lexsort((np.arange(s.size), -s))
-    return [int(i) for i in order[: max(0, n)]]
-
-
-def _average_ranks(v: np.ndarray) -> np.ndarray:
-    order = np.argsort(v, kind="stable")
-    ranks = np.empty(v.size, dtype=np.float64)
-    sv = v[order]
-    start = 0
-    for end in range(1, v.size + 1):
-        if end == v.size or sv[end] != sv[start]:
-            ranks[order[start:end]] = 0.5 * (start + end - 1) + 1.0
-            start = end
-    return ranks
+    layer index first); all of them when n exceeds the layer count."""
+    s = _host_f64(scores, "scores", 1)
+    n = max(0, min(int(n), s.size))
+    idx = np.empty(max(n, 1), dtype=np.int32)
+    check("w8a8_select_protected", load().w8a8_select_protected(_dp(s), s.size, n, _dp(idx)))
+    return [int(i) for i in idx[:n]]
 
 
 def rank_stability(scores_a, scores_b) -> float:
     """Spearman rank correlation between two score vectors (average ranks
     for ties)."""
-    ra = _average_ranks(np.asarray(scores_a, dtype=np.float64))
-    rb = _average_ranks(np.asarray(scores_b, dtype=np.float64))
-    ra -= ra.mean()
-    rb -= rb.mean()
-    return float((ra * rb).sum() / np.sqrt((ra * ra).sum() * (rb * rb).sum()))
+    a = _host_f64(scores_a, "scores_a", 1)
+    b = _host_f64(scores_b, "scores_b", 1)
+    if a.size != b.size:
+        raise ValueError("the two score vectors must have the same length")
+    rho = ctypes.c_double()
+    check("w8a8_rank_correlation",
+          load().w8a8_rank_correlation(_dp(a), _dp(b), a.size, ctypes.byref(rho)))
+    return rho.value

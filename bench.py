@@ -546,56 +546,124 @@ def dequant_bytes(fmt: str, N: int, K: int) -> int:
 # CPU oracle baseline
 # --------------------------------------------------------------------------
 
+class _OracleLinear:
+    """The oracle on the first `rows` token rows of one seeded linear: for a
+    W8A8 layer smoothing + per-token quant + int32 GEMM + bf16 epilogue
+    (weights prepared outside the timing), for a protected layer the bf16
+    linear with binary64 sums."""
+
+    def __init__(self, c, protected: bool):
+        import oracle
+
+        self.o = oracle
+        self.c, self.protected = c, protected
+        self.M, self.N, self.K = c["M"], c["N"], c["K"]
+        self.X = c["X"].reshape(self.M, self.K)
+        if not protected:
+            lam = oracle.smooth_factors(oracle.act_absmax(c["X"], self.M, self.K), c["W"],
+                                        self.N, self.K, 0.5)
+            self.Wq, self.ws, self.il = oracle.prepare_weight(c["W"], lam, self.N, self.K)
+        self.tq = 0.0   # quant-step seconds of the last run
+
+    def run(self, rows: int) -> float:
+        o, N, K = self.o, self.N, self.K
+        t = time.perf_counter()
+        if self.protected:
+            o.bf16_linear(self.X[:rows], self.c["W"], self.c["bias"], rows, N, K)
+            self.tq = 0.0
+            return time.perf_counter() - t
+        Xq, xs = o.quant_act(self.X[:rows], self.il, rows, K)
+        t1 = time.perf_counter()
+        Y = o.w8a8_linear(Xq, xs, self.Wq, self.ws, self.c["bias"], rows, N, K)
+        dt = time.perf_counter() - t
+        self.tq = t1 - t
+        # the timed routine against the oracle's unfused int32 GEMM +
+        # epilogue on its first and last row (guards the timed work itself)
+        for r in (0, rows - 1):
+            acc = o.gemm_i32(Xq[r:r + 1], self.Wq, 1, N, K)
+            if not np.array_equal(o.epilogue(acc, xs[r:r + 1], self.ws, self.c["bias"], 1, N),
+                                  Y[r:r + 1]):
+                raise SystemExit(f"oracle w8a8_linear disagrees with gemm_i32 + epilogue, row {r}")
+        return dt
+
+    def rows_for(self, seconds: float) -> tuple[int, float]:
+        """Rows whose run takes about `seconds` (a 16-row probe, then once
+        more from a mid-sized run, which a small probe overstates on many
+        cores), and the measured time of that run."""
+        rows, dt = 16, self.run(16)
+        for _ in range(2):
+            if rows >= self.M or dt >= 0.8 * seconds:
+                break
+            rows = int(min(self.M, max(16, rows * seconds / max(dt, 1e-6))))
+            rows = max(16, rows // 16 * 16)
+            dt = self.run(rows)
+        return rows, dt
+
+
 def cpu_baseline(workload: str, target_s: float = 10.0):
-    """The oracle (quant + int32 GEMM + epilogue) on a bounded sample of
-    token rows of the workload's first W8A8 linear, on this host's cores."""
+    """The CPU oracle timed on a bounded sample of the workload on this
+    host's cores (OpenMP over token rows).
+
+    ffn_up / ffn_down: the W8A8 linear on as many token rows as take about
+    target_s (the whole linear up to three times when it is faster).
+    dit_block / backbone: each distinct linear shape (W8A8 or protected) on
+    a row sample of about target_s / shapes, extrapolated to the workload as
+    the sum over shapes of (time per row x M x number of such linears)."""
     import oracle
 
     oracle.build()
-    if workload == "ffn_down":
-        c = synth.ffn_down_case()
+    if workload in ("ffn_up", "ffn_down"):
+        c = synth.ffn_down_case() if workload == "ffn_down" else synth.ffn_up_case()
+        lin = _OracleLinear(c, False)
+        M, N, K = lin.M, lin.N, lin.K
+        rows, dt = lin.rows_for(target_s)
+        reps, q = 1, lin.tq
+        while rows >= M and dt < target_s and reps < 3:
+            dt += lin.run(rows)
+            q += lin.tq
+            reps += 1
+        tops = 2.0 * rows * N * K * reps / dt / 1e12
+        what = f"{rows} of {M} token rows" if reps == 1 else f"{reps} runs of all {M} token rows"
+        return {"value": round(tops, 6), "unit": "TOPS", "cores": oracle.num_threads(),
+                "kind": "oracle",
+                "quant_GB_s": round((3 * rows * K + 4 * rows) * reps / q / 1e9, 3),
+                "gemm_epilogue_TOPS": round(2.0 * rows * N * K * reps / (dt - q) / 1e12, 6),
+                "sample": f"{what} of the {M}x{K}->{N} linear: smoothing + per-token quant + "
+                          f"int32 GEMM + bf16 epilogue (weights prepared outside the timing), "
+                          f"{dt:.1f} s"}
+    if workload == "dit_block":
+        # the four linears of a block, counted once per CFG branch (the two
+        # branches' linears differ only in their seeded weights)
+        shapes = [(synth.block_case(0, li), synth.BLOCK_SHAPES[li][0] == "ffn_down", 2)
+                  for li in range(4)]
+        label = "one DiT block, both CFG branches"
+    elif workload == "backbone":
+        flags = L.protected_layers(211, 17)
+        counts = {}
+        for i in range(211):
+            key = (i % 4, flags[i])
+            counts[key] = counts.get(key, 0) + 2          # both branches
+        shapes = [(synth.block_case(0, li), prot, n) for (li, prot), n in sorted(counts.items())]
+        label = "211 linears x 2 branches"
     else:
-        c = synth.ffn_up_case()
-    M, N, K = c["M"], c["N"], c["K"]
-    lam = oracle.smooth_factors(oracle.act_absmax(c["X"], M, K), c["W"], N, K, 0.5)
-    Wq, ws, il = oracle.prepare_weight(c["W"], lam, N, K)   # offline, not timed
-    X = c["X"].reshape(M, K)
-
-    tq = [0.0]   # time in the quant step, summed over the timed runs
-
-    def run(rows):
-        t = time.perf_counter()
-        Xq, xs = oracle.quant_act(X[:rows], il, rows, K)
-        t1 = time.perf_counter()
-        oracle.w8a8_linear(Xq, xs, Wq, ws, c["bias"], rows, N, K)
-        tq[0] = t1 - t
-        return time.perf_counter() - t
-
-    # Size the sample from a small probe, then once more from a mid-sized
-    # run (a 16-row probe overstates the per-row time on many cores); if the
-    # whole linear takes less than target_s, time it repeatedly (at most 3x).
-    rows, dt = 16, run(16)
-    for _ in range(2):
-        if rows >= M or dt >= 0.8 * target_s:
-            break
-        rows = int(min(M, max(16, rows * target_s / max(dt, 1e-6))))
-        rows = max(16, rows // 16 * 16)
-        dt = run(rows)
-    reps = 1
-    q = tq[0]
-    while rows >= M and dt < target_s and reps < 3:
-        dt += run(rows)
-        q += tq[0]
-        reps += 1
-    tops = 2.0 * rows * N * K * reps / dt / 1e12
-    what = f"{rows} of {M} token rows" if reps == 1 else f"{reps} runs of all {M} token rows"
-    return {"value": round(tops, 6), "unit": "TOPS", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "quant_GB_s": round((3 * rows * K + 4 * rows) * reps / q / 1e9, 3),
-            "gemm_epilogue_TOPS": round(2.0 * rows * N * K * reps / (dt - q) / 1e12, 6),
-            "sample": f"{what} of the {M}x{K}->{N} linear: smoothing + per-token quant + "
-                      f"int32 GEMM + bf16 epilogue (weights prepared outside the timing), "
-                      f"{dt:.1f} s"}
+        return None
+    per = []
+    total_s = 0.0
+    total_ops = 0
+    for c, prot, count in shapes:
+        lin = _OracleLinear(c, prot)
+        rows, dt = lin.rows_for(target_s / len(shapes))
+        row_s = dt / rows
+        total_s += row_s * lin.M * count
+        total_ops += 2 * lin.M * lin.N * lin.K * count
+        per.append(f"{'bf16' if prot else 'W8A8'} {lin.M}x{lin.K}->{lin.N} x{count}: "
+                   f"{rows} rows in {dt:.2f} s")
+    return {"value": round(total_ops / total_s / 1e12, 6), "unit": "TOPS",
+            "cores": oracle.num_threads(), "kind": "oracle (extrapolated)",
+            "step_s_extrapolated": round(total_s, 2),
+            "sample": f"{label}: each distinct linear timed on a row sample, the step's time "
+                      f"extrapolated as the sum over shapes of time per row x {synth.TOKENS} "
+                      f"rows x count (" + "; ".join(per) + ")"}
 
 
 # --------------------------------------------------------------------------
@@ -625,10 +693,24 @@ def counter_traffic(workload: str):
 COPY_BYTES = 512 << 20
 
 
-def counter_run(layers, dev, reps: int = 3, codes: str = "workload"):
+def counter_run(layers, dev, reps: int = 3, codes: str = "workload", path: str = "w8a8"):
     """codes="uniform" replaces the workload's int8 codes (X and W) by
     uniform random ones in [-127, 127], to compare the clock the GPU holds
-    under the two (same launches, same scales)."""
+    under the two (same launches, same scales). path="bf16" runs the
+    workload's protected layer (bf16_linear) instead of the W8A8 one."""
+    if path == "bf16":
+        lin = max((x for x in layers if x.lay.protected), key=lambda x: x.ops)
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(reps):
+            ops.bf16_linear(lin.xs[0], lin.lay.W, lin.lay.bias, out=lin.Y)
+            torch.cuda.synchronize()
+            torch.neg(src, out=dst)
+            torch.cuda.synchronize()
+        log(f"counter run: {reps} x bf16_linear {lin.M}x{lin.lay.K}->{lin.lay.N}, "
+            f"{reps} x neg over {COPY_BYTES} bytes")
+        return lin
     lin = max((x for x in layers if not x.lay.protected), key=lambda x: x.ops)
     ws = L.Workspace(dev)
     Xq, xs = ws.get(lin.M, lin.lay.K)
@@ -737,6 +819,8 @@ def main():
                     help="only the short launch sequence the counter passes profile")
     ap.add_argument("--counter-codes", choices=["workload", "uniform"], default="workload",
                     help="int8 codes of the counter run: the workload's, or uniform random")
+    ap.add_argument("--counter-path", choices=["w8a8", "bf16"], default="w8a8",
+                    help="the linear the counter run launches: W8A8, or the protected bf16 one")
     ap.add_argument("--counters-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 counter runs into profiles/ (no GPU)")
     args = ap.parse_args()
@@ -764,7 +848,7 @@ def main():
     log(f"workload {args.workload}: {len(layers)} linears prepared in "
         f"{time.perf_counter() - t_build:.1f} s")
     if args.counter_run:
-        counter_run(layers, dev, codes=args.counter_codes)
+        counter_run(layers, dev, codes=args.counter_codes, path=args.counter_path)
         return
 
     # per-kernel durations inside the timed steps (events between kernels)
@@ -883,7 +967,8 @@ def main():
         accuracy = accuracy_report(layers, dev)
 
     cpu = None
-    if not args.no_cpu_baseline and args.workload in ("ffn_up", "ffn_down"):
+    if not args.no_cpu_baseline and args.workload in ("ffn_up", "ffn_down", "dit_block",
+                                                       "backbone"):
         log("timing the CPU oracle on a bounded sample ...")
         cpu = cpu_baseline(args.workload, args.cpu_seconds)
 

@@ -53,6 +53,9 @@ MUTANTS = {
     "half_truncates": ("q = nearbyint(ldexp(fabs(d), -ulp_exp));", "q = floor(ldexp(fabs(d), -ulp_exp));"),
     "half_no_subnormals": ("    if (ulp_exp < -24)\n        ulp_exp = -24;\n    q = nearbyint(ldexp(fabs(d), -ulp_exp));",
                            "    if (ulp_exp < -14)\n        ulp_exp = -14;\n    q = nearbyint(ldexp(fabs(d), -ulp_exp));"),
+    # coding against the unrounded scale is what the common GGUF encoder
+    # does; under this repository's reading (codes on the stored grid) it is
+    # a deviation the pins must notice, not a claim that the encoder is wrong
     "q8_0_codes_from_unrounded_scale": ("inv = ds != 0.0f ? 1.0f / ds : 0.0f;", "inv = s != 0.0f ? 1.0f / s : 0.0f;"),
     "q8_0_no_clamp": ("                if (c > 127.0f)\n                    c = 127.0f;\n", ""),
     "q8_0_no_scale_cap": ("            if (s > ORACLE_HALF_MAX)\n                s = ORACLE_HALF_MAX;\n", ""),

@@ -107,6 +107,23 @@ w8a8_status w8a8_act_absmax(const uint16_t *X, int64_t M, int64_t K,
 w8a8_status w8a8_act_moments(const uint16_t *X, int64_t M, int64_t K, void *work,
                              double *stats, w8a8_stream stream);
 
+/* w8a8_act_moments for callers that cannot allocate device memory or pass
+ * a workspace (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same kernels, results bit-identical to
+ * w8a8_act_moments on the same X, with the workgroup states in a
+ * W8A8_MOMENTS_WORK_BYTES device array that the library itself holds, one
+ * per GPU, from that GPU's first call until the process ends. That array is
+ * a fixed size for every input, so the limits are those of
+ * w8a8_act_moments (M and K out of range: W8A8_ERR_SHAPE or
+ * W8A8_ERR_UNSUPPORTED). The call allocates nothing; its first call on a
+ * device looks the array's address up (hipGetSymbolAddress), so the device
+ * of X, stats and stream must be the current device. Nothing in the array
+ * needs to start at zero. Calls on one GPU share the array: calls that can
+ * overlap there (different streams without ordering) race and give wrong
+ * statistics; order them on one stream. */
+w8a8_status w8a8_act_moments_noalloc(const uint16_t *X, int64_t M, int64_t K,
+                                     double *stats, w8a8_stream stream);
+
 /* Protection choice (Section 3, "Activation-fragility profiling and
  * protection": the layers whose inputs are most fragile stay in bf16, N = 17
  * of 211 per branch, and the ranking is checked for stability between the

@@ -30,6 +30,7 @@ SIGNATURES = {
     "w8a8_last_hip_error": ([], ctypes.c_char_p),
     "w8a8_act_absmax": ([_P, _I64, _I64, _P, _P], _S),
     "w8a8_act_moments": ([_P, _I64, _I64, _P, _P, _P], _S),
+    "w8a8_act_moments_noalloc": ([_P, _I64, _I64, _P, _P], _S),
     "w8a8_fragility_scores": ([_P, _I64, _I64, _I64, _I64, _P], _S),
     "w8a8_select_protected": ([_P, _I64, _I64, _P], _S),
     "w8a8_rank_correlation": ([_P, _P, _I64, _P], _S),

@@ -131,6 +131,16 @@ w8a8_status w8a8_act_moments(const uint16_t *X, int64_t M, int64_t K, void *work
                                                as_stream(stream)));
 }
 
+w8a8_status w8a8_act_moments_noalloc(const uint16_t *X, int64_t M, int64_t K, double *stats,
+                                     w8a8_stream stream) {
+    if (X == nullptr || stats == nullptr) return W8A8_ERR_NULL;
+    W8A8_TRY(check_rows(M, kMaxRows));
+    W8A8_TRY(check_k(K));
+    if (!aligned(X, 16) || !aligned(stats, 8)) return W8A8_ERR_ALIGN;
+    W8A8_TRY(check_alias({{stats, 32}}, {{X, 2 * M * K}}));
+    return hip_status(w8a8::launch_act_moments_noalloc(X, M * K, stats, as_stream(stream)));
+}
+
 w8a8_status w8a8_smooth_factors(const float *act_absmax, const uint16_t *W, int64_t N,
                                 int64_t K, double alpha, float *lambda, w8a8_stream stream) {
     if (act_absmax == nullptr || W == nullptr || lambda == nullptr) return W8A8_ERR_NULL;

@@ -30,6 +30,10 @@ hipError_t launch_col_absmax(const uint16_t *src, int64_t R, int64_t K,
 constexpr int kMomentBlocks = 1024;
 hipError_t launch_act_moments(const uint16_t *X, int64_t n, double *work, double *stats,
                               hipStream_t stream);
+// The same with the workgroup states in the library's file-scope device
+// array of the current device (no workspace, no allocation).
+hipError_t launch_act_moments_noalloc(const uint16_t *X, int64_t n, double *stats,
+                                      hipStream_t stream);
 
 // GGUF Q8_0: codes qs [N][K] and binary16 scales d [N][K/32] of W [N][K]
 // bf16 (32 | K), and back to bf16(d * q).

@@ -18,7 +18,16 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
+#include <mutex>
+
 #include "internal.h"
+
+// Workgroup states of w8a8_act_moments_noalloc, for callers that cannot
+// allocate: one file-scope device array instead of a caller workspace. Each
+// GPU the library runs on holds its own copy until the process ends; host
+// code never uses this name as an address (see moments_scratch below).
+static __device__ __align__(256) double scratch[6 * w8a8::kMomentBlocks];
 
 namespace w8a8 {
 namespace {
@@ -205,6 +214,50 @@ __global__ __launch_bounds__(kMomentBlocks) void moments_final_kernel(
 }
 
 }  // namespace
+
+namespace {
+
+// Device address of `scratch` on each GPU, looked up once per device with
+// that device current (each GPU has its own copy at its own address).
+constexpr int kMaxDevices = 256;
+std::atomic<double *> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+hipError_t moments_scratch(double **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    double *p = g_scratch[dev].load(std::memory_order_acquire);
+    if (p == nullptr) {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        p = g_scratch[dev].load(std::memory_order_relaxed);
+        if (p == nullptr) {
+            void *q = nullptr;
+            e = hipGetSymbolAddress(&q, HIP_SYMBOL(scratch));
+            if (e != hipSuccess) return e;
+            if (q == nullptr) return hipErrorInvalidSymbol;
+            p = static_cast<double *>(q);
+            g_scratch[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return hipSuccess;
+}
+
+}  // namespace
+
+static_assert(sizeof(scratch) == 6 * kMomentBlocks * sizeof(double), "scratch size");
+
+hipError_t launch_act_moments_noalloc(const uint16_t *X, int64_t n, double *stats,
+                                      hipStream_t stream) {
+    double *work = nullptr;
+    const hipError_t e = moments_scratch(&work);
+    if (e != hipSuccess) return e;
+    // Every workgroup of the pass writes its state before the final merge
+    // reads it (stream order), so nothing needs clearing between calls.
+    return launch_act_moments(X, n, work, stats, stream);
+}
 
 hipError_t launch_act_moments(const uint16_t *X, int64_t n, double *work, double *stats,
                               hipStream_t stream) {

@@ -93,6 +93,20 @@ def w8a8_act_moments(X: torch.Tensor, work: torch.Tensor | None = None,
     return stats
 
 
+def w8a8_act_moments_noalloc(X: torch.Tensor, out: torch.Tensor) -> torch.Tensor:
+    """w8a8_act_moments with no workspace: the library's own device array
+    holds the partial states (for callers that cannot allocate; `out`, float64
+    [4] on X's device, is required). Calls that overlap on one GPU race."""
+    _need(X, "X", torch.bfloat16, 2)
+    M, K = X.shape
+    stats = _out(out, (4,), torch.float64, X.device, "out")
+    lib = load()
+    with torch.cuda.device(X.device):
+        check("w8a8_act_moments_noalloc",
+              lib.w8a8_act_moments_noalloc(_ptr(X), M, K, _ptr(stats), _stream(X.device)))
+    return stats
+
+
 def w8a8_smooth_factors(act_absmax: torch.Tensor, W: torch.Tensor, alpha: float = 0.5,
                         out: torch.Tensor | None = None) -> torch.Tensor:
     """lambda_j = s_j^alpha / max_i |W_ij|^(1 - alpha) -> fp32 [K]."""

@@ -171,6 +171,20 @@ def test_calibration_validation(lib):
     assert g(A + 2, 8, 64, C, None) == ALIGN
 
 
+def test_moments_noalloc_validation(lib):
+    f = lib.w8a8_act_moments_noalloc
+    assert f(None, 8, 64, C, None) == NULL
+    assert f(A, 8, 64, None, None) == NULL
+    assert f(A, 0, 64, C, None) == SHAPE
+    assert f(A, (1 << 22) + 1, 64, C, None) == SHAPE
+    assert f(A, 8, 0, C, None) == SHAPE
+    assert f(A, 8, 96, C, None) == UNSUP
+    assert f(A, 8, 65536 + 64, C, None) == UNSUP
+    assert f(A + 2, 8, 64, C, None) == ALIGN
+    assert f(A, 8, 64, C + 4, None) == ALIGN
+    assert f(A, 8, 64, A + 64, None) == ALIAS        # stats inside X
+
+
 def test_moments_validation(lib):
     f = lib.w8a8_act_moments
     assert f(None, 8, 64, B, C, None) == NULL

@@ -99,6 +99,10 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, int8_t *lds, uint32_t off) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LDS_AS void *)lds, 16, off, 0, 0, 0);
 }
+// 4 bytes per lane: 256 bytes of LDS per wave instruction, lane l at +4 l.
+__device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t r, int8_t *lds, uint32_t off) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LDS_AS void *)lds, 4, off, 0, 0, 0);
+}
 // Instruction-group ordering for the scheduler (sched_group_barrier masks:
 // 0x008 MFMA, 0x100 LDS read, 0x020 global/buffer read). One MFMA, then one
 // LDS read while any remain, then one buffer load while any remain, repeated:
@@ -406,6 +410,66 @@ struct Epi {
                         static_cast<uint16_t>(static_cast<uint32_t>(v[e >> 1]) >> (16 * (e & 1))),
                         ry, off, 0, 0);
                 }
+            }
+        }
+    }
+
+    // store_slices with the operands read from their LDS copy as each
+    // group of four channels is converted (tile-local token mbase.., channel
+    // nbase..; n0 is the tile's first channel), not held in registers for
+    // the whole epilogue. N % 8 == 0.
+    template <class Acc>
+    __device__ __forceinline__ void store_slices_lds(const Acc (&acc)[TI][TJ], int8_t *stage,
+                                                     const float *xs_l, const float *ws_l,
+                                                     const uint16_t *b_l, void *Yout, int m0,
+                                                     int rows_x, int mbase, int nbase, int n0,
+                                                     int N, int frow, int fhalf, int lane) const {
+        static_assert(EPI != kStoreI32, "row stores are for the bf16 epilogues");
+        constexpr int CPR = 64 * TI / 16;  // 16-byte chunks per row
+        constexpr int ROUNDS = 32 * CPR / 64;
+        static_assert(32 * CPR % 64 == 0, "whole store rounds");
+        const __amdgpu_buffer_rsrc_t ry =
+            make_rsrc(static_cast<int8_t *>(Yout) + static_cast<int64_t>(m0) * N * 2,
+                      static_cast<uint32_t>(rows_x) * N * 2u);
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) {
+            const float xv = EPI == kDequantBf16 ? xs_l[mbase + 32 * j + frow] : 0.0f;
+#pragma unroll
+            for (int i = 0; i < TI; ++i)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int c = 32 * i + 8 * g + 4 * fhalf;
+                    float4 w4 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                    if constexpr (EPI == kDequantBf16)
+                        w4 = *reinterpret_cast<const float4 *>(ws_l + nbase + c);
+                    uint2 b2 = make_uint2(0u, 0u);
+                    if constexpr (HAS_BIAS) b2 = *reinterpret_cast<const uint2 *>(b_l + nbase + c);
+                    const float wv[4] = {w4.x, w4.y, w4.z, w4.w};
+                    const uint32_t bw[2] = {b2.x, b2.y};
+                    float y[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float a = static_cast<float>(acc[i][j][4 * g + e]);
+                        const float b =
+                            __uint_as_float((e & 1) ? (bw[e >> 1] & 0xffff0000u) : (bw[e >> 1] << 16));
+                        if constexpr (EPI == kDequantBf16)
+                            y[e] = __builtin_fmaf(a, xv * wv[e], b);
+                        else
+                            y[e] = a + b;
+                    }
+                    *reinterpret_cast<v2u *>(stage + frow * kRowStride + c * 2) =
+                        v2u{f32x2_to_bf16x2(y[0], y[1]), f32x2_to_bf16x2(y[2], y[3])};
+                }
+#pragma unroll
+            for (int r = 0; r < ROUNDS; ++r) {
+                const int id = r * 64 + lane;
+                const int row = id / CPR;
+                const int c = id % CPR;
+                const v4i v = *reinterpret_cast<const v4i *>(stage + row * kRowStride + c * 16);
+                const int n = n0 + nbase + 8 * c;
+                const uint32_t base = static_cast<uint32_t>(mbase + 32 * j + row) * N;
+                const uint32_t off = n + 8 <= N ? (base + n) * 2u : kOutOfRange;
+                __builtin_amdgcn_raw_buffer_store_b128(v, ry, off, 0, 0);
             }
         }
     }
@@ -974,6 +1038,203 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_2s_kernel(
 }
 
 // --------------------------------------------------------------------------
+// gemm_pt_kernel: gemm_2s_kernel's 12-wave tile (288 x 256, 96 x 64 per
+// wave, four loading waves, two-slot ring of 128-byte K tiles) made
+// persistent. Workgroup b walks tiles b, b + G, b + 2G, ... (G = gridDim.x,
+// a multiple of 8, so every tile of a workgroup maps to the XCD it runs on
+// and the tiles resident on an XCD at any time are those gemm_2s_kernel's
+// round would place there). What a new workgroup would wait for is fetched
+// while the previous tile drains:
+//   - the next tile's first K tile is loaded at the boundary of the current
+//     tile's second-to-last K tile, into the slot it frees;
+//   - its second K tile right after the epilogue, into the slot that staged
+//     the output rows;
+//   - the epilogue operands (x_scale, w_scale, bias) by direct-to-LDS
+//     dword loads from a wave that issues no tile loads, one tile ahead of
+//     their use.
+// Slots alternate over the workgroup's whole K-tile sequence. Each slot holds
+// X then W contiguously (68 KB), so one slot can stage all 12 waves' 32-token
+// output slices (55 KB). Needs 256 <= K bytes, N % 8 == 0 and w_scale / bias
+// 16 / 8-byte aligned (the launcher checks).
+// --------------------------------------------------------------------------
+template <class Op, int EPI, bool HAS_BIAS>
+__global__ __launch_bounds__(768) void gemm_pt_kernel(
+    const int8_t *__restrict__ X, const int8_t *__restrict__ W, const float *__restrict__ xs,
+    const float *__restrict__ ws, const uint16_t *__restrict__ bias, int M, int N, int Kb,
+    void *__restrict__ Yout, int tiles_m, int tiles_n) {
+    constexpr int BM = 288, BN = 256, BK = 128, SWZ = 1, GROUP_M = 8;
+    constexpr int WAVES_N = 4;
+    constexpr int WTM = 96, WTN = 64;
+    constexpr int TJ = WTM / 32, TI = WTN / 32;
+    constexpr int NI = 4;                 // loading waves
+    constexpr int EPW = NI;               // the wave that loads the epilogue operands
+    constexpr int LX = BM * BK / 1024 / NI;  // 9 DMA blocks per loading wave, X
+    constexpr int LW = BN * BK / 1024 / NI;  // 8, W
+    constexpr int LOADS = LX + LW;
+    constexpr int XSLOT = BM * BK;
+    constexpr int SLOT = (BM + BN) * BK;
+    constexpr int ROWS_PER_DMA = 1024 / BK;  // 8 rows of a panel per 1 KiB block
+    using EpiT = Epi<TI, TJ, EPI, true, HAS_BIAS>;
+    static_assert(12 * EpiT::kSliceBytes <= SLOT, "output slices stage in one slot");
+    // epilogue operands: x_scale [320] (BM rounded up to whole 64-lane
+    // dword loads), w_scale [256], bias [256] bf16
+    constexpr int EP_XS = 320 * 4, EP_WS = BN * 4, EP_B = BN * 2;
+    constexpr int NXS = EP_XS / 256, NWS = EP_WS / 256, NB = EP_B / 256;
+    static_assert(2 * SLOT + EP_XS + EP_WS + EP_B <= 160 * 1024, "LDS");
+
+    __shared__ __attribute__((aligned(1024))) int8_t smem[2 * SLOT + EP_XS + EP_WS + EP_B];
+    float *ep_xs = reinterpret_cast<float *>(smem + 2 * SLOT);
+    float *ep_ws = reinterpret_cast<float *>(smem + 2 * SLOT + EP_XS);
+    uint16_t *ep_b = reinterpret_cast<uint16_t *>(smem + 2 * SLOT + EP_XS + EP_WS);
+    keep_args(xs, ws, bias, Yout);
+
+    const int total = tiles_m * tiles_n;
+    const int lane = threadIdx.x & 63;
+    const int wave = wave_id();
+    const int mbase = (wave / WAVES_N) * WTM;
+    const int nbase = (wave % WAVES_N) * WTN;
+    const bool loader = wave < NI;
+    const int iw = loader ? wave : 0;
+    const int KT = Kb / BK;  // >= 2, the launcher guarantees BK divides Kb
+    // Lane part of every DMA offset: block iw + i NI starts 32 i rows below
+    // block iw, and the swizzle key of a row does not change over 32 rows.
+    const uint32_t off0 = dma_offset<BK, SWZ>(iw, lane, Kb);
+    const uint32_t panel_step = static_cast<uint32_t>(NI * ROWS_PER_DMA) * Kb;
+
+    auto slot_ptr = [&](int q) { return smem + (q & 1) * SLOT; };
+    struct Tile {
+        int m0, n0, rows_x, rows_w;
+        __amdgpu_buffer_rsrc_t rx, rw;
+    };
+    auto tile_of = [&](int t) {
+        int tm, tn;
+        map_tile<GROUP_M>(t, tiles_m, tiles_n, tm, tn);
+        Tile r;
+        r.m0 = tm * BM;
+        r.n0 = tn * BN;
+        r.rows_x = min(BM, M - r.m0);
+        r.rows_w = min(BN, N - r.n0);
+        r.rx = make_rsrc(X + static_cast<int64_t>(r.m0) * Kb, static_cast<uint32_t>(r.rows_x) * Kb);
+        r.rw = make_rsrc(W + static_cast<int64_t>(r.n0) * Kb, static_cast<uint32_t>(r.rows_w) * Kb);
+        return r;
+    };
+    // Load i of this wave's share of K tile kt of `tl` into the slot of
+    // sequence number q: W blocks first, then X blocks.
+    // (The opaque copy of off0 keeps the compiler from hoisting the 17
+    // per-load sums out of the loops, which would hold 17 registers.)
+    auto issue_one = [&](const Tile &tl, int kt, int q, int i) {
+        if (!loader) return;
+        int8_t *slot = slot_ptr(q);
+        uint32_t base = off0;
+        asm volatile("" : "+v"(base));
+        if (i < LW)
+            dma16(tl.rw, slot + XSLOT + (iw + i * NI) * 1024, base + (i * panel_step + kt * BK));
+        else
+            dma16(tl.rx, slot + (iw + (i - LW) * NI) * 1024,
+                  base + ((i - LW) * panel_step + kt * BK));
+    };
+    // The epilogue operands of `tl` into LDS (wave EPW; zero past M / N).
+    auto issue_ep = [&](const Tile &tl) {
+        if (wave != EPW || EPI == kStoreI32) return;
+        if constexpr (EPI == kDequantBf16) {
+            const __amdgpu_buffer_rsrc_t rxs =
+                make_rsrc(xs + tl.m0, static_cast<uint32_t>(tl.rows_x) * 4u);
+            const __amdgpu_buffer_rsrc_t rws =
+                make_rsrc(ws + tl.n0, static_cast<uint32_t>(tl.rows_w) * 4u);
+#pragma unroll
+            for (int i = 0; i < NXS; ++i)
+                dma4(rxs, reinterpret_cast<int8_t *>(ep_xs) + 256 * i, 4u * lane + 256u * i);
+#pragma unroll
+            for (int i = 0; i < NWS; ++i)
+                dma4(rws, reinterpret_cast<int8_t *>(ep_ws) + 256 * i, 4u * lane + 256u * i);
+        }
+        const __amdgpu_buffer_rsrc_t rb =
+            make_rsrc(HAS_BIAS ? bias + tl.n0 : bias,
+                      HAS_BIAS ? static_cast<uint32_t>(tl.rows_w) * 2u : 0u);
+#pragma unroll
+        for (int i = 0; i < NB; ++i)
+            dma4(rb, reinterpret_cast<int8_t *>(ep_b) + 256 * i, 4u * lane + 256u * i);
+    };
+
+    Mma1<Op, BK, TI, TJ, SWZ> mma;
+    int t = blockIdx.x;
+    Tile cur = tile_of(t);
+    int q = 0;  // sequence number of the current tile's first K tile
+
+    // Prologue of the first tile: K tiles 0 and 1, its epilogue operands.
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) issue_one(cur, 0, 0, i);
+    issue_ep(cur);
+    wait_vmcnt<0>();
+    barrier();
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) issue_one(cur, 1, 1, i);
+    mma.init(lane, mbase, nbase);
+    mma.template load<0>(slot_ptr(0), slot_ptr(0) + XSLOT);
+
+    auto boundary = [&] {
+        wait_lgkmcnt0();  // this wave's reads of the current slot are done
+        wait_vmcnt<0>();  // and its loads of the next K tile have landed
+        barrier();
+    };
+    for (;;) {
+        // Lane-dependent addresses are rederived per tile from an opaque
+        // copy of the lane id rather than hoisted and held across tiles.
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        const int tn_ = t + static_cast<int>(gridDim.x);
+        const bool has_next = tn_ < total;
+        const Tile nxt = tile_of(has_next ? tn_ : t);
+        int kt = 0;
+        auto issue_kt2 = [&](int i) { issue_one(cur, kt + 2, q + kt + 2, i); };
+        for (; kt + 2 < KT; ++kt)
+            mma.template tile<false, LOADS>(slot_ptr(q + kt), slot_ptr(q + kt) + XSLOT,
+                                            slot_ptr(q + kt + 1), slot_ptr(q + kt + 1) + XSLOT,
+                                            boundary, issue_kt2);
+        // K tile KT-2: its boundary sends the next tile's first K tile into
+        // the slot it frees.
+        auto issue_next0 = [&](int i) {
+            if (has_next) issue_one(nxt, 0, q + KT, i);
+        };
+        mma.template tile<false, LOADS>(slot_ptr(q + kt), slot_ptr(q + kt) + XSLOT,
+                                        slot_ptr(q + kt + 1), slot_ptr(q + kt + 1) + XSLOT,
+                                        boundary, issue_next0);
+        ++kt;
+        mma.template tile<true, 0>(slot_ptr(q + kt), slot_ptr(q + kt) + XSLOT,
+                                   slot_ptr(q + kt), slot_ptr(q + kt) + XSLOT, [] {},
+                                   [](int) {});
+        // Epilogue. The slot of K tile KT-1 stages the output rows; the
+        // other slot holds the next tile's first K tile.
+        int8_t *stage = slot_ptr(q + KT - 1);
+        wait_lgkmcnt0();
+        wait_vmcnt<0>();  // loaders: the next first K tile; EPW: the operands
+        barrier();
+        EpiT epi;
+        if constexpr (EPI == kStoreI32) {
+            epi.store(mma.acc, Yout, cur.m0, cur.rows_x, mbase, cur.n0 + nbase, N, ln & 31,
+                      ln >> 5);
+        } else {
+            epi.store_slices_lds(mma.acc, stage + wave * EpiT::kSliceBytes, ep_xs, ep_ws, ep_b,
+                                 Yout, cur.m0, cur.rows_x, mbase, nbase, cur.n0, N, ln & 31,
+                                 ln >> 5, ln);
+        }
+        if (!has_next) break;
+        wait_lgkmcnt0();
+        barrier();  // staging slot and operand area free
+        q += KT;
+        cur = nxt;
+        t = tn_;
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) issue_one(cur, 1, q + 1, i);
+        issue_ep(cur);
+        int ln2 = lane;
+        asm volatile("" : "+v"(ln2));
+        mma.init(ln2, mbase, nbase);
+        mma.template load<0>(slot_ptr(q), slot_ptr(q) + XSLOT);
+    }
+}
+
+// --------------------------------------------------------------------------
 // gemm_ws_kernel: NPROD producer waves issue the tile loads, WAVES_M x
 // WAVES_N consumer waves multiply. One barrier per K tile hands slots over:
 //   barrier #0: tile 0 has landed;
@@ -1174,6 +1435,54 @@ struct Specialized {
     }
 };
 
+// The persistent 288 x 256 kernel: one workgroup per CU (a multiple of 8,
+// at most one per tile), each walking its tiles.
+int persistent_grid() {
+    static int cached[256] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 256) return 0;
+    if (cached[dev] == 0) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        cached[dev] = cus / 8 * 8;
+    }
+    return cached[dev];
+}
+
+template <class Op, int EPI>
+struct Persistent {
+    template <bool HB>
+    static const void *fn() {
+        return reinterpret_cast<const void *>(&gemm_pt_kernel<Op, EPI, HB>);
+    }
+    // Whether the persistent kernel takes this launch: whole rounds of
+    // 288 x 256 tiles to walk, at least two K tiles, and the vector
+    // epilogue's layout (N % 8 == 0, w_scale / bias aligned).
+    static bool applies(const GemmArgs &a, int grid) {
+        const int64_t tiles = static_cast<int64_t>((a.M + 287) / 288) * ((a.N + 255) / 256);
+        return grid >= 8 && tiles > grid && a.Kb % 128 == 0 && a.Kb >= 256 && a.N % 8 == 0 &&
+               (reinterpret_cast<uintptr_t>(a.ws) & 15) == 0 &&
+               (reinterpret_cast<uintptr_t>(a.bias) & 7) == 0;
+    }
+    static hipError_t launch(const GemmArgs &a, int grid) {
+        int tiles_m = (a.M + 287) / 288;
+        int tiles_n = (a.N + 255) / 256;
+        const bool has_bias = EPI != kStoreI32 && a.bias != nullptr;
+        const void *f = has_bias ? fn<true>() : fn<false>();
+        const int8_t *X = a.X;
+        const int8_t *W = a.W;
+        const float *xs = a.xs;
+        const float *ws = a.ws;
+        const uint16_t *bias = a.bias;
+        int M = a.M, N = a.N, Kb = a.Kb;
+        void *Y = a.Y;
+        void *args[] = {&X, &W, &xs, &ws, &bias, &M, &N, &Kb, &Y, &tiles_m, &tiles_n};
+        return hipLaunchKernel(f, dim3(static_cast<unsigned>(grid)), dim3(768), args, 0,
+                               a.stream);
+    }
+};
+
 template <class Op, int BM, int BN, int WAVES_M, int WAVES_N, int SWZ, int GROUP_M, int EPI>
 struct TwoSlot {
     template <bool NV, bool HB>
@@ -1241,8 +1550,11 @@ template <class Op, int EPI>
 hipError_t launch_default(const GemmArgs &a) {
     if (a.Kb % 128 == 0) {
         switch (pick_tiles(a.M, a.N)) {
-        case 0:
+        case 0: {
+            const int grid = persistent_grid();
+            if (Persistent<Op, EPI>::applies(a, grid)) return Persistent<Op, EPI>::launch(a, grid);
             return TwoSlot<Op, 288, 256, 3, 4, 1, 8, EPI>::launch(a);
+        }
         case 1:
             return TwoSlot<Op, 192, 256, 2, 4, 1, 4, EPI>::launch(a);
         case 2:

@@ -539,7 +539,7 @@ def dequant_bytes(fmt: str, N: int, K: int) -> int:
     planes read once, the bf16 weights written once."""
     if fmt == "q8_0":
         return N * K + 2 * (N * K // 32) + 2 * N * K
-    return N * K // 2 + 2 * (N * K // 32) + 4 * (N * K // 256) + 2 * N * K
+    return N * K // 2 + 12 * (N * K // 256) + 4 * (N * K // 256) + 2 * N * K
 
 
 # --------------------------------------------------------------------------

@@ -278,15 +278,20 @@ w8a8_status q8_0_linear(const uint16_t *X, const int8_t *qs, const uint16_t *d,
 
 /* ---------------------------------------------------------------------- */
 /* GGUF Q4_K weight-only (Section 3, "GGUF k-quants": 4-bit codes in       */
-/* super-blocks; the encoder is the paper's own). A super-block is 256     */
-/* consecutive weights of a row, cut into 8 sub-blocks of 32; sub-block j  */
-/* reads back as d*sc_j*q - dmin*m_j with q in [0,15], sc_j, m_j in [0,63] */
-/* and binary16 d, dmin per super-block. Stored planar:                    */
+/* super-blocks, 4.5 bits per weight; the encoder is the paper's own). A   */
+/* super-block is 256 consecutive weights of a row, cut into 8 sub-blocks  */
+/* of 32; sub-block j reads back as d*sc_j*q - dmin*m_j with q in [0,15],  */
+/* sc_j, m_j in [0,63] and binary16 d, dmin per super-block. Stored planar: */
 /*   qs [N][K/2]  two 4-bit codes per byte, even k in the low nibble       */
-/*   sc, mn [N][K/32]  one byte per sub-block (6-bit values)               */
+/*   scales [N][K/256][12]  the super-block's sc_j and m_j in the GGUF     */
+/*     k-quant scale layout: for j < 4, bytes j and j+4 hold sc_j and m_j  */
+/*     in their low 6 bits; for j >= 4, byte j+4 holds the low 4 bits of   */
+/*     sc_j (low nibble) and m_j (high nibble), and their top 2 bits are   */
+/*     the top 2 bits of bytes j-4 (sc_j) and j (m_j)                      */
 /*   d, dmin [N][K/256]  binary16 bits                                     */
-/* (4.625 bits per weight). K must be a multiple of 256, else              */
-/* W8A8_ERR_UNSUPPORTED; qs 16-byte aligned, d and dmin 2-byte aligned.    */
+/* (4 + (96 + 32)/256 = 4.5 bits per weight). K must be a multiple of 256, */
+/* else W8A8_ERR_UNSUPPORTED; qs 16-byte aligned, scales 4-byte, d and     */
+/* dmin 2-byte aligned.                                                    */
 /* ---------------------------------------------------------------------- */
 
 /* Encode, round to nearest on a min-max grid (binary32, one rounding per
@@ -297,23 +302,24 @@ w8a8_status q8_0_linear(const uint16_t *X, const int8_t *qs, const uint16_t *d,
  * q = clamp(rint((w + dmin*m_j)*RN32(1/(d*sc_j))), 0, 15) (0 where d*sc_j
  * is 0). W [N][K] bf16, 16-byte aligned. Outputs must not overlap W or
  * each other. */
-w8a8_status q4_k_quantize(const uint16_t *W, int64_t N, int64_t K, uint8_t *qs, uint8_t *sc,
-                          uint8_t *mn, uint16_t *d, uint16_t *dmin, w8a8_stream stream);
+w8a8_status q4_k_quantize(const uint16_t *W, int64_t N, int64_t K, uint8_t *qs,
+                          uint8_t *scales, uint16_t *d, uint16_t *dmin,
+                          w8a8_stream stream);
 
 /* Decode: W[n][k] = bf16(RN32(d*sc_j*q - dmin*m_j)) (d*sc_j*q is exact in
  * binary32). W [N][K] bf16, 16-byte aligned, must not overlap the planes. */
-w8a8_status q4_k_dequantize(const uint8_t *qs, const uint8_t *sc, const uint8_t *mn,
-                            const uint16_t *d, const uint16_t *dmin, int64_t N, int64_t K,
-                            uint16_t *W, w8a8_stream stream);
+w8a8_status q4_k_dequantize(const uint8_t *qs, const uint8_t *scales,
+                            const uint16_t *d, const uint16_t *dmin, int64_t N,
+                            int64_t K, uint16_t *W, w8a8_stream stream);
 
 /* The weight-only linear on the decoded weights: Y = bf16_linear(X,
  * decode(planes), bias). The decoded weights go to `work` (caller-owned,
  * 2 N K bytes, 16-byte aligned, overwritten). X [M][K] bf16, bias [N] bf16
  * or NULL -> Y [M][N] bf16; limits as bf16_linear. */
-w8a8_status q4_k_linear(const uint16_t *X, const uint8_t *qs, const uint8_t *sc,
-                        const uint8_t *mn, const uint16_t *d, const uint16_t *dmin,
-                        const uint16_t *bias, int64_t M, int64_t N, int64_t K, uint16_t *work,
-                        uint16_t *Y, w8a8_stream stream);
+w8a8_status q4_k_linear(const uint16_t *X, const uint8_t *qs, const uint8_t *scales,
+                        const uint16_t *d, const uint16_t *dmin, const uint16_t *bias,
+                        int64_t M, int64_t N, int64_t K, uint16_t *work, uint16_t *Y,
+                        w8a8_stream stream);
 
 #ifdef __cplusplus
 }

@@ -74,8 +74,10 @@ def _load():
         "oracle_q8_0_quantize": ([P, I64, I64, P, P], None),
         "oracle_q8_0_dequantize": ([P, P, I64, I64, P], None),
         "oracle_adaln_modulate": ([P, P, P, I64, I64, ctypes.c_double, P], None),
-        "oracle_q4_k_quantize": ([P, I64, I64, P, P, P, P, P], None),
-        "oracle_q4_k_dequantize": ([P, P, P, P, P, I64, I64, P], None),
+        "oracle_q4_k_quantize": ([P, I64, I64, P, P, P, P], None),
+        "oracle_q4_k_dequantize": ([P, P, P, P, I64, I64, P], None),
+        "oracle_q4_k_pack_scales": ([P, P, P], None),
+        "oracle_q4_k_unpack_scales": ([P, P, P], None),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -329,24 +331,53 @@ Q4_K_SUB = 32
 
 def q4_k_quantize(W, N: int, K: int):
     """W [N][K] bf16 bits -> dict of the Q4_K planes: qs uint8 [N][K/2] (two
-    4-bit codes per byte, even k low), sc and mn uint8 [N][K/32], d and dmin
-    binary16 bits [N][K/256]."""
+    4-bit codes per byte, even k low), scales uint8 [N][K/256 * 12] (each
+    super-block's eight 6-bit sub-block scales and offsets, packed), d and
+    dmin binary16 bits [N][K/256]."""
     W = _c(W, np.uint16)
     qs = np.zeros(N * K // 2, np.uint8)
-    sc = np.zeros(N * (K // Q4_K_SUB), np.uint8)
-    mn = np.zeros(N * (K // Q4_K_SUB), np.uint8)
+    scales = np.zeros(N * (K // Q4_K_SUPER) * 12, np.uint8)
     d = np.zeros(N * (K // Q4_K_SUPER), np.uint16)
     dmin = np.zeros(N * (K // Q4_K_SUPER), np.uint16)
-    _load().oracle_q4_k_quantize(_p(W), N, K, _p(qs), _p(sc), _p(mn), _p(d), _p(dmin))
-    return {"qs": qs.reshape(N, K // 2), "sc": sc.reshape(N, K // Q4_K_SUB),
-            "mn": mn.reshape(N, K // Q4_K_SUB), "d": d.reshape(N, K // Q4_K_SUPER),
-            "dmin": dmin.reshape(N, K // Q4_K_SUPER)}
+    _load().oracle_q4_k_quantize(_p(W), N, K, _p(qs), _p(scales), _p(d), _p(dmin))
+    return {"qs": qs.reshape(N, K // 2), "scales": scales.reshape(N, (K // Q4_K_SUPER) * 12),
+            "d": d.reshape(N, K // Q4_K_SUPER), "dmin": dmin.reshape(N, K // Q4_K_SUPER)}
+
+
+def q4_k_pack_scales(sc, mn) -> np.ndarray:
+    """The 12 bytes holding eight 6-bit sub-block scales and offsets."""
+    sc = _c(np.asarray(sc).reshape(8), np.uint8)
+    mn = _c(np.asarray(mn).reshape(8), np.uint8)
+    out = np.zeros(12, np.uint8)
+    _load().oracle_q4_k_pack_scales(_p(sc), _p(mn), _p(out))
+    return out
+
+
+def q4_k_unpack_scales(packed):
+    """(sc [8], mn [8]) from 12 packed bytes."""
+    packed = _c(np.asarray(packed).reshape(12), np.uint8)
+    sc = np.zeros(8, np.uint8)
+    mn = np.zeros(8, np.uint8)
+    _load().oracle_q4_k_unpack_scales(_p(packed), _p(sc), _p(mn))
+    return sc, mn
+
+
+def q4_k_sub_scales(q, N: int, K: int):
+    """The planes' sub-block scales and offsets unpacked: (sc, mn), each
+    uint8 [N][K/32]."""
+    sb = K // Q4_K_SUPER
+    packed = np.asarray(q["scales"], np.uint8).reshape(N * sb, 12)
+    sc = np.zeros((N * sb, 8), np.uint8)
+    mn = np.zeros((N * sb, 8), np.uint8)
+    for i in range(N * sb):
+        sc[i], mn[i] = q4_k_unpack_scales(packed[i])
+    return sc.reshape(N, K // Q4_K_SUB), mn.reshape(N, K // Q4_K_SUB)
 
 
 def q4_k_dequantize(q, N: int, K: int) -> np.ndarray:
     """bf16 bits [N][K] of bf16(RN32(d * sc * code - dmin * mn))."""
-    planes = [_c(q["qs"], np.uint8), _c(q["sc"], np.uint8), _c(q["mn"], np.uint8),
-              _c(q["d"], np.uint16), _c(q["dmin"], np.uint16)]
+    planes = [_c(q["qs"], np.uint8), _c(q["scales"], np.uint8), _c(q["d"], np.uint16),
+              _c(q["dmin"], np.uint16)]
     W = np.zeros(N * K, np.uint16)
     _load().oracle_q4_k_dequantize(*[_p(a) for a in planes], N, K, _p(W))
     return W.reshape(N, K)

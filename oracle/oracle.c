@@ -533,8 +533,9 @@ void oracle_q8_0_dequantize(const int8_t *qs, const uint16_t *d, int64_t N, int6
 /* sub-blocks of 32. A sub-block j reads back as                          */
 /*   w = d * sc_j * q - dmin * m_j,  q in [0, 15], sc_j and m_j in [0, 63] */
 /* with d and dmin binary16 per super-block. Stored planar:               */
-/*   qs [N][K/2] (k even in the low nibble), sc and mn [N][K/32] bytes,    */
-/*   d and dmin [N][K/256] binary16 bits.                                 */
+/*   qs [N][K/2] (k even in the low nibble), scales [N][K/256][12] (the   */
+/*   eight 6-bit sc_j and m_j of a super-block, packed below), d and dmin  */
+/*   [N][K/256] binary16 bits: 4.5 bits per weight.                        */
 /* ------------------------------------------------------------------ */
 
 #define ORACLE_Q4_K_SUPER 256
@@ -602,21 +603,56 @@ static void q4_k_super_block(const uint16_t *w, uint8_t *codes, uint8_t *sc, uin
     }
 }
 
-/* W [N][K] bf16 (K a multiple of 256) -> qs [N][K/2], sc, mn [N][K/32],
- * d, dmin [N][K/256]. */
-void oracle_q4_k_quantize(const uint16_t *W, int64_t N, int64_t K, uint8_t *qs, uint8_t *sc,
-                          uint8_t *mn, uint16_t *d, uint16_t *dmin)
+/* The 8 sub-blocks' 6-bit scales sc_j and offsets m_j of a super-block in
+ * 12 bytes, the GGUF k-quant scale layout (so that a super-block takes
+ * 4 + (96 + 32) / 256 = 4.5 bits per weight): for j < 4, byte j holds sc_j
+ * and byte j + 4 holds m_j in their low 6 bits; for j >= 4, byte j + 4
+ * holds the low 4 bits of sc_j (low nibble) and of m_j (high nibble), and
+ * their top 2 bits go to the top 2 bits of bytes j - 4 (sc_j) and j (m_j). */
+void oracle_q4_k_pack_scales(const uint8_t *sc, const uint8_t *mn, uint8_t *out)
+{
+    int j;
+    for (j = 0; j < 12; ++j)
+        out[j] = 0;
+    for (j = 0; j < 4; ++j) {
+        out[j] |= (uint8_t)(sc[j] & 63);
+        out[j + 4] |= (uint8_t)(mn[j] & 63);
+    }
+    for (j = 4; j < 8; ++j) {
+        out[j + 4] = (uint8_t)((sc[j] & 15) | ((mn[j] & 15) << 4));
+        out[j - 4] |= (uint8_t)((sc[j] >> 4) << 6);
+        out[j] |= (uint8_t)((mn[j] >> 4) << 6);
+    }
+}
+
+void oracle_q4_k_unpack_scales(const uint8_t *in, uint8_t *sc, uint8_t *mn)
+{
+    int j;
+    for (j = 0; j < 4; ++j) {
+        sc[j] = (uint8_t)(in[j] & 63);
+        mn[j] = (uint8_t)(in[j + 4] & 63);
+    }
+    for (j = 4; j < 8; ++j) {
+        sc[j] = (uint8_t)((in[j + 4] & 15) | ((in[j - 4] >> 6) << 4));
+        mn[j] = (uint8_t)((in[j + 4] >> 4) | ((in[j] >> 6) << 4));
+    }
+}
+
+/* W [N][K] bf16 (K a multiple of 256) -> qs [N][K/2], scales [N][K/256][12]
+ * (packed as above), d, dmin [N][K/256]. */
+void oracle_q4_k_quantize(const uint16_t *W, int64_t N, int64_t K, uint8_t *qs,
+                          uint8_t *scales, uint16_t *d, uint16_t *dmin)
 {
     int64_t n;
 #pragma omp parallel for schedule(static)
     for (n = 0; n < N; ++n) {
         int64_t sb, k;
-        uint8_t codes[ORACLE_Q4_K_SUPER];
+        uint8_t codes[ORACLE_Q4_K_SUPER], sc[8], mn[8];
         for (sb = 0; sb < K / ORACLE_Q4_K_SUPER; ++sb) {
-            const int64_t sub = n * (K / ORACLE_Q4_K_SUB) + sb * 8;
             const int64_t sup = n * (K / ORACLE_Q4_K_SUPER) + sb;
-            q4_k_super_block(W + n * K + sb * ORACLE_Q4_K_SUPER, codes, sc + sub, mn + sub,
-                             d + sup, dmin + sup);
+            q4_k_super_block(W + n * K + sb * ORACLE_Q4_K_SUPER, codes, sc, mn, d + sup,
+                             dmin + sup);
+            oracle_q4_k_pack_scales(sc, mn, scales + 12 * sup);
             for (k = 0; k < ORACLE_Q4_K_SUPER; k += 2)
                 qs[(n * K + sb * ORACLE_Q4_K_SUPER + k) / 2] =
                     (uint8_t)(codes[k] | (codes[k + 1] << 4));
@@ -627,21 +663,23 @@ void oracle_q4_k_quantize(const uint16_t *W, int64_t N, int64_t K, uint8_t *qs, 
 /* W'[n][k] = bf16(RN32(d * sc_j * q - dmin * m_j)): d * sc_j * q (at most
  * 11 + 6 + 4 significant bits) and dmin * m_j are exact in binary32, their
  * difference is rounded once to binary32, then to bf16. */
-void oracle_q4_k_dequantize(const uint8_t *qs, const uint8_t *sc, const uint8_t *mn,
-                            const uint16_t *d, const uint16_t *dmin, int64_t N, int64_t K,
-                            uint16_t *W)
+void oracle_q4_k_dequantize(const uint8_t *qs, const uint8_t *scales, const uint16_t *d,
+                            const uint16_t *dmin, int64_t N, int64_t K, uint16_t *W)
 {
     int64_t n, k;
 #pragma omp parallel for schedule(static) private(k)
     for (n = 0; n < N; ++n)
         for (k = 0; k < K; ++k) {
-            const int64_t j = n * (K / ORACLE_Q4_K_SUB) + k / ORACLE_Q4_K_SUB;
             const int64_t t = n * (K / ORACLE_Q4_K_SUPER) + k / ORACLE_Q4_K_SUPER;
+            const int j = (int)((k % ORACLE_Q4_K_SUPER) / ORACLE_Q4_K_SUB);
+            uint8_t sc[8], mn[8];
             const uint8_t byte = qs[(n * K + k) / 2];
             const float q = (float)((k & 1) ? byte >> 4 : byte & 15);
-            const float s = half_to_float(d[t]) * (float)sc[j];
-            const float o = half_to_float(dmin[t]) * (float)mn[j];
-            const float v = s * q - o;
+            float s, o, v;
+            oracle_q4_k_unpack_scales(scales + 12 * t, sc, mn);
+            s = half_to_float(d[t]) * (float)sc[j];
+            o = half_to_float(dmin[t]) * (float)mn[j];
+            v = s * q - o;
             W[n * K + k] = double_to_bf16((double)v);
         }
 }

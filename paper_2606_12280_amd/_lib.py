@@ -45,9 +45,9 @@ SIGNATURES = {
     "q8_0_quantize": ([_P, _I64, _I64, _P, _P, _P], _S),
     "q8_0_dequantize": ([_P, _P, _I64, _I64, _P, _P], _S),
     "q8_0_linear": ([_P, _P, _P, _P, _I64, _I64, _I64, _P, _P, _P], _S),
-    "q4_k_quantize": ([_P, _I64, _I64, _P, _P, _P, _P, _P, _P], _S),
-    "q4_k_dequantize": ([_P, _P, _P, _P, _P, _I64, _I64, _P, _P], _S),
-    "q4_k_linear": ([_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P, _P, _P], _S),
+    "q4_k_quantize": ([_P, _I64, _I64, _P, _P, _P, _P, _P], _S),
+    "q4_k_dequantize": ([_P, _P, _P, _P, _I64, _I64, _P, _P], _S),
+    "q4_k_linear": ([_P, _P, _P, _P, _P, _P, _I64, _I64, _I64, _P, _P, _P], _S),
 }
 
 _lib = None

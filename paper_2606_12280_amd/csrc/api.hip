@@ -14,7 +14,7 @@
 
 namespace {
 
-constexpr int kAbiVersion = 1;
+constexpr int kAbiVersion = 2;
 constexpr int64_t kMaxRows = 1LL << 22;      // M (and N of the row kernels): grid size
 constexpr int64_t kMaxN = 1LL << 20;         // GEMM output channels: 32-bit store offsets
 constexpr int64_t kMaxMN = 1LL << 38;        // GEMM tiles: work-items below 2^32
@@ -318,51 +318,53 @@ w8a8_status q8_0_linear(const uint16_t *X, const int8_t *qs, const uint16_t *d,
 
 // Q4_K plane sizes in bytes for W [N][K].
 struct Q4kPlanes {
-    int64_t qs, sub, super;
+    int64_t qs, scales, super;
 };
-static Q4kPlanes q4_k_planes(int64_t N, int64_t K) { return {N * K / 2, N * (K / 32), 2 * N * (K / 256)}; }
+static Q4kPlanes q4_k_planes(int64_t N, int64_t K) {
+    return {N * K / 2, 12 * N * (K / 256), 2 * N * (K / 256)};
+}
 
-static w8a8_status check_q4_k_args(const uint8_t *qs, const uint8_t *sc, const uint8_t *mn,
-                            const uint16_t *d, const uint16_t *dmin, int64_t N, int64_t K) {
-    if (qs == nullptr || sc == nullptr || mn == nullptr || d == nullptr || dmin == nullptr)
+static w8a8_status check_q4_k_args(const uint8_t *qs, const uint8_t *scales, const uint16_t *d,
+                                   const uint16_t *dmin, int64_t N, int64_t K) {
+    if (qs == nullptr || scales == nullptr || d == nullptr || dmin == nullptr)
         return W8A8_ERR_NULL;
     W8A8_TRY(check_rows(N, kMaxRows));
     W8A8_TRY(check_k(K));
     if (K % 256 != 0) return W8A8_ERR_UNSUPPORTED;
-    if (!aligned(qs, 16) || !aligned(d, 2) || !aligned(dmin, 2)) return W8A8_ERR_ALIGN;
+    if (!aligned(qs, 16) || !aligned(scales, 4) || !aligned(d, 2) || !aligned(dmin, 2))
+        return W8A8_ERR_ALIGN;
     return W8A8_OK;
 }
 
-w8a8_status q4_k_quantize(const uint16_t *W, int64_t N, int64_t K, uint8_t *qs, uint8_t *sc,
-                          uint8_t *mn, uint16_t *d, uint16_t *dmin, w8a8_stream stream) {
+w8a8_status q4_k_quantize(const uint16_t *W, int64_t N, int64_t K, uint8_t *qs, uint8_t *scales,
+                          uint16_t *d, uint16_t *dmin, w8a8_stream stream) {
     if (W == nullptr) return W8A8_ERR_NULL;
-    W8A8_TRY(check_q4_k_args(qs, sc, mn, d, dmin, N, K));
+    W8A8_TRY(check_q4_k_args(qs, scales, d, dmin, N, K));
     if (!aligned(W, 16)) return W8A8_ERR_ALIGN;
     const Q4kPlanes b = q4_k_planes(N, K);
-    W8A8_TRY(check_alias({{qs, b.qs}, {sc, b.sub}, {mn, b.sub}, {d, b.super}, {dmin, b.super}},
+    W8A8_TRY(check_alias({{qs, b.qs}, {scales, b.scales}, {d, b.super}, {dmin, b.super}},
                          {{W, 2 * N * K}}));
-    return hip_status(w8a8::launch_q4_k_quantize(W, N, K, qs, sc, mn, d, dmin, as_stream(stream)));
+    return hip_status(w8a8::launch_q4_k_quantize(W, N, K, qs, scales, d, dmin, as_stream(stream)));
 }
 
-w8a8_status q4_k_dequantize(const uint8_t *qs, const uint8_t *sc, const uint8_t *mn,
-                            const uint16_t *d, const uint16_t *dmin, int64_t N, int64_t K,
-                            uint16_t *W, w8a8_stream stream) {
+w8a8_status q4_k_dequantize(const uint8_t *qs, const uint8_t *scales, const uint16_t *d,
+                            const uint16_t *dmin, int64_t N, int64_t K, uint16_t *W,
+                            w8a8_stream stream) {
     if (W == nullptr) return W8A8_ERR_NULL;
-    W8A8_TRY(check_q4_k_args(qs, sc, mn, d, dmin, N, K));
+    W8A8_TRY(check_q4_k_args(qs, scales, d, dmin, N, K));
     if (!aligned(W, 16)) return W8A8_ERR_ALIGN;
     const Q4kPlanes b = q4_k_planes(N, K);
-    W8A8_TRY(check_alias({{W, 2 * N * K}}, {{qs, b.qs}, {sc, b.sub}, {mn, b.sub}, {d, b.super},
-                                             {dmin, b.super}}));
+    W8A8_TRY(check_alias({{W, 2 * N * K}},
+                         {{qs, b.qs}, {scales, b.scales}, {d, b.super}, {dmin, b.super}}));
     return hip_status(
-        w8a8::launch_q4_k_dequantize(qs, sc, mn, d, dmin, N, K, W, as_stream(stream)));
+        w8a8::launch_q4_k_dequantize(qs, scales, d, dmin, N, K, W, as_stream(stream)));
 }
 
-w8a8_status q4_k_linear(const uint16_t *X, const uint8_t *qs, const uint8_t *sc,
-                        const uint8_t *mn, const uint16_t *d, const uint16_t *dmin,
-                        const uint16_t *bias, int64_t M, int64_t N, int64_t K, uint16_t *work,
-                        uint16_t *Y, w8a8_stream stream) {
+w8a8_status q4_k_linear(const uint16_t *X, const uint8_t *qs, const uint8_t *scales,
+                        const uint16_t *d, const uint16_t *dmin, const uint16_t *bias, int64_t M,
+                        int64_t N, int64_t K, uint16_t *work, uint16_t *Y, w8a8_stream stream) {
     if (missing(X, M) || work == nullptr || missing(Y, M)) return W8A8_ERR_NULL;
-    W8A8_TRY(check_q4_k_args(qs, sc, mn, d, dmin, N, K));
+    W8A8_TRY(check_q4_k_args(qs, scales, d, dmin, N, K));
     W8A8_TRY(check_tokens(M));
     W8A8_TRY(check_rows(N, kMaxN));
     if (M * N > kMaxMN) return W8A8_ERR_SHAPE;
@@ -370,11 +372,11 @@ w8a8_status q4_k_linear(const uint16_t *X, const uint8_t *qs, const uint8_t *sc,
         return W8A8_ERR_ALIGN;
     const Q4kPlanes b = q4_k_planes(N, K);
     W8A8_TRY(check_alias({{work, 2 * N * K}, {Y, 2 * M * N}},
-                         {{X, 2 * M * K}, {qs, b.qs}, {sc, b.sub}, {mn, b.sub}, {d, b.super},
+                         {{X, 2 * M * K}, {qs, b.qs}, {scales, b.scales}, {d, b.super},
                           {dmin, b.super}, {bias, bias ? 2 * N : 0}}));
     if (M == 0) return W8A8_OK;
     const hipStream_t s = as_stream(stream);
-    W8A8_TRY(hip_status(w8a8::launch_q4_k_dequantize(qs, sc, mn, d, dmin, N, K, work, s)));
+    W8A8_TRY(hip_status(w8a8::launch_q4_k_dequantize(qs, scales, d, dmin, N, K, work, s)));
     return hip_status(w8a8::launch_gemm_bf16(X, work, bias, M, N, K, Y, s));
 }
 

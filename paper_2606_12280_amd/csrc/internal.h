@@ -51,14 +51,16 @@ hipError_t launch_adaln_quant_act(const uint16_t *X, const uint16_t *shift,
                                   hipStream_t stream);
 
 // GGUF Q4_K (256 | K): W [N][K] bf16 -> codes qs [N][K/2] (two per byte,
-// even k low), 6-bit sub-block scales sc and offsets mn [N][K/32] (bytes),
-// binary16 super-block scales d and dmin [N][K/256]; and back to
+// even k low), the 6-bit sub-block scales and offsets packed 12 bytes per
+// super-block in scales [N][K/256][12] (4-byte aligned), binary16
+// super-block scales d and dmin [N][K/256]; and back to
 // bf16(RN32(d * sc * q - dmin * mn)).
-hipError_t launch_q4_k_quantize(const uint16_t *W, int64_t N, int64_t K, uint8_t *qs, uint8_t *sc,
-                                uint8_t *mn, uint16_t *d, uint16_t *dmin, hipStream_t stream);
-hipError_t launch_q4_k_dequantize(const uint8_t *qs, const uint8_t *sc, const uint8_t *mn,
-                                  const uint16_t *d, const uint16_t *dmin, int64_t N, int64_t K,
-                                  uint16_t *W, hipStream_t stream);
+hipError_t launch_q4_k_quantize(const uint16_t *W, int64_t N, int64_t K, uint8_t *qs,
+                                uint8_t *scales, uint16_t *d, uint16_t *dmin,
+                                hipStream_t stream);
+hipError_t launch_q4_k_dequantize(const uint8_t *qs, const uint8_t *scales, const uint16_t *d,
+                                  const uint16_t *dmin, int64_t N, int64_t K, uint16_t *W,
+                                  hipStream_t stream);
 
 // dst[k] = 0 for k < K (a fill kernel, so that the call can be captured).
 hipError_t launch_zero_f32(float *dst, int64_t K, hipStream_t stream);

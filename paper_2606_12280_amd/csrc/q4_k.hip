@@ -13,11 +13,15 @@
 //   3. s_j = d * sc_j and o_j = dmin * m_j (exact),
 //      q = clamp(rint((w + o_j) * RN32(1/s_j)), 0, 15)   (0 where s_j = 0).
 // A weight reads back as bf16(RN32(s_j * q - o_j)) (s_j * q is exact).
-// Stored planar: qs [N][K/2] (even k in the low nibble), sc and mn
-// [N][K/32] bytes, d and dmin [N][K/256] binary16: 4.625 bits per weight.
+// Stored planar: qs [N][K/2] (even k in the low nibble), scales
+// [N][K/256][12] (a super-block's eight 6-bit sc_j and m_j in the GGUF
+// k-quant scale layout: for j < 4 bytes j and j + 4 hold sc_j and m_j in
+// their low 6 bits; for j >= 4 byte j + 4 holds the low nibbles of sc_j and
+// m_j, and their top two bits sit at the top of bytes j - 4 and j), d and
+// dmin [N][K/256] binary16: 4 + (96 + 32) / 256 = 4.5 bits per weight.
 //
 // Dequantize is an HBM-bound stream: per weight 1/2 byte of codes and 1/16
-// of 6-bit planes in, 2 bytes of bf16 out.
+// byte of scales in, 2 bytes of bf16 out.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -64,12 +68,18 @@ __device__ __forceinline__ float group8_max(float v) {
     return v;
 }
 
+__device__ __forceinline__ uint32_t group8_or(uint32_t v) {
+#pragma unroll
+    for (int m = 1; m < kSubs; m <<= 1) v |= __shfl_xor(v, m, 64);
+    return v;
+}
+
 // One thread per sub-block; the 8 threads of a super-block are 8
-// consecutive lanes and agree on d and dmin through lane shuffles.
+// consecutive lanes, agree on d and dmin through lane shuffles, and OR
+// their 6-bit values into the super-block's 12 scale bytes.
 __global__ __launch_bounds__(256) void q4_k_quantize_kernel(
     const uint16_t *__restrict__ W, int64_t subs, uint8_t *__restrict__ qs,
-    uint8_t *__restrict__ sc, uint8_t *__restrict__ mn, uint16_t *__restrict__ d,
-    uint16_t *__restrict__ dmin) {
+    uint32_t *__restrict__ scales, uint16_t *__restrict__ d, uint16_t *__restrict__ dmin) {
     const int64_t j = unit_index();
     // subs is a multiple of 8 and groups of 8 lanes are aligned, so a
     // super-block's lanes are either all in range or all out.
@@ -107,8 +117,29 @@ __global__ __launch_bounds__(256) void q4_k_quantize_kernel(
     const float inv_dm = fdm != 0.0f ? 1.0f / fdm : 0.0f;
     const float cs = fminf(rintf(a * inv_d), 63.0f);
     const float cm = fminf(rintf(b * inv_dm), 63.0f);
-    sc[j] = static_cast<uint8_t>(cs);
-    mn[j] = static_cast<uint8_t>(cm);
+    {
+        const uint32_t vs = static_cast<uint32_t>(cs), vm = static_cast<uint32_t>(cm);
+        const int jj = static_cast<int>(j & (kSubs - 1));
+        const int sh = 8 * (jj & 3);
+        uint32_t w0, w1, w2 = 0u;  // scale bytes 0-3, 4-7, 8-11
+        if (jj < 4) {
+            w0 = vs << sh;
+            w1 = vm << sh;
+        } else {
+            w0 = (vs >> 4) << (sh + 6);
+            w1 = (vm >> 4) << (sh + 6);
+            w2 = ((vs & 15u) | ((vm & 15u) << 4)) << sh;
+        }
+        w0 = group8_or(w0);
+        w1 = group8_or(w1);
+        w2 = group8_or(w2);
+        if (jj == 0) {
+            uint32_t *o = scales + 3 * (j / kSubs);
+            o[0] = w0;
+            o[1] = w1;
+            o[2] = w2;
+        }
+    }
     const float s = fd * cs, o = fdm * cm;
     const float inv = s != 0.0f ? 1.0f / s : 0.0f;
     uint32_t packed[4] = {0, 0, 0, 0};
@@ -120,19 +151,30 @@ __global__ __launch_bounds__(256) void q4_k_quantize_kernel(
     reinterpret_cast<uint4 *>(qs)[j] = make_uint4(packed[0], packed[1], packed[2], packed[3]);
 }
 
-// One thread per 8 weights: 4 bytes of codes, the sub-block's two 6-bit
-// values and the super-block's two scales in, 16 bytes of bf16 out, so a
-// wave's stores cover 1 KiB contiguously.
+// One thread per 8 weights: 4 bytes of codes, the super-block's 12 scale
+// bytes and two scales in, 16 bytes of bf16 out, so a wave's stores cover
+// 1 KiB contiguously.
 __global__ __launch_bounds__(256) void q4_k_dequantize_kernel(
-    const uint32_t *__restrict__ qs, const uint8_t *__restrict__ sc,
-    const uint8_t *__restrict__ mn, const uint16_t *__restrict__ d,
-    const uint16_t *__restrict__ dmin, int64_t octets, u32x4 *__restrict__ W) {
+    const uint32_t *__restrict__ qs, const uint32_t *__restrict__ scales,
+    const uint16_t *__restrict__ d, const uint16_t *__restrict__ dmin, int64_t octets,
+    u32x4 *__restrict__ W) {
     const int64_t t = unit_index();
     if (t >= octets) return;
-    const int64_t j = t >> 2;  // sub-block (4 octets each)
-    const int64_t g = t >> 5;  // super-block (32 octets each)
-    const float s = half_bits_to_float(d[g]) * static_cast<float>(sc[j]);
-    const float o = half_bits_to_float(dmin[g]) * static_cast<float>(mn[j]);
+    const int jj = static_cast<int>((t >> 2) & (kSubs - 1));  // sub-block in its super-block
+    const int64_t g = t >> 5;                                    // super-block (32 octets)
+    const uint32_t w0 = scales[3 * g], w1 = scales[3 * g + 1], w2 = scales[3 * g + 2];
+    const int sh = 8 * (jj & 3);
+    uint32_t vs, vm;
+    if (jj < 4) {
+        vs = (w0 >> sh) & 63u;
+        vm = (w1 >> sh) & 63u;
+    } else {
+        const uint32_t lo = (w2 >> sh) & 255u;
+        vs = (lo & 15u) | (((w0 >> (sh + 6)) & 3u) << 4);
+        vm = (lo >> 4) | (((w1 >> (sh + 6)) & 3u) << 4);
+    }
+    const float s = half_bits_to_float(d[g]) * static_cast<float>(vs);
+    const float o = half_bits_to_float(dmin[g]) * static_cast<float>(vm);
     const uint32_t q = __builtin_nontemporal_load(qs + t);
     uint32_t out[4];
 #pragma unroll
@@ -154,20 +196,22 @@ dim3 grid_for(int64_t n) {
 
 }  // namespace
 
-hipError_t launch_q4_k_quantize(const uint16_t *W, int64_t N, int64_t K, uint8_t *qs, uint8_t *sc,
-                                uint8_t *mn, uint16_t *d, uint16_t *dmin, hipStream_t stream) {
+hipError_t launch_q4_k_quantize(const uint16_t *W, int64_t N, int64_t K, uint8_t *qs,
+                                uint8_t *scales, uint16_t *d, uint16_t *dmin,
+                                hipStream_t stream) {
     const int64_t subs = N * (K / kSub);
     hipLaunchKernelGGL(q4_k_quantize_kernel, grid_for(subs), dim3(256), 0, stream, W, subs,
-                       qs, sc, mn, d, dmin);
+                       qs, reinterpret_cast<uint32_t *>(scales), d, dmin);
     return hipGetLastError();
 }
 
-hipError_t launch_q4_k_dequantize(const uint8_t *qs, const uint8_t *sc, const uint8_t *mn,
-                                  const uint16_t *d, const uint16_t *dmin, int64_t N, int64_t K,
-                                  uint16_t *W, hipStream_t stream) {
+hipError_t launch_q4_k_dequantize(const uint8_t *qs, const uint8_t *scales, const uint16_t *d,
+                                  const uint16_t *dmin, int64_t N, int64_t K, uint16_t *W,
+                                  hipStream_t stream) {
     const int64_t octets = N * K / 8;
     hipLaunchKernelGGL(q4_k_dequantize_kernel, grid_for(octets), dim3(256), 0, stream,
-                       reinterpret_cast<const uint32_t *>(qs), sc, mn, d, dmin, octets,
+                       reinterpret_cast<const uint32_t *>(qs),
+                       reinterpret_cast<const uint32_t *>(scales), d, dmin, octets,
                        reinterpret_cast<u32x4 *>(W));
     return hipGetLastError();
 }

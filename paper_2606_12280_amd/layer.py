@@ -65,7 +65,7 @@ def prepare_q8_0(W: torch.Tensor, bias: torch.Tensor | None) -> PreparedLinear:
 
 def prepare_q4_k(W: torch.Tensor, bias: torch.Tensor | None) -> PreparedLinear:
     """Encode W once (offline) as GGUF Q4_K: 4-bit codes in super-blocks of
-    256 (4.625 bits per weight in the planar layout)."""
+    256 (4.5 bits per weight)."""
     N, K = W.shape
     return PreparedLinear(False, N, K, bias, q4k=ops.q4_k_quantize(W))
 

@@ -314,13 +314,14 @@ Q4_K_SUB = 32
 
 class Q4K:
     """The planes of a Q4_K weight [N, K]: qs uint8 [N, K/2] (two 4-bit codes
-    per byte, even k low), sc and mn uint8 [N, K/32] (6-bit sub-block scales
-    and offsets), d and dmin float16 [N, K/256] (super-block scales)."""
+    per byte, even k low), scales uint8 [N, K/256 * 12] (each super-block's
+    eight 6-bit sub-block scales and offsets, packed), d and dmin float16
+    [N, K/256] (super-block scales): 4.5 bits per weight."""
 
-    __slots__ = ("qs", "sc", "mn", "d", "dmin")
+    __slots__ = ("qs", "scales", "d", "dmin")
 
-    def __init__(self, qs, sc, mn, d, dmin):
-        self.qs, self.sc, self.mn, self.d, self.dmin = qs, sc, mn, d, dmin
+    def __init__(self, qs, scales, d, dmin):
+        self.qs, self.scales, self.d, self.dmin = qs, scales, d, dmin
 
     @property
     def shape(self) -> tuple[int, int]:
@@ -328,14 +329,13 @@ class Q4K:
 
     @property
     def nbytes(self) -> int:
-        return sum(t.numel() * t.element_size() for t in (self.qs, self.sc, self.mn, self.d, self.dmin))
+        return sum(t.numel() * t.element_size() for t in (self.qs, self.scales, self.d, self.dmin))
 
     def check(self, device=None) -> tuple[int, int]:
         _need(self.qs, "qs", torch.uint8, 2, device)
         N, K = self.shape
         dev = self.qs.device
-        for name, t, dt, cols in (("sc", self.sc, torch.uint8, K // Q4_K_SUB),
-                                  ("mn", self.mn, torch.uint8, K // Q4_K_SUB),
+        for name, t, dt, cols in (("scales", self.scales, torch.uint8, K // Q4_K_SUPER * 12),
                                   ("d", self.d, torch.float16, K // Q4_K_SUPER),
                                   ("dmin", self.dmin, torch.float16, K // Q4_K_SUPER)):
             _need(t, name, dt, 2, dev)
@@ -344,7 +344,7 @@ class Q4K:
         return N, K
 
     def ptrs(self):
-        return [_ptr(t) for t in (self.qs, self.sc, self.mn, self.d, self.dmin)]
+        return [_ptr(t) for t in (self.qs, self.scales, self.d, self.dmin)]
 
 
 def q4_k_quantize(W: torch.Tensor) -> Q4K:
@@ -353,8 +353,7 @@ def q4_k_quantize(W: torch.Tensor) -> Q4K:
     N, K = W.shape
     dev = W.device
     q = Q4K(torch.empty(N, K // 2, dtype=torch.uint8, device=dev),
-            torch.empty(N, K // Q4_K_SUB, dtype=torch.uint8, device=dev),
-            torch.empty(N, K // Q4_K_SUB, dtype=torch.uint8, device=dev),
+            torch.empty(N, K // Q4_K_SUPER * 12, dtype=torch.uint8, device=dev),
             torch.empty(N, K // Q4_K_SUPER, dtype=torch.float16, device=dev),
             torch.empty(N, K // Q4_K_SUPER, dtype=torch.float16, device=dev))
     lib = load()
@@ -364,7 +363,7 @@ def q4_k_quantize(W: torch.Tensor) -> Q4K:
 
 
 def q4_k_dequantize(q: Q4K, out: torch.Tensor | None = None) -> torch.Tensor:
-    """bf16(d * sc * code - dmin * mn) as bf16 [N, K]."""
+    """bf16(d * sc * code - dmin * m) as bf16 [N, K]."""
     N, K = q.check()
     dev = q.qs.device
     W = _out(out, (N, K), torch.bfloat16, dev, "out")

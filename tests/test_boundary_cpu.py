@@ -47,7 +47,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.w8a8_abi_version() == 1
+    assert lib.w8a8_abi_version() == 2
     for s in range(7):
         assert lib.w8a8_status_string(s)
     assert lib.w8a8_status_string(99) == b"unknown status"
@@ -119,8 +119,8 @@ def test_empty_token_batch_is_a_no_op(lib):
     assert lib.bf16_linear(None, B, None, 0, 8, 0, None, None) == SHAPE
     assert lib.q8_0_linear(None, B, C, None, 0, 8, 64, D, None, None) == OK
     assert lib.q8_0_linear(None, B, C, None, 0, 8, 64, None, None, None) == NULL
-    assert lib.q4_k_linear(None, B, C, D, E, F, None, 0, 8, 256, G, None, None) == OK
-    assert lib.q4_k_linear(None, B, C, D, E, F, None, 0, 8, 128, G, None, None) == UNSUP
+    assert lib.q4_k_linear(None, B, C, D, E, None, 0, 8, 256, G, None, None) == OK
+    assert lib.q4_k_linear(None, B, C, D, E, None, 0, 8, 128, G, None, None) == UNSUP
     assert lib.w8a8_gemm_config(0, 8, 64, 0, None, None, None) == NULL
 
 
@@ -228,29 +228,32 @@ def test_q8_0_validation(lib):
 
 def test_q4_k_validation(lib):
     q = lib.q4_k_quantize
-    assert q(None, 8, 256, B, C, D, E, F, None) == NULL
-    assert q(A, 8, 256, B, C, D, E, None, None) == NULL
-    assert q(A, 0, 256, B, C, D, E, F, None) == SHAPE
-    assert q(A, 8, 128, B, C, D, E, F, None) == UNSUP          # K % 256 != 0
-    assert q(A, 8, 96, B, C, D, E, F, None) == UNSUP
-    assert q(A + 2, 8, 256, B, C, D, E, F, None) == ALIGN
-    assert q(A, 8, 256, B + 8, C, D, E, F, None) == ALIGN       # codes
-    assert q(A, 8, 256, B, C, D, E + 1, F, None) == ALIGN       # d
-    assert q(A, 8, 256, A + 64, C, D, E, F, None) == ALIAS      # codes inside W
-    assert q(A, 8, 256, B, B + 512, D, E, F, None) == ALIAS     # sc inside the codes (1 KiB)
-    assert q(A, 8, 256, B, C, C + 32, E, F, None) == ALIAS      # mn inside sc (64 B)
-    assert q(A, 8, 256, B, C, D, E, E + 8, None) == ALIAS       # dmin inside d (16 B)
+    assert q(None, 8, 256, B, C, D, E, None) == NULL
+    assert q(A, 8, 256, B, C, D, None, None) == NULL
+    assert q(A, 8, 256, B, None, D, E, None) == NULL
+    assert q(A, 0, 256, B, C, D, E, None) == SHAPE
+    assert q(A, 8, 128, B, C, D, E, None) == UNSUP          # K % 256 != 0
+    assert q(A, 8, 96, B, C, D, E, None) == UNSUP
+    assert q(A + 2, 8, 256, B, C, D, E, None) == ALIGN
+    assert q(A, 8, 256, B + 8, C, D, E, None) == ALIGN       # codes
+    assert q(A, 8, 256, B, C + 2, D, E, None) == ALIGN       # packed scales
+    assert q(A, 8, 256, B, C, D + 1, E, None) == ALIGN       # d
+    assert q(A, 8, 256, A + 64, C, D, E, None) == ALIAS      # codes inside W
+    assert q(A, 8, 256, B, B + 1020, D, E, None) == ALIAS    # scales overlap the codes (1 KiB)
+    assert q(A, 8, 256, B, C, C + 92, E, None) == ALIAS      # d overlaps the scales (96 B)
+    assert q(A, 8, 256, B, C, D, D + 8, None) == ALIAS       # dmin inside d (16 B)
+    assert q(A, 8, 256, B, C, D, D + 16, None) != ALIAS      # dmin right after d
     dq = lib.q4_k_dequantize
-    assert dq(A, B, C, D, E, 8, 256, None, None) == NULL
-    assert dq(A, B, C, D, E, 8, 256, A + 16, None) == ALIAS
-    assert dq(A, B, C, D, E, 8, 256, F + 8, None) == ALIGN
+    assert dq(A, B, C, D, 8, 256, None, None) == NULL
+    assert dq(A, B, C, D, 8, 256, A + 16, None) == ALIAS
+    assert dq(A, B, C, D, 8, 256, F + 8, None) == ALIGN
     f = lib.q4_k_linear
-    assert f(A, B, C, D, E, F, None, 4, 8, 256, G, None, None) == NULL
-    assert f(A, B, C, D, E, F, None, 4, 8, 256, None, G, None) == NULL
-    assert f(A, B, C, D, E, F, None, 4, 8, 256, G, G, None) == ALIAS     # Y inside work
-    assert f(A, B, C, D, E, F, None, 4, 8, 256, B, G, None) == ALIAS     # work over the codes
-    assert f(A, B, C, D, E, F, None, 4, 8, 512 + 64, G, 0x7F0700000000, None) == UNSUP
-    assert f(A, B, C, D, E, F, None, -1, 8, 256, G, 0x7F0700000000, None) == SHAPE
+    assert f(A, B, C, D, E, None, 4, 8, 256, G, None, None) == NULL
+    assert f(A, B, C, D, E, None, 4, 8, 256, None, G, None) == NULL
+    assert f(A, B, C, D, E, None, 4, 8, 256, G, G, None) == ALIAS     # Y inside work
+    assert f(A, B, C, D, E, None, 4, 8, 256, B, G, None) == ALIAS     # work over the codes
+    assert f(A, B, C, D, E, None, 4, 8, 512 + 64, G, 0x7F0700000000, None) == UNSUP
+    assert f(A, B, C, D, E, None, -1, 8, 256, G, 0x7F0700000000, None) == SHAPE
 
 
 def test_adaln_validation(lib):

@@ -566,13 +566,13 @@ def _q4k_case(seed, N, K):
 
 
 def _q4k_host(q):
-    return {"qs": host(q.qs), "sc": host(q.sc), "mn": host(q.mn),
+    return {"qs": host(q.qs), "scales": host(q.scales),
             "d": host(q.d).view(np.uint16), "dmin": host(q.dmin).view(np.uint16)}
 
 
 def _check_q4k_planes(q, ref):
     got = _q4k_host(q)
-    for name in ("qs", "sc", "mn", "d", "dmin"):
+    for name in ("qs", "scales", "d", "dmin"):
         assert np.array_equal(got[name], ref[name]), name
 
 
@@ -623,12 +623,13 @@ def test_q4_k_decode_of_arbitrary_planes():
     value and a wide range of binary16 scales) matches the oracle."""
     rng = np.random.default_rng(161)
     N, K = 16, 1024
+    packed = np.stack([oracle.q4_k_pack_scales(rng.integers(0, 64, 8), rng.integers(0, 64, 8))
+                       for _ in range(N * K // 256)])
     ref = {"qs": rng.integers(0, 256, (N, K // 2)).astype(np.uint8),
-           "sc": rng.integers(0, 64, (N, K // 32)).astype(np.uint8),
-           "mn": rng.integers(0, 64, (N, K // 32)).astype(np.uint8),
+           "scales": packed.reshape(N, K // 256 * 12),
            "d": rng.lognormal(-6, 3, (N, K // 256)).astype(np.float16).view(np.uint16),
            "dmin": rng.lognormal(-6, 3, (N, K // 256)).astype(np.float16).view(np.uint16)}
-    q = ops.Q4K(dev(ref["qs"]), dev(ref["sc"]), dev(ref["mn"]),
+    q = ops.Q4K(dev(ref["qs"]), dev(ref["scales"]),
                 dev(ref["d"].view(np.float16)), dev(ref["dmin"].view(np.float16)))
     assert np.array_equal(host_bits(ops.q4_k_dequantize(q)), oracle.q4_k_dequantize(ref, N, K))
 

@@ -71,7 +71,11 @@ MUTANTS = {
     "q4_k_super_scale_over_64": ("*d = float_to_half(cap_half(amax / 63.0f));", "*d = float_to_half(cap_half(amax / 64.0f));"),
     "q4_k_step_over_16": ("a[j] = (hi - lo) / 15.0f;", "a[j] = (hi - lo) / 16.0f;"),
     "q4_k_min_not_clamped_to_zero": ("float lo = 0.0f, hi = -INFINITY;", "float lo = INFINITY, hi = -INFINITY;"),
-    "q4_k_decode_drops_offset": ("const float v = s * q - o;", "const float v = s * q;"),
+    "q4_k_pack_high_bits_shift": ("out[j - 4] |= (uint8_t)((sc[j] >> 4) << 6);",
+                                  "out[j - 4] |= (uint8_t)((sc[j] >> 2) << 6);"),
+    "q4_k_unpack_offset_nibble": ("mn[j] = (uint8_t)((in[j + 4] >> 4) | ((in[j] >> 6) << 4));",
+                                  "mn[j] = (uint8_t)((in[j + 4] & 15) | ((in[j] >> 6) << 4));"),
+    "q4_k_decode_drops_offset": ("v = s * q - o;", "v = s * q;"),
     "q4_k_no_code_clamp": ("            if (c > 15.0f)\n                c = 15.0f;\n", ""),
     "adaln_sample_variance": ("rstd = 1.0 / sqrt(ss / (double)K + eps);", "rstd = 1.0 / sqrt(ss / (double)(K - 1) + eps);"),
     "adaln_eps_outside_root": ("rstd = 1.0 / sqrt(ss / (double)K + eps);", "rstd = 1.0 / (sqrt(ss / (double)K) + eps);"),
@@ -125,6 +129,7 @@ PINS = [
     pins.test_adaln_matches_torch_layer_norm_fp64,
     pins.test_adaln_special_rows_and_modulation,
     pins.test_adaln_eps_enters_under_the_root,
+    pins.test_q4_k_scale_packing,
     pins.test_q4_k_exact_grid_round_trip,
     pins.test_q4_k_codes_are_nearest_on_the_stored_grid,
     pins.test_q4_k_error_bound_and_scale_ranges,

@@ -634,9 +634,61 @@ def test_q8_0_linear_against_numpy_fp64():
 # offsets under binary16 super-block scales)
 # --------------------------------------------------------------------------
 
+def _pack_k4(sc, mn):
+    """Test-side packer of the 12-byte k-quant scale layout, written from its
+    definition: for j < 4, byte j = sc_j and byte j + 4 = m_j (low 6 bits);
+    for j >= 4, byte j + 4 = (sc_j & 15) | (m_j & 15) << 4, and the top two
+    bits of sc_j and m_j go to the top of bytes j - 4 and j. sc, mn are
+    [..., 8]; returns [..., 12]."""
+    sc = np.asarray(sc, np.uint32)
+    mn = np.asarray(mn, np.uint32)
+    out = np.zeros(sc.shape[:-1] + (12,), np.uint32)
+    out[..., 0:4] = (sc[..., 0:4] & 63) | ((sc[..., 4:8] >> 4) << 6)
+    out[..., 4:8] = (mn[..., 0:4] & 63) | ((mn[..., 4:8] >> 4) << 6)
+    out[..., 8:12] = (sc[..., 4:8] & 15) | ((mn[..., 4:8] & 15) << 4)
+    return out.astype(np.uint8)
+
+
+def _unpack_k4(packed):
+    """Inverse of _pack_k4: [..., 12] -> (sc [..., 8], mn [..., 8])."""
+    b = np.asarray(packed, np.uint32)
+    sc = np.concatenate([b[..., 0:4] & 63, (b[..., 8:12] & 15) | ((b[..., 0:4] >> 6) << 4)], -1)
+    mn = np.concatenate([b[..., 4:8] & 63, (b[..., 8:12] >> 4) | ((b[..., 4:8] >> 6) << 4)], -1)
+    return sc.astype(np.uint8), mn.astype(np.uint8)
+
+
+def _sub_planes(q, N, K):
+    """q with its packed scales unpacked (test-side) into sc, mn [N][K/32]."""
+    sc, mn = _unpack_k4(np.asarray(q["scales"]).reshape(N, K // 256, 12))
+    return dict(q, sc=sc.reshape(N, K // 32), mn=mn.reshape(N, K // 32))
+
+
+def test_q4_k_scale_packing():
+    """The oracle's 12-byte packing of eight 6-bit scales and offsets against
+    a worked example (bytes derived by hand from the layout) and against the
+    test-side packer on random values; round trip; 4.5 bits per weight."""
+    sc, mn = [1, 2, 3, 4, 48, 49, 50, 63], [5, 6, 7, 8, 33, 17, 62, 0]
+    want = [193, 194, 195, 196, 133, 70, 199, 8, 16, 17, 226, 15]
+    assert oracle.q4_k_pack_scales(sc, mn).tolist() == want
+    assert _pack_k4(np.array(sc), np.array(mn)).tolist() == want
+    got_sc, got_mn = oracle.q4_k_unpack_scales(np.array(want, np.uint8))
+    assert got_sc.tolist() == sc and got_mn.tolist() == mn
+    rng = np.random.default_rng(156)
+    for _ in range(200):
+        a, b = rng.integers(0, 64, 8), rng.integers(0, 64, 8)
+        p = oracle.q4_k_pack_scales(a, b)
+        assert np.array_equal(p, _pack_k4(a, b))
+        ua, ub = _unpack_k4(p)
+        assert np.array_equal(ua, a) and np.array_equal(ub, b)
+    q = oracle.q4_k_quantize(synth.rand_bf16(157, (3, 512), 0.02), 3, 512)
+    bits = 8 * sum(q[k].nbytes for k in ("qs", "scales", "d", "dmin"))
+    assert bits == 4.5 * 3 * 512
+
+
 def _q4_k_grid(q, N, K):
     """Per-weight step s = d*sc and offset o = dmin*mn, and the codes, as
     float64 arrays [N][K] (from the stored planes, not from the weights)."""
+    q = _sub_planes(q, N, K)
     rep_sub = lambda a: np.repeat(a.astype(np.float64), 32, axis=1)
     rep_sup = lambda a: np.repeat(_f16(a).astype(np.float64), 256, axis=1)
     s = rep_sup(q["d"]) * rep_sub(q["sc"])
@@ -683,7 +735,7 @@ def test_q4_k_exact_grid_round_trip():
                 want_q[n, col:col + 32] = codes
     B = synth.to_bf16_bits(W)
     assert np.array_equal(bf16_to_f64(B).reshape(N, K), W.astype(np.float64))
-    q = oracle.q4_k_quantize(B, N, K)
+    q = _sub_planes(oracle.q4_k_quantize(B, N, K), N, K)
     assert np.all(_f16(q["d"]) == h) and np.all(_f16(q["dmin"]) == h)
     assert np.array_equal(q["sc"], want_sc) and np.array_equal(q["mn"], want_mn)
     assert np.array_equal(q["qs"], (want_q[:, 0::2] | (want_q[:, 1::2] << 4)).astype(np.uint8))
@@ -724,7 +776,7 @@ def test_q4_k_error_bound_and_scale_ranges():
     floor in place of round-to-nearest for the 6-bit scales and offsets."""
     N, K = 64, 1024
     B = _q4_k_random_weights(152, N, K)
-    q = oracle.q4_k_quantize(B, N, K)
+    q = _sub_planes(oracle.q4_k_quantize(B, N, K), N, K)
     s, o, _ = _q4_k_grid(q, N, K)
     w = bf16_to_f64(B).reshape(N, K)
     r = bf16_to_f64(oracle.q4_k_dequantize(q, N, K)).reshape(N, K)
@@ -748,7 +800,7 @@ def test_q4_k_grid_spans_each_sub_block():
     6-bit offsets or scales down instead of to nearest."""
     N, K = 64, 1024
     B = _q4_k_random_weights(155, N, K)
-    q = oracle.q4_k_quantize(B, N, K)
+    q = _sub_planes(oracle.q4_k_quantize(B, N, K), N, K)
     w = bf16_to_f64(B).reshape(N, K // 32, 32)
     lo = np.minimum(w.min(axis=2), 0.0)
     span = (w.max(axis=2) - lo) / 15
@@ -773,7 +825,7 @@ def test_q4_k_special_blocks():
     W[0, 512] = 3.0e9
     W[0, 513] = -1.0e6
     B = synth.to_bf16_bits(W)
-    q = oracle.q4_k_quantize(B, 1, 768)
+    q = _sub_planes(oracle.q4_k_quantize(B, 1, 768), 1, 768)
     r = bf16_to_f64(oracle.q4_k_dequantize(q, 1, 768))[0]
     assert q["d"][0, 0] == 0 and q["dmin"][0, 0] == 0
     assert not q["sc"][0, :8].any() and not q["mn"][0, :8].any() and not q["qs"][0, :128].any()
@@ -790,9 +842,10 @@ def test_q4_k_dequantize_is_binary32_then_bf16():
     import torch
     rng = np.random.default_rng(153)
     N, K = 4, 512
+    sc = rng.integers(0, 64, (N, K // 256, 8))
+    mn = rng.integers(0, 64, (N, K // 256, 8))
     q = {"qs": rng.integers(0, 256, (N, K // 2)).astype(np.uint8),
-         "sc": rng.integers(0, 64, (N, K // 32)).astype(np.uint8),
-         "mn": rng.integers(0, 64, (N, K // 32)).astype(np.uint8),
+         "scales": _pack_k4(sc, mn).reshape(N, K // 256 * 12),
          "d": np.array([[oracle.float_to_half(float(v)) for v in rng.lognormal(-7, 2, K // 256)]
                         for _ in range(N)], np.uint16),
          "dmin": np.array([[oracle.float_to_half(float(v)) for v in rng.lognormal(-7, 2, K // 256)]

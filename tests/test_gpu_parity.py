@@ -276,6 +276,43 @@ def test_w8a8_linear_large_ragged(M, N, K, with_bias):
     check_w8a8_output(host_bits(Y), Yref, acc, xs, ws, b)
 
 
+# Shapes that take the persistent 288 x 256 kernel (more tiles than CUs, N a
+# multiple of 8, at least three 128-byte K tiles): ragged M with the fewest
+# K tiles it runs (3), a tile count between one and two rounds (418 tiles,
+# ragged in both M and N: some workgroups walk two tiles, the others one),
+# and a long row of tiles.
+PERSISTENT_SHAPES = [(4571, 16376, 384), (3163, 9720, 1024), (2000, 16384, 512),
+                     (576, 131072, 384)]
+
+
+@pytest.mark.parametrize("M,N,K", PERSISTENT_SHAPES)
+def test_persistent_gemm_whole_outputs(M, N, K):
+    """The persistent kernel on whole outputs: int32 accumulators bit-exact,
+    the dequantizing epilogue with and without a bias within tolerance, and
+    bf16_linear (also persistent here) within its bound on sampled rows."""
+    assert ops.w8a8_gemm_config(M, N, K) == (288, 256, 768)
+    A = synth.rand_i8([120, M, K], (M, K))
+    B = synth.rand_i8([121, N, K], (N, K))
+    acc = oracle.gemm_i32(A, B, M, N, K)
+    Ad, Bd = dev(A), dev(B)
+    assert np.array_equal(host(ops.w8a8_gemm_i32(Ad, Bd)), acc)
+    rng = np.random.default_rng([122, M, N, K])
+    xs = rng.uniform(1e-3, 1e-1, M).astype(np.float32)
+    ws = rng.uniform(1e-4, 1e-2, N).astype(np.float32)
+    b = synth.rand_bf16([123, N], (N,), 0.5)
+    zero = np.zeros(N, np.uint16)
+    Y = host_bits(ops.w8a8_linear(Ad, dev(xs), Bd, dev(ws), dev_bf16(b)))
+    check_w8a8_output(Y, oracle.epilogue(acc, xs, ws, b, M, N), acc, xs, ws, b)
+    Y0 = host_bits(ops.w8a8_linear(Ad, dev(xs), Bd, dev(ws), None))
+    check_w8a8_output(Y0, oracle.epilogue(acc, xs, ws, zero, M, N), acc, xs, ws, zero)
+    del acc, Y, Y0
+    c = synth.linear_case([124, M, N, K], M, N, K)
+    Yb = host_bits(ops.bf16_linear(dev_bf16(c["X"]), dev_bf16(c["W"]), dev_bf16(c["bias"])))
+    rows = np.unique(np.concatenate([[0, M - 1], np.arange(0, M, 288),
+                                     rng.choice(M, min(M, 32), replace=False)]))
+    check_bf16_output(Yb[rows], c["X"].reshape(M, K)[rows], c["W"].reshape(N, K), c["bias"])
+
+
 @pytest.mark.parametrize("K", [16384, 65536])
 def test_gemm_i32_extremes(K):
     """All +-127 codes: |acc| = 127^2 K, the largest sum (1.06e9 at the

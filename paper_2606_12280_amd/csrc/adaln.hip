@@ -15,14 +15,15 @@
 // X is read once and the codes written once; run apart, the two steps would
 // also write h and read it back (2 bytes each per element).
 //
-// Work mapping as in the quant kernel: a group of G waves owns a row, each
-// lane CH chunks of 8 columns (consecutive lanes on consecutive 16-byte
-// chunks), with its 8*CH smoothing multipliers and modulation values (as
-// binary64) kept in registers across the RPW rows it walks; with RPW > 1 the
-// next row is prefetched. The three row reductions (sum, centered sum of
-// squares, absmax) run as lane butterflies, then across the G waves through
-// LDS. The binary64 arithmetic (half the binary32 rate) bounds the kernel,
-// not its bytes.
+// Work mapping: a group of G waves owns a row, each lane CH chunks of 8
+// columns (consecutive lanes on consecutive 16-byte chunks), with its 8*CH
+// smoothing multipliers and modulation values (as binary64) kept in
+// registers across the rows it walks. One launch holds as many groups as the
+// GPU keeps resident, each walking an equal share of the rows with the next
+// row prefetched. The three row reductions (sum, centered sum of squares,
+// absmax) run as lane butterflies, then across the G waves through LDS. The
+// vector ALU bounds the kernel, not its bytes: about 30 instructions per
+// element, a third of them binary64.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -41,14 +42,34 @@ typedef unsigned int v2u __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-__device__ __forceinline__ uint4 load_stream(const uint4 *p) {
-    const v4u v = __builtin_nontemporal_load(reinterpret_cast<const v4u *>(p));
+// Row loads and stores go through raw buffer instructions with a per-row
+// resource: a lane whose chunk lies past the row, or a row past the input,
+// falls outside the resource's range, so the hardware reads zeros and drops
+// the store. Every wave then issues the same memory instructions for every
+// row, with no branch around them, which lets the compiler count them
+// exactly and wait for the current row's loads only, not the prefetched
+// next row's. (nt: streamed, not kept in the caches.)
+constexpr int kBufferWord3 = 0x00020000;  // raw buffer, 32-bit data format
+constexpr int kNontemporal = 2;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, static_cast<int>(bytes),
+                                             kBufferWord3);
+}
+
+__device__ __forceinline__ int wave_index() {
+    return __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+}
+
+__device__ __forceinline__ uint4 load_chunk(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    const v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNontemporal);
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-__device__ __forceinline__ void store_stream(uint2 *p, uint32_t lo, uint32_t hi) {
+__device__ __forceinline__ void store_codes(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t lo,
+                                            uint32_t hi) {
     const v2u v = {lo, hi};
-    __builtin_nontemporal_store(v, reinterpret_cast<v2u *>(p));
+    __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, kNontemporal);
 }
 
 // The 8 bf16 values of a chunk, widened (exactly).
@@ -89,24 +110,37 @@ __device__ __forceinline__ uint32_t bf16_bits_past_midpoint(double d, float f) {
 __device__ __forceinline__ double wave_sum(double v) { return lanes::sum(v); }
 __device__ __forceinline__ float wave_max(float v) { return lanes::max(v); }
 
-__device__ __forceinline__ uint32_t code(float v, float r) {
-    float c = rintf(v * r);
-    c = fminf(fmaxf(c, -127.0f), 127.0f);
-    return static_cast<uint32_t>(static_cast<int32_t>(c)) & 0xffu;
+// The code of v at multiplier r, clamp(rint(v * r), -127, 127), in the low
+// byte of the returned word: the product is clamped first (rint is monotone
+// and the bounds are integers, so the order does not matter; a NaN product
+// clamps to -127 either way), then adding 1.5 * 2^23 rounds it to the nearest
+// integer, ties to even, and leaves that integer in two's complement in the
+// low mantissa bits.
+__device__ __forceinline__ uint32_t code_word(float v, float r) {
+    const float c = fminf(fmaxf(v * r, -127.0f), 127.0f);
+    return __float_as_uint(c + 0x1.8p23f);
 }
 
-template <int G, int CH, int RPW, int WPB>
+// The low bytes of four words, a in byte 0 (three v_perm_b32).
+__device__ __forceinline__ uint32_t pack4(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+    const uint32_t ab = __builtin_amdgcn_perm(b, a, 0x0c0c0400u);
+    const uint32_t cd = __builtin_amdgcn_perm(d, c, 0x0c0c0400u);
+    return __builtin_amdgcn_perm(cd, ab, 0x05040100u);
+}
+
+template <int G, int CH, int WPB>
 __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
     const uint16_t *__restrict__ src, const uint16_t *__restrict__ shift,
     const uint16_t *__restrict__ scale, const float *__restrict__ mul, int64_t R, int64_t K,
-    double eps, int8_t *__restrict__ out, float *__restrict__ xscale) {
+    double eps, int rows_per_group, int8_t *__restrict__ out, float *__restrict__ xscale) {
     constexpr int SLOTS = WPB / G;
     static_assert(SLOTS * G == WPB, "G must divide WPB");
     __shared__ double red_sum[SLOTS][G];
     __shared__ double red_sq[SLOTS][G];
     __shared__ float red_max[SLOTS][G];
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    // wave-uniform (in a scalar register), so that the row resources are too
+    const int wave = wave_index();
     const int sub = wave / G;
     const int gw = wave % G;
     const int64_t nchunk = K >> 3;
@@ -132,39 +166,64 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
         for (int e = 0; e < 8; ++e) {
             one_sc[c][e] = 1.0 + static_cast<double>(fs[e]);
             shd[c][e] = static_cast<double>(fh[e]);
+            // opaque: kept in registers across the rows rather than derived
+            // again from the bf16 words for every row (three binary64
+            // operations per element)
+            asm volatile("" : "+v"(one_sc[c][e]), "+v"(shd[c][e]));
         }
     }
+    // The two divisions by K: a multiplication by 1/K when K is a power of
+    // two (exact, so the same bits as the division), else the division.
+    const bool k_pow2 = (K & (K - 1)) == 0;
+    const double inv_k = 1.0 / static_cast<double>(K);
+
+    // the rows' resources: K bf16 in, K codes out, one scale out; empty past
+    // the input
+    const auto row_in = [&](int64_t r) {
+        return make_rsrc(src + r * K, r < R ? static_cast<uint32_t>(K) * 2u : 0u);
+    };
+    uint32_t in_off[CH], out_off[CH];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+        in_off[c] = live[c] ? static_cast<uint32_t>(col[c]) * 16u : 0xfffffff0u;
+        out_off[c] = live[c] ? static_cast<uint32_t>(col[c]) * 8u : 0xfffffff8u;
+    }
+    const uint32_t scale_off = (gw == 0 && lane == 0) ? 0u : 4u;
 
     uint4 x[CH];
     {
-        const bool ok = group < R;
-        const uint4 *srow = reinterpret_cast<const uint4 *>(src + (ok ? group : 0) * K);
+        const __amdgpu_buffer_rsrc_t rin = row_in(group);
 #pragma unroll
-        for (int c = 0; c < CH; ++c)
-            x[c] = (ok && live[c]) ? load_stream(srow + col[c]) : make_uint4(0u, 0u, 0u, 0u);
+        for (int c = 0; c < CH; ++c) x[c] = load_chunk(rin, in_off[c]);
     }
-    for (int it = 0; it < RPW; ++it) {
+    for (int it = 0; it < rows_per_group; ++it) {
         const int64_t row = group + it * groups;
+        // the next row (past the last row of the group it lies past the
+        // input, so nothing is read)
         uint4 xn[CH];
-        if (it + 1 < RPW) {
-            const int64_t nrow = row + groups;
-            const bool ok = nrow < R;
-            const uint4 *srow = reinterpret_cast<const uint4 *>(src + (ok ? nrow : 0) * K);
+        {
+            const __amdgpu_buffer_rsrc_t rin = row_in(row + groups);
 #pragma unroll
-            for (int c = 0; c < CH; ++c)
-                xn[c] = (ok && live[c]) ? load_stream(srow + col[c]) : make_uint4(0u, 0u, 0u, 0u);
+            for (int c = 0; c < CH; ++c) xn[c] = load_chunk(rin, in_off[c]);
         }
 
-        // mean (columns past K hold zeros and add nothing)
-        double s = 0.0;
+        // the row in binary64 (exact) and its sum; columns past K hold zeros
+        // and add nothing
+        // (two partial sums per lane, halving the dependent chain)
+        double xd[CH][8];
+        double s0 = 0.0, s1 = 0.0;
 #pragma unroll
         for (int c = 0; c < CH; ++c) {
             float v[8];
             widen8(x[c], v);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) s += static_cast<double>(v[e]);
+            for (int e = 0; e < 8; ++e) {
+                xd[c][e] = static_cast<double>(v[e]);
+                if (e & 1) s1 += xd[c][e];
+                else s0 += xd[c][e];
+            }
         }
-        s = wave_sum(s);
+        double s = wave_sum(s0 + s1);
         if constexpr (G > 1) {
             if (lane == 0) red_sum[sub][gw] = s;
             __syncthreads();
@@ -172,22 +231,22 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
 #pragma unroll
             for (int i = 1; i < G; ++i) s += red_sum[sub][i];
         }
-        const double mean = s / static_cast<double>(K);
+        const double mean = k_pow2 ? s * inv_k : s / static_cast<double>(K);
 
-        // centered sum of squares (only live columns)
-        double q = 0.0;
+        // centered values (kept for the modulation) and their sum of squares
+        // (only live columns)
+        double q0 = 0.0, q1 = 0.0;
 #pragma unroll
         for (int c = 0; c < CH; ++c) {
             if (!live[c]) continue;
-            float v[8];
-            widen8(x[c], v);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const double d = static_cast<double>(v[e]) - mean;
-                q = __builtin_fma(d, d, q);
+                xd[c][e] -= mean;
+                if (e & 1) q1 = __builtin_fma(xd[c][e], xd[c][e], q1);
+                else q0 = __builtin_fma(xd[c][e], xd[c][e], q0);
             }
         }
-        q = wave_sum(q);
+        double q = wave_sum(q0 + q1);
         if constexpr (G > 1) {
             if (lane == 0) red_sq[sub][gw] = q;
             __syncthreads();
@@ -195,19 +254,19 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
 #pragma unroll
             for (int i = 1; i < G; ++i) q += red_sq[sub][i];
         }
-        const double rstd = 1.0 / sqrt(q / static_cast<double>(K) + eps);
+        const double var = k_pow2 ? q * inv_k : q / static_cast<double>(K);
+        const double rstd = 1.0 / sqrt(var + eps);
 
-        // modulate, round to bf16 (kept packed in x), smoothed absmax
+        // modulate, round to bf16, smooth (kept in registers), absmax
+        float hv[CH][8];
         float amax = 0.0f;
 #pragma unroll
         for (int c = 0; c < CH; ++c) {
-            float v[8], f[8];
-            widen8(x[c], v);
+            float f[8];
             bool mid = false;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const double n = (static_cast<double>(v[e]) - mean) * rstd;
-                const double t = __builtin_fma(n, one_sc[c][e], shd[c][e]);
+                const double t = __builtin_fma(xd[c][e] * rstd, one_sc[c][e], shd[c][e]);
                 f[e] = static_cast<float>(t);
                 mid |= bf16_midpoint(f[e]);
             }
@@ -218,21 +277,21 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     if (!bf16_midpoint(f[e])) continue;
-                    const double n = (static_cast<double>(v[e]) - mean) * rstd;
-                    const double t = __builtin_fma(n, one_sc[c][e], shd[c][e]);
+                    const double t = __builtin_fma(xd[c][e] * rstd, one_sc[c][e], shd[c][e]);
                     const uint32_t h = bf16_bits_past_midpoint(t, f[e]);
                     const int sh = 16 * (e & 1);
                     w[e >> 1] = (w[e >> 1] & ~(0xffffu << sh)) | (h << sh);
                 }
             }
-            x[c] = make_uint4(w[0], w[1], w[2], w[3]);
-            if (live[c]) {
-                const float mv[8] = {ma[c].x, ma[c].y, ma[c].z, ma[c].w,
-                                     mb[c].x, mb[c].y, mb[c].z, mb[c].w};
-                float h[8];
-                widen8(x[c], h);
+            float h[8];
+            widen8(make_uint4(w[0], w[1], w[2], w[3]), h);
+            const float mv[8] = {ma[c].x, ma[c].y, ma[c].z, ma[c].w,
+                                 mb[c].x, mb[c].y, mb[c].z, mb[c].w};
 #pragma unroll
-                for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(h[e] * mv[e]));
+            for (int e = 0; e < 8; ++e) hv[c][e] = h[e] * mv[e];
+            if (live[c]) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(hv[c][e]));
             }
         }
         amax = wave_max(amax);
@@ -243,7 +302,7 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
             for (int i = 0; i < G; ++i) amax = fmaxf(amax, red_max[sub][i]);
         }
 
-        if (row < R) {
+        {
             float scl = 0.0f;
             float r = 0.0f;
             const bool nonzero = amax >= kTinyAbsmax;
@@ -251,41 +310,69 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
                 scl = amax / 127.0f;
                 r = 127.0f / amax;
             }
-            if (gw == 0 && lane == 0) xscale[row] = scl;
-            uint2 *orow = reinterpret_cast<uint2 *>(out + row * K);
+            const bool in = row < R;
+            const __amdgpu_buffer_rsrc_t rs = make_rsrc(xscale + (in ? row : 0), in ? 4u : 0u);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(scl), rs, scale_off, 0, 0);
+            const __amdgpu_buffer_rsrc_t ro =
+                make_rsrc(out + (in ? row : 0) * K, in ? static_cast<uint32_t>(K) : 0u);
 #pragma unroll
             for (int c = 0; c < CH; ++c) {
-                if (!live[c]) continue;
                 uint32_t lo = 0u;
                 uint32_t hi = 0u;
                 if (nonzero) {
-                    float h[8];
-                    widen8(x[c], h);
-                    lo = code(h[0] * ma[c].x, r) | code(h[1] * ma[c].y, r) << 8 |
-                         code(h[2] * ma[c].z, r) << 16 | code(h[3] * ma[c].w, r) << 24;
-                    hi = code(h[4] * mb[c].x, r) | code(h[5] * mb[c].y, r) << 8 |
-                         code(h[6] * mb[c].z, r) << 16 | code(h[7] * mb[c].w, r) << 24;
+                    lo = pack4(code_word(hv[c][0], r), code_word(hv[c][1], r),
+                               code_word(hv[c][2], r), code_word(hv[c][3], r));
+                    hi = pack4(code_word(hv[c][4], r), code_word(hv[c][5], r),
+                               code_word(hv[c][6], r), code_word(hv[c][7], r));
                 }
-                store_stream(orow + col[c], lo, hi);
+                store_codes(ro, out_off[c], lo, hi);
             }
         }
-        if (it + 1 < RPW) {
 #pragma unroll
-            for (int c = 0; c < CH; ++c) x[c] = xn[c];
-        }
+        for (int c = 0; c < CH; ++c) x[c] = xn[c];
     }
 }
 
-template <int G, int CH, int RPW, int WPB>
+// Groups that the GPU holds at once for this instantiation (CUs x resident
+// workgroups per CU x groups per workgroup), once per device.
+template <int G, int CH, int WPB>
+int64_t resident_groups() {
+    static int64_t cached[256] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 256) return 0;
+    if (cached[dev] == 0) {
+        int cus = 0;
+        int per_cu = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &per_cu, reinterpret_cast<const void *>(&adaln_quant_rows_kernel<G, CH, WPB>),
+                WPB * 64, 0) != hipSuccess)
+            return 0;
+        cached[dev] = static_cast<int64_t>(cus) * per_cu * (WPB / G);
+    }
+    return cached[dev];
+}
+
+// One round of groups: as many as the GPU holds at once (fewer for short
+// inputs), each walking rows_per_group rows, so that the per-column
+// constants each group loads serve several rows and no second, partial
+// round of groups is left at the end.
+template <int G, int CH, int WPB>
 hipError_t launch(const uint16_t *src, const uint16_t *shift, const uint16_t *scale,
                   const float *mul, int64_t R, int64_t K, double eps, int8_t *out,
                   float *xscale, hipStream_t stream) {
     constexpr int SLOTS = WPB / G;
-    const int64_t groups = (R + RPW - 1) / RPW;
+    if (R <= 0) return hipSuccess;
+    int64_t resident = resident_groups<G, CH, WPB>();
+    if (resident <= 0) resident = 256;
+    const int64_t rpg = (R + resident - 1) / resident;
+    if (rpg > INT32_MAX) return hipErrorInvalidValue;
+    const int64_t groups = (R + rpg - 1) / rpg;
     const int64_t blocks = (groups + SLOTS - 1) / SLOTS;
-    hipLaunchKernelGGL((adaln_quant_rows_kernel<G, CH, RPW, WPB>),
-                       dim3(static_cast<unsigned>(blocks)), dim3(WPB * 64), 0, stream, src, shift,
-                       scale, mul, R, K, eps, out, xscale);
+    hipLaunchKernelGGL((adaln_quant_rows_kernel<G, CH, WPB>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(WPB * 64), 0, stream, src, shift, scale, mul, R, K, eps,
+                       static_cast<int>(rpg), out, xscale);
     return hipGetLastError();
 }
 
@@ -298,14 +385,11 @@ hipError_t launch_adaln_quant_act(const uint16_t *X, const uint16_t *shift,
     // A group covers G * 64 * CH * 8 columns; K <= 8192 (checked by the API:
     // a group of 8 waves with 4 chunks per lane would need more than the 256
     // registers two waves per SIMD may hold).
-    if (K <= 512) return launch<1, 1, 2, 4>(X, shift, scale, inv_lambda, M, K, eps, Xq, x_scale, stream);
-    if (K <= 1024) return launch<2, 1, 2, 4>(X, shift, scale, inv_lambda, M, K, eps, Xq, x_scale, stream);
-    if (K <= 2048) return launch<4, 1, 2, 4>(X, shift, scale, inv_lambda, M, K, eps, Xq, x_scale, stream);
-    // At K = 4096 a group walks two rows, loading the second while it works
-    // on the first (4608 x 4096: 25.7 against 29.3 us for one row per group,
-    // in one job; three rows per group measured the same as two).
-    if (K <= 4096) return launch<4, 2, 2, 4>(X, shift, scale, inv_lambda, M, K, eps, Xq, x_scale, stream);
-    return launch<8, 2, 1, 8>(X, shift, scale, inv_lambda, M, K, eps, Xq, x_scale, stream);
+    if (K <= 512) return launch<1, 1, 4>(X, shift, scale, inv_lambda, M, K, eps, Xq, x_scale, stream);
+    if (K <= 1024) return launch<2, 1, 4>(X, shift, scale, inv_lambda, M, K, eps, Xq, x_scale, stream);
+    if (K <= 2048) return launch<4, 1, 4>(X, shift, scale, inv_lambda, M, K, eps, Xq, x_scale, stream);
+    if (K <= 4096) return launch<4, 2, 4>(X, shift, scale, inv_lambda, M, K, eps, Xq, x_scale, stream);
+    return launch<8, 2, 8>(X, shift, scale, inv_lambda, M, K, eps, Xq, x_scale, stream);
 }
 
 }  // namespace w8a8

@@ -29,6 +29,7 @@
 #include <stdint.h>
 
 #include "internal.h"
+#include "row_io.h"
 #include "wave_reduce.h"
 
 namespace w8a8 {
@@ -36,41 +37,14 @@ namespace {
 
 constexpr float kTinyAbsmax = 0x1p-96f;  // rows below quantize to zero
 
-typedef unsigned int v4u __attribute__((ext_vector_type(4)));
-typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+using rows::code_word;
+using rows::load_chunk;
+using rows::make_rsrc;
+using rows::pack4;
+using rows::store_codes;
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-// Row loads and stores go through raw buffer instructions with a per-row
-// resource: a lane whose chunk lies past the row, or a row past the input,
-// falls outside the resource's range, so the hardware reads zeros and drops
-// the store. Every wave then issues the same memory instructions for every
-// row, with no branch around them, which lets the compiler count them
-// exactly and wait for the current row's loads only, not the prefetched
-// next row's. (nt: streamed, not kept in the caches.)
-constexpr int kBufferWord3 = 0x00020000;  // raw buffer, 32-bit data format
-constexpr int kNontemporal = 2;
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, static_cast<int>(bytes),
-                                             kBufferWord3);
-}
-
-__device__ __forceinline__ int wave_index() {
-    return __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
-}
-
-__device__ __forceinline__ uint4 load_chunk(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-    const v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNontemporal);
-    return make_uint4(v.x, v.y, v.z, v.w);
-}
-
-__device__ __forceinline__ void store_codes(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t lo,
-                                            uint32_t hi) {
-    const v2u v = {lo, hi};
-    __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, kNontemporal);
-}
 
 // The 8 bf16 values of a chunk, widened (exactly).
 __device__ __forceinline__ void widen8(const uint4 &x, float (&v)[8]) {
@@ -110,24 +84,6 @@ __device__ __forceinline__ uint32_t bf16_bits_past_midpoint(double d, float f) {
 __device__ __forceinline__ double wave_sum(double v) { return lanes::sum(v); }
 __device__ __forceinline__ float wave_max(float v) { return lanes::max(v); }
 
-// The code of v at multiplier r, clamp(rint(v * r), -127, 127), in the low
-// byte of the returned word: the product is clamped first (rint is monotone
-// and the bounds are integers, so the order does not matter; a NaN product
-// clamps to -127 either way), then adding 1.5 * 2^23 rounds it to the nearest
-// integer, ties to even, and leaves that integer in two's complement in the
-// low mantissa bits.
-__device__ __forceinline__ uint32_t code_word(float v, float r) {
-    const float c = fminf(fmaxf(v * r, -127.0f), 127.0f);
-    return __float_as_uint(c + 0x1.8p23f);
-}
-
-// The low bytes of four words, a in byte 0 (three v_perm_b32).
-__device__ __forceinline__ uint32_t pack4(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
-    const uint32_t ab = __builtin_amdgcn_perm(b, a, 0x0c0c0400u);
-    const uint32_t cd = __builtin_amdgcn_perm(d, c, 0x0c0c0400u);
-    return __builtin_amdgcn_perm(cd, ab, 0x05040100u);
-}
-
 template <int G, int CH, int WPB>
 __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
     const uint16_t *__restrict__ src, const uint16_t *__restrict__ shift,
@@ -140,7 +96,7 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
     __shared__ float red_max[SLOTS][G];
     const int lane = threadIdx.x & 63;
     // wave-uniform (in a scalar register), so that the row resources are too
-    const int wave = wave_index();
+    const int wave = rows::wave_index();
     const int sub = wave / G;
     const int gw = wave % G;
     const int64_t nchunk = K >> 3;
@@ -311,8 +267,7 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
                 r = 127.0f / amax;
             }
             const bool in = row < R;
-            const __amdgpu_buffer_rsrc_t rs = make_rsrc(xscale + (in ? row : 0), in ? 4u : 0u);
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(scl), rs, scale_off, 0, 0);
+            rows::store_f32(make_rsrc(xscale + (in ? row : 0), in ? 4u : 0u), scale_off, scl);
             const __amdgpu_buffer_rsrc_t ro =
                 make_rsrc(out + (in ? row : 0) * K, in ? static_cast<uint32_t>(K) : 0u);
 #pragma unroll
@@ -333,27 +288,6 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
     }
 }
 
-// Groups that the GPU holds at once for this instantiation (CUs x resident
-// workgroups per CU x groups per workgroup), once per device.
-template <int G, int CH, int WPB>
-int64_t resident_groups() {
-    static int64_t cached[256] = {};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 256) return 0;
-    if (cached[dev] == 0) {
-        int cus = 0;
-        int per_cu = 0;
-        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
-                hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                &per_cu, reinterpret_cast<const void *>(&adaln_quant_rows_kernel<G, CH, WPB>),
-                WPB * 64, 0) != hipSuccess)
-            return 0;
-        cached[dev] = static_cast<int64_t>(cus) * per_cu * (WPB / G);
-    }
-    return cached[dev];
-}
-
 // One round of groups: as many as the GPU holds at once (fewer for short
 // inputs), each walking rows_per_group rows, so that the per-column
 // constants each group loads serve several rows and no second, partial
@@ -364,9 +298,11 @@ hipError_t launch(const uint16_t *src, const uint16_t *shift, const uint16_t *sc
                   float *xscale, hipStream_t stream) {
     constexpr int SLOTS = WPB / G;
     if (R <= 0) return hipSuccess;
-    int64_t resident = resident_groups<G, CH, WPB>();
-    if (resident <= 0) resident = 256;
-    const int64_t rpg = (R + resident - 1) / resident;
+    static int64_t resident[256] = {};
+    const int64_t rpg = rows::rows_per_group(
+        R, rows::resident_groups(
+               reinterpret_cast<const void *>(&adaln_quant_rows_kernel<G, CH, WPB>), WPB * 64,
+               SLOTS, resident));
     if (rpg > INT32_MAX) return hipErrorInvalidValue;
     const int64_t groups = (R + rpg - 1) / rpg;
     const int64_t blocks = (groups + SLOTS - 1) / SLOTS;

@@ -8,9 +8,10 @@
 // Row quantization: a group of G wavefronts owns one row. Each lane owns CH
 // chunks of 8 columns (consecutive lanes on consecutive 16-byte chunks, so
 // every wave load is one contiguous 1 KiB) and keeps the matching 8 smoothing
-// multipliers of each chunk in registers for all the rows it visits. A group
-// walks RPW rows, loading the next row while it reduces and writes the
-// current one:
+// multipliers of each chunk in registers for all the rows it visits. One
+// launch holds as many groups as the GPU keeps resident, each walking an
+// equal share of the rows and loading the next row while it reduces and
+// writes the current one:
 //   absmax over the row (lane shuffles, then across the G waves in LDS),
 //   scale, then 8 codes per chunk as one 8-byte store.
 // The smoothed value float(x) * mul is recomputed for the coding pass rather
@@ -22,6 +23,7 @@
 #include <stdint.h>
 
 #include "internal.h"
+#include "row_io.h"
 #include "wave_reduce.h"
 
 namespace w8a8 {
@@ -33,13 +35,6 @@ __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w 
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
 __device__ __forceinline__ float wave_max(float v) { return lanes::max(v); }
-
-// One code: clamp(rint(v * r), -127, 127) packed into the low byte.
-__device__ __forceinline__ uint32_t code(float v, float r) {
-    float c = rintf(v * r);
-    c = fminf(fmaxf(c, -127.0f), 127.0f);
-    return static_cast<uint32_t>(static_cast<int32_t>(c)) & 0xffu;
-}
 
 // The 8 smoothed values of one chunk: float(x_e) * mul_e, one binary32
 // rounding each.
@@ -55,19 +50,6 @@ __device__ __forceinline__ void smooth8(const uint4 &x, const float4 &ma, const 
     v[7] = bf16_hi(x.w) * mb.w;
 }
 
-typedef unsigned int v4u __attribute__((ext_vector_type(4)));
-typedef unsigned int v2u __attribute__((ext_vector_type(2)));
-
-__device__ __forceinline__ uint4 load_stream(const uint4 *p) {
-    const v4u v = __builtin_nontemporal_load(reinterpret_cast<const v4u *>(p));
-    return make_uint4(v.x, v.y, v.z, v.w);
-}
-
-__device__ __forceinline__ void store_stream(uint2 *p, uint32_t lo, uint32_t hi) {
-    const v2u v = {lo, hi};
-    __builtin_nontemporal_store(v, reinterpret_cast<v2u *>(p));
-}
-
 __device__ __forceinline__ float absmax8(const uint4 &x, const float4 &ma, const float4 &mb,
                                          float a) {
     float v[8];
@@ -77,55 +59,59 @@ __device__ __forceinline__ float absmax8(const uint4 &x, const float4 &ma, const
     return a;
 }
 
-// WPB waves per block hold WPB / G row groups. Every wave runs exactly RPW
-// iterations, so the LDS barrier is uniform; rows past R are masked. Group g
-// of the grid visits rows g, g + groups, g + 2 groups, ...
-template <int G, int CH, int RPW, int WPB>
+// WPB waves per block hold WPB / G row groups. Every wave runs exactly
+// rows_per_group iterations, so the LDS barrier is uniform; rows past R read
+// zeros and store nothing. Group g of the grid visits rows g, g + groups,
+// g + 2 groups, ... With PF the next row is loaded while the current one is
+// reduced and coded. Without (the K = 65536 group has no register room for
+// a second row) a group takes one row and the grid covers the rows.
+template <int G, int CH, int WPB, bool PF>
 __global__ __launch_bounds__(WPB * 64) void smooth_quant_rows_kernel(
     const uint16_t *__restrict__ src, const float *__restrict__ mul, int64_t R,
-    int64_t K, int8_t *__restrict__ out, float *__restrict__ scale) {
+    int64_t K, int rows_per_group, int8_t *__restrict__ out, float *__restrict__ scale) {
     constexpr int SLOTS = WPB / G;
     static_assert(SLOTS * G == WPB, "G must divide WPB");
     __shared__ float red[2][SLOTS][G];
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = rows::wave_index();
     const int sub = wave / G;
     const int gw = wave % G;
     const int64_t nchunk = K >> 3;
     const int64_t group = static_cast<int64_t>(blockIdx.x) * SLOTS + sub;
     const int64_t groups = static_cast<int64_t>(gridDim.x) * SLOTS;
 
-    int64_t col[CH];
-    bool live[CH];
+    // chunk c of the lane: col(c); a chunk past K has its byte offsets past
+    // the row, so its loads read zeros and its stores are dropped
+    const uint32_t col0 = static_cast<uint32_t>(gw * 64 + lane);
+    const auto col = [&](int c) { return col0 + static_cast<uint32_t>(c * G * 64); };
     float4 ma[CH], mb[CH];
     const float4 *m4 = reinterpret_cast<const float4 *>(mul);
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
-        col[c] = static_cast<int64_t>(c) * (G * 64) + gw * 64 + lane;
-        live[c] = col[c] < nchunk;
-        ma[c] = live[c] ? m4[2 * col[c]] : make_float4(0.f, 0.f, 0.f, 0.f);
-        mb[c] = live[c] ? m4[2 * col[c] + 1] : make_float4(0.f, 0.f, 0.f, 0.f);
+        const bool live = col(c) < nchunk;
+        ma[c] = live ? m4[2 * col(c)] : make_float4(0.f, 0.f, 0.f, 0.f);
+        mb[c] = live ? m4[2 * col(c) + 1] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
+    const uint32_t scale_off = (gw == 0 && lane == 0) ? 0u : 4u;
+    // the rows' resources: K bf16 in, K codes out, one scale out; empty past
+    // the input
+    const auto load_row = [&](int64_t r, uint4 (&x)[CH]) {
+        const __amdgpu_buffer_rsrc_t rin =
+            rows::make_rsrc(src + r * K, r < R ? static_cast<uint32_t>(K) * 2u : 0u);
+#pragma unroll
+        for (int c = 0; c < CH; ++c) x[c] = rows::load_chunk(rin, col(c) * 16u);
+    };
 
     uint4 x[CH];
-    {
-        const bool ok = group < R;
-        const uint4 *srow = reinterpret_cast<const uint4 *>(src + (ok ? group : 0) * K);
-#pragma unroll
-        for (int c = 0; c < CH; ++c)
-            x[c] = (ok && live[c]) ? load_stream(srow + col[c]) : make_uint4(0u, 0u, 0u, 0u);
-    }
-    for (int it = 0; it < RPW; ++it) {
+    if constexpr (PF) load_row(group, x);
+    const int n_rows = PF ? rows_per_group : 1;
+    for (int it = 0; it < n_rows; ++it) {
         const int64_t row = group + it * groups;
         uint4 xn[CH];
-        if (it + 1 < RPW) {
-            const int64_t nrow = row + groups;
-            const bool ok = nrow < R;
-            const uint4 *srow = reinterpret_cast<const uint4 *>(src + (ok ? nrow : 0) * K);
-#pragma unroll
-            for (int c = 0; c < CH; ++c)
-                xn[c] = (ok && live[c]) ? load_stream(srow + col[c]) : make_uint4(0u, 0u, 0u, 0u);
-        }
+        // the next row (past the group's last row it lies past the input,
+        // so nothing is read)
+        if constexpr (PF) load_row(row + groups, xn);
+        else load_row(row, x);
         float amax = 0.0f;
 #pragma unroll
         for (int c = 0; c < CH; ++c) amax = absmax8(x[c], ma[c], mb[c], amax);
@@ -136,51 +122,62 @@ __global__ __launch_bounds__(WPB * 64) void smooth_quant_rows_kernel(
 #pragma unroll
             for (int i = 0; i < G; ++i) amax = fmaxf(amax, red[it & 1][sub][i]);
         }
-        if (row < R) {
-            float sc = 0.0f;
-            float r = 0.0f;
-            const bool nonzero = amax >= kTinyAbsmax;
-            if (nonzero) {
-                sc = amax / 127.0f;
-                r = 127.0f / amax;
-            }
-            if (gw == 0 && lane == 0) scale[row] = sc;
-            uint2 *orow = reinterpret_cast<uint2 *>(out + row * K);
-#pragma unroll
-            for (int c = 0; c < CH; ++c) {
-                if (!live[c]) continue;
-                uint32_t lo = 0u;
-                uint32_t hi = 0u;
-                if (nonzero) {
-                    float t[8];
-                    smooth8(x[c], ma[c], mb[c], t);
-                    lo = code(t[0], r) | code(t[1], r) << 8 | code(t[2], r) << 16 |
-                         code(t[3], r) << 24;
-                    hi = code(t[4], r) | code(t[5], r) << 8 | code(t[6], r) << 16 |
-                         code(t[7], r) << 24;
-                }
-                store_stream(orow + col[c], lo, hi);
-            }
+        float sc = 0.0f;
+        float r = 0.0f;
+        const bool nonzero = amax >= kTinyAbsmax;
+        if (nonzero) {
+            sc = amax / 127.0f;
+            r = 127.0f / amax;
         }
-        if (it + 1 < RPW) {
+        const bool in = row < R;
+        rows::store_f32(rows::make_rsrc(scale + (in ? row : 0), in ? 4u : 0u), scale_off, sc);
+        const __amdgpu_buffer_rsrc_t ro =
+            rows::make_rsrc(out + (in ? row : 0) * K, in ? static_cast<uint32_t>(K) : 0u);
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            uint32_t lo = 0u;
+            uint32_t hi = 0u;
+            if (nonzero) {
+                float t[8];
+                smooth8(x[c], ma[c], mb[c], t);
+                lo = rows::pack4(rows::code_word(t[0], r), rows::code_word(t[1], r),
+                                 rows::code_word(t[2], r), rows::code_word(t[3], r));
+                hi = rows::pack4(rows::code_word(t[4], r), rows::code_word(t[5], r),
+                                 rows::code_word(t[6], r), rows::code_word(t[7], r));
+            }
+            rows::store_codes(ro, col(c) * 8u, lo, hi);
+        }
+        if constexpr (PF) {
 #pragma unroll
             for (int c = 0; c < CH; ++c) x[c] = xn[c];
         }
     }
 }
 
-template <int G, int CH, int RPW, int WPB>
+// One round of groups: as many as the GPU holds at once (fewer for short
+// inputs), each walking an equal share of the rows.
+template <int G, int CH, int WPB, bool PF>
 hipError_t launch_rows(const uint16_t *src, const float *mul, int64_t R, int64_t K,
                        int8_t *out, float *scale, hipStream_t stream) {
     constexpr int SLOTS = WPB / G;
-    const int64_t groups = (R + RPW - 1) / RPW;
+    if (R <= 0) return hipSuccess;
+    static int64_t resident[256] = {};
+    const int64_t rpg =
+        PF ? rows::rows_per_group(
+                 R, rows::resident_groups(
+                        reinterpret_cast<const void *>(&smooth_quant_rows_kernel<G, CH, WPB, PF>),
+                        WPB * 64, SLOTS, resident))
+           : 1;
+    if (rpg > INT32_MAX) return hipErrorInvalidValue;
+    const int64_t groups = (R + rpg - 1) / rpg;
     const int64_t blocks = (groups + SLOTS - 1) / SLOTS;
-    // A grid of 2^32 work-items or more cannot be launched. Only R = 2^22
-    // rows with K > 32768 get there, 512 GB of bf16, more than the GPU holds.
+    // A grid of 2^32 work-items or more cannot be launched. Only one row per
+    // group gets there: R = 2^22 rows with K > 32768, 512 GB of bf16, more
+    // than the GPU holds.
     if (blocks * WPB * 64 >= (INT64_C(1) << 32)) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((smooth_quant_rows_kernel<G, CH, RPW, WPB>),
+    hipLaunchKernelGGL((smooth_quant_rows_kernel<G, CH, WPB, PF>),
                        dim3(static_cast<unsigned>(blocks)), dim3(WPB * 64), 0, stream, src, mul,
-                       R, K, out, scale);
+                       R, K, static_cast<int>(rpg), out, scale);
     return hipGetLastError();
 }
 
@@ -290,19 +287,14 @@ hipError_t launch_smooth_quant_rows(const uint16_t *src, const float *mul, int64
                                     int64_t K, int8_t *out, float *scale,
                                     hipStream_t stream) {
     // A group covers 512 * G * CH columns; take the smallest that holds K.
-    // Up to K = 32768 a group has at most 8 waves and walks two rows (each
-    // next one prefetched); at K = 4096 and 16384 three (4608 x 4096: 11.96
-    // against 12.91 us for two; 4608 x 16384: 40.6 against 41.0-42.6 us; in
-    // one job each). The K = 65536 group of 16 waves has no register room
-    // for a prefetched row and walks one.
-    if (K <= 512) return launch_rows<1, 1, 2, 4>(src, mul, R, K, out, scale, stream);
-    if (K <= 1024) return launch_rows<2, 1, 2, 4>(src, mul, R, K, out, scale, stream);
-    if (K <= 2048) return launch_rows<4, 1, 2, 4>(src, mul, R, K, out, scale, stream);
-    if (K <= 4096) return launch_rows<4, 2, 3, 4>(src, mul, R, K, out, scale, stream);
-    if (K <= 8192) return launch_rows<8, 2, 2, 8>(src, mul, R, K, out, scale, stream);
-    if (K <= 16384) return launch_rows<8, 4, 3, 8>(src, mul, R, K, out, scale, stream);
-    if (K <= 32768) return launch_rows<8, 8, 2, 8>(src, mul, R, K, out, scale, stream);
-    return launch_rows<16, 8, 1, 16>(src, mul, R, K, out, scale, stream);  // K <= 65536
+    if (K <= 512) return launch_rows<1, 1, 4, true>(src, mul, R, K, out, scale, stream);
+    if (K <= 1024) return launch_rows<2, 1, 4, true>(src, mul, R, K, out, scale, stream);
+    if (K <= 2048) return launch_rows<4, 1, 4, true>(src, mul, R, K, out, scale, stream);
+    if (K <= 4096) return launch_rows<4, 2, 4, true>(src, mul, R, K, out, scale, stream);
+    if (K <= 8192) return launch_rows<8, 2, 8, true>(src, mul, R, K, out, scale, stream);
+    if (K <= 16384) return launch_rows<8, 4, 8, true>(src, mul, R, K, out, scale, stream);
+    if (K <= 32768) return launch_rows<8, 8, 8, true>(src, mul, R, K, out, scale, stream);
+    return launch_rows<16, 8, 16, false>(src, mul, R, K, out, scale, stream);  // K <= 65536
 }
 
 hipError_t launch_reciprocal(const float *lam, int64_t K, float *inv, hipStream_t stream) {

@@ -149,6 +149,20 @@ def device_inputs(M, K, dev, gen, n, gelu: bool):
     return out
 
 
+def modulate(layers, dev, seed: int) -> None:
+    """Give the QKV and FFN-up layers (the inputs a DiT block modulates with
+    adaLN) a per-layer shift and scale, bf16 N(0, 0.05) and N(0, 0.1): their
+    activation step becomes w8a8_adaln_quant_act."""
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seed)
+    for lin in layers:
+        if lin.lay.protected or not any(t in lin.name for t in ("qkv", "ffn_up")):
+            continue
+        K = lin.lay.K
+        lin.mod = tuple((torch.randn(K, device=dev, generator=gen) * sd).bfloat16()
+                        for sd in (0.05, 0.1))
+
+
 def build_workload(name: str, dev, pool: int):
     if name in ("q8_0_ffn_up", "q4_k_ffn_up"):
         c = synth.ffn_up_case()
@@ -807,6 +821,9 @@ def main():
                     choices=["ffn_up", "ffn_down", "dit_block", "backbone", "q8_0_ffn_up",
                              "q4_k_ffn_up", "adaln_ffn_up"])
     ap.add_argument("--pool", type=int, default=4, help="distinct inputs rotated over steps")
+    ap.add_argument("--adaln", action="store_true",
+                    help="dit_block / backbone: the QKV and FFN-up inputs go through the fused "
+                         "adaLN step (w8a8_adaln_quant_act) instead of w8a8_quant_act")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-accuracy", action="store_true",
                     help="skip the error report against a binary64 product")
@@ -844,6 +861,10 @@ def main():
 
     t_build = time.perf_counter()
     layers = build_workload(args.workload, dev, args.pool)
+    if args.adaln:
+        if args.workload not in ("dit_block", "backbone"):
+            raise SystemExit("--adaln applies to --workload dit_block and backbone")
+        modulate(layers, dev, 11)
     torch.cuda.synchronize()
     log(f"workload {args.workload}: {len(layers)} linears prepared in "
         f"{time.perf_counter() - t_build:.1f} s")
@@ -967,8 +988,8 @@ def main():
         accuracy = accuracy_report(layers, dev)
 
     cpu = None
-    if not args.no_cpu_baseline and args.workload in ("ffn_up", "ffn_down", "dit_block",
-                                                       "backbone"):
+    if not args.no_cpu_baseline and not args.adaln and args.workload in (
+            "ffn_up", "ffn_down", "dit_block", "backbone"):
         log("timing the CPU oracle on a bounded sample ...")
         cpu = cpu_baseline(args.workload, args.cpu_seconds)
 
@@ -981,8 +1002,11 @@ def main():
                         "q8_0_ffn_up": "DiT FFN up-projection 4608x4096->16384 with GGUF Q8_0 weights",
                         "q4_k_ffn_up": "DiT FFN up-projection 4608x4096->16384 with GGUF Q4_K weights"}[args.workload],
            "tokens": M0, "linears": len(layers), "protected": len(prot),
+           "adaln_inputs": sum(lin.mod is not None for lin in layers),
            "input_pool": args.pool if args.workload in ("ffn_up", "ffn_down", "adaln_ffn_up") else None,
            "smoothquant_alpha": 0.5}
+    if args.adaln:
+        cfg["workload"] += ", QKV and FFN-up inputs through the fused adaLN step"
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TOPS", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),

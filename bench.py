@@ -245,16 +245,47 @@ def run_step(layers, it: int, ws: L.Workspace, events=None):
             events[li][2].record()
 
 
-def measure(layers, steps: int, warmup: int, dev, per_kernel: bool, warm_ms: float = 200.0):
+class BranchStreams:
+    """The two CFG branches of a step on two streams of default priority:
+    their layers are independent (separate weights, separate inputs), so the
+    kernels of one branch can fill the GPU where the other's leave it idle
+    (the per-XCD tail of a GEMM, the ramp of a launch). Layer i of each
+    branch is issued in turn; each stream has its own workspace."""
+
+    def __init__(self, layers, dev):
+        self.branches = [[lin for lin in layers if lin.name.startswith(f"b{b}_")] for b in (0, 1)]
+        if len(self.branches[0]) + len(self.branches[1]) != len(layers) or \
+                len(self.branches[0]) != len(self.branches[1]):
+            raise SystemExit("--branch-streams needs the two branches' layers b0_* and b1_*")
+        self.streams = [torch.cuda.Stream(device=dev) for _ in range(2)]
+        self.ws = [L.Workspace(dev) for _ in range(2)]
+
+    def step(self, it: int):
+        cur = torch.cuda.current_stream()
+        for st in self.streams:
+            st.wait_stream(cur)
+        for pair in zip(*self.branches):
+            for b in (0, 1):
+                with torch.cuda.stream(self.streams[b]):
+                    run_step([pair[b]], it, self.ws[b])
+        for st in self.streams:
+            cur.wait_stream(st)
+
+
+def measure(layers, steps: int, warmup: int, dev, per_kernel: bool, warm_ms: float = 200.0,
+            branch_streams: bool = False):
     ws = L.Workspace(dev)
+    two = BranchStreams(layers, dev) if branch_streams and not per_kernel else None
+    step = (lambda it, e=None: two.step(it)) if two else \
+        (lambda it, e=None: run_step(layers, it, ws, e))
     for i in range(warmup):
-        run_step(layers, i, ws)
+        step(i)
     torch.cuda.synchronize()
     # keep the GPU busy long enough for its clocks to settle before timing
     t_end = time.perf_counter() + warm_ms * 1e-3
     i = warmup
     while time.perf_counter() < t_end:
-        run_step(layers, i, ws)
+        step(i)
         torch.cuda.synchronize()
         i += 1
     ev = None
@@ -267,7 +298,7 @@ def measure(layers, steps: int, warmup: int, dev, per_kernel: bool, warm_ms: flo
     wall0 = time.perf_counter()
     t0.record()
     for s in range(steps):
-        run_step(layers, warmup + s, ws, ev[s] if ev else None)
+        step(warmup + s, ev[s] if ev else None)
     t1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -821,6 +852,9 @@ def main():
                     choices=["ffn_up", "ffn_down", "dit_block", "backbone", "q8_0_ffn_up",
                              "q4_k_ffn_up", "adaln_ffn_up"])
     ap.add_argument("--pool", type=int, default=4, help="distinct inputs rotated over steps")
+    ap.add_argument("--branch-streams", action="store_true",
+                    help="dit_block / backbone: the step time with the two CFG branches issued "
+                         "on two streams (per-kernel figures stay single-stream)")
     ap.add_argument("--adaln", action="store_true",
                     help="dit_block / backbone: the QKV and FFN-up inputs go through the fused "
                          "adaLN step (w8a8_adaln_quant_act) instead of w8a8_quant_act")
@@ -876,7 +910,10 @@ def main():
     step_ms_ev, _, quant_us, gemm_us = measure(layers, args.steps, args.warmup, dev, True)
     gemm_each = measure.gemm_each
     # the step time proper, without per-kernel events
-    step_ms, wall_ms, _, _ = measure(layers, args.steps, args.warmup, dev, False)
+    if args.branch_streams and args.workload not in ("dit_block", "backbone"):
+        raise SystemExit("--branch-streams applies to --workload dit_block and backbone")
+    step_ms, wall_ms, _, _ = measure(layers, args.steps, args.warmup, dev, False,
+                                     branch_streams=args.branch_streams)
     total_ops = sum(lin.ops for lin in layers)
     value = total_ops / (step_ms * 1e-3) / 1e12
 
@@ -1007,6 +1044,8 @@ def main():
            "smoothquant_alpha": 0.5}
     if args.adaln:
         cfg["workload"] += ", QKV and FFN-up inputs through the fused adaLN step"
+    if args.branch_streams:
+        cfg["workload"] += ", the two branches on two streams"
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TOPS", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),

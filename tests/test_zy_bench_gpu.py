@@ -53,3 +53,30 @@ def test_bench_json_line(capsys, monkeypatch):
     # per-token and per-channel 8-bit grids with outlier channels smoothed
     assert a["bf16"]["rel_frobenius"] < a["w8a8"]["rel_frobenius"] < 0.05
     assert d["cpu_baseline"] is None
+
+
+def test_branch_streams_write_the_same_outputs():
+    """The DiT block's two branches issued on two streams (bench.py
+    --branch-streams) give every layer the same output bits as the one-stream
+    step, with the adaLN-fused inputs included."""
+    sys.path.insert(0, ROOT)
+    import torch
+
+    import bench
+    from paper_2606_12280_amd import layer as L
+
+    dev = torch.device("cuda:0")
+    print("dit_block, one stream against two", flush=True)
+    layers = bench.build_workload("dit_block", dev, 1)
+    bench.modulate(layers, dev, 11)
+    assert sum(lin.mod is not None for lin in layers) == 4
+    bench.run_step(layers, 0, L.Workspace(dev))
+    torch.cuda.synchronize()
+    one = [lin.Y.clone() for lin in layers]
+    for lin in layers:
+        lin.Y.zero_()
+    two = bench.BranchStreams(layers, dev)
+    two.step(0)
+    torch.cuda.synchronize()
+    for lin, y in zip(layers, one):
+        assert torch.equal(lin.Y.view(torch.int16), y.view(torch.int16)), lin.name

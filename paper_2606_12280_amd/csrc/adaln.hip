@@ -22,8 +22,8 @@
 // GPU keeps resident, each walking an equal share of the rows with the next
 // row prefetched. The three row reductions (sum, centered sum of squares,
 // absmax) run as lane butterflies, then across the G waves through LDS. The
-// vector ALU bounds the kernel, not its bytes: about 30 instructions per
-// element, a third of them binary64.
+// vector ALU's issue bounds the kernel, not its bytes: about 27 instructions
+// per element, a third of them binary64.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -136,7 +136,7 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
     // the rows' resources: K bf16 in, K codes out, one scale out; empty past
     // the input
     const auto row_in = [&](int64_t r) {
-        return make_rsrc(src + r * K, r < R ? static_cast<uint32_t>(K) * 2u : 0u);
+        return make_rsrc(src + (r < R ? r : 0) * K, r < R ? static_cast<uint32_t>(K) * 2u : 0u);
     };
     uint32_t in_off[CH], out_off[CH];
 #pragma unroll

@@ -97,7 +97,7 @@ __global__ __launch_bounds__(WPB * 64) void smooth_quant_rows_kernel(
     // the input
     const auto load_row = [&](int64_t r, uint4 (&x)[CH]) {
         const __amdgpu_buffer_rsrc_t rin =
-            rows::make_rsrc(src + r * K, r < R ? static_cast<uint32_t>(K) * 2u : 0u);
+            rows::make_rsrc(src + (r < R ? r : 0) * K, r < R ? static_cast<uint32_t>(K) * 2u : 0u);
 #pragma unroll
         for (int c = 0; c < CH; ++c) x[c] = rows::load_chunk(rin, col(c) * 16u);
     };

@@ -57,6 +57,19 @@ def test_quant_act_bit_exact(M, K):
     assert np.array_equal(Xq, Xq_ref)
 
 
+@pytest.mark.parametrize("M,K", [(300001, 64), (65537, 1024), (20011, 4096)])
+def test_quant_act_many_rows_per_group(M, K):
+    """Long inputs: one launch holds as many row groups as the GPU keeps
+    resident and each walks dozens of rows, the last of them ragged; every
+    code and scale bit-exact."""
+    rng = np.random.default_rng([102, M, K])
+    X = synth.to_bf16_bits(synth.outlier_activations(rng, M, K, max(1, K // 100), 20.0))
+    lam = np.exp(rng.uniform(-2, 2, K)).astype(np.float32)
+    Xq, xs, Xq_ref, xs_ref = _quant_case(X, lam, M, K)
+    assert np.array_equal(xs, xs_ref)
+    assert np.array_equal(Xq, Xq_ref)
+
+
 def test_quant_act_special_rows():
     """Zero, tiny (below 2^-96), constant, one-hot and tie rows."""
     K = 256
@@ -725,6 +738,13 @@ def _check_adaln(X, shift, scale, il, M, K, eps=1e-6):
                                  (64, 8192)])
 def test_adaln_quant_act_bit_exact(M, K):
     _check_adaln(*_adaln_inputs([180, M, K], M, K), M, K)
+
+
+@pytest.mark.parametrize("M,K", [(200003, 64), (30011, 1024), (9001, 4096)])
+def test_adaln_quant_act_many_rows_per_group(M, K):
+    """Long inputs: each resident row group walks dozens of rows, the last of
+    them ragged; codes and scales bit-exact."""
+    _check_adaln(*_adaln_inputs([183, M, K], M, K), M, K)
 
 
 def test_adaln_quant_act_special_rows():

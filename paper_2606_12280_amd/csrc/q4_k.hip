@@ -162,20 +162,21 @@ __global__ __launch_bounds__(256) void q4_k_dequantize_kernel(
     if (t >= octets) return;
     const int jj = static_cast<int>((t >> 2) & (kSubs - 1));  // sub-block in its super-block
     const int64_t g = t >> 5;                                    // super-block (32 octets)
-    const uint32_t w0 = scales[3 * g], w1 = scales[3 * g + 1], w2 = scales[3 * g + 2];
-    const int sh = 8 * (jj & 3);
-    uint32_t vs, vm;
-    if (jj < 4) {
-        vs = (w0 >> sh) & 63u;
-        vm = (w1 >> sh) & 63u;
-    } else {
-        const uint32_t lo = (w2 >> sh) & 255u;
-        vs = (lo & 15u) | (((w0 >> (sh + 6)) & 3u) << 4);
-        vm = (lo >> 4) | (((w1 >> (sh + 6)) & 3u) << 4);
-    }
-    const float s = half_bits_to_float(d[g]) * static_cast<float>(vs);
-    const float o = half_bits_to_float(dmin[g]) * static_cast<float>(vm);
+    // Every load first, none behind a branch: the codes, the super-block's
+    // three scale words and its two binary16 scales go out together, so a
+    // thread waits for one memory round trip, not two.
     const uint32_t q = __builtin_nontemporal_load(qs + t);
+    const uint32_t w0 = scales[3 * g], w1 = scales[3 * g + 1], w2 = scales[3 * g + 2];
+    const uint16_t dh = d[g], mh = dmin[g];
+    // the sub-block's 6-bit scale and offset, for both halves of the layout,
+    // then the one for jj (a select, so both halves of a wave agree on the
+    // path)
+    const int sh = 8 * (jj & 3);
+    const uint32_t lo = (w2 >> sh) & 255u;
+    const uint32_t vs = jj < 4 ? (w0 >> sh) & 63u : (lo & 15u) | (((w0 >> (sh + 6)) & 3u) << 4);
+    const uint32_t vm = jj < 4 ? (w1 >> sh) & 63u : (lo >> 4) | (((w1 >> (sh + 6)) & 3u) << 4);
+    const float s = half_bits_to_float(dh) * static_cast<float>(vs);
+    const float o = half_bits_to_float(mh) * static_cast<float>(vm);
     uint32_t out[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {

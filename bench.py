@@ -272,12 +272,37 @@ class BranchStreams:
             cur.wait_stream(st)
 
 
+def captured_steps(step, layers, warmup: int):
+    """The step as HIP graphs, one per input of the rotation (a graph holds
+    fixed pointers): captured once each after an eager warm-up on the
+    capture stream, then replayed. The kernels of the step allocate nothing
+    and issue no memset, so a replay does what the eager step does."""
+    n = max(len(lin.xs) for lin in layers)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for i in range(n):
+            step(warmup + i)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graphs = {}
+    for i in range(n):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step(warmup + i)
+        graphs[(warmup + i) % n] = g
+    torch.cuda.synchronize()
+    return lambda it, e=None: graphs[it % n].replay()
+
+
 def measure(layers, steps: int, warmup: int, dev, per_kernel: bool, warm_ms: float = 200.0,
-            branch_streams: bool = False):
+            branch_streams: bool = False, graph: bool = False):
     ws = L.Workspace(dev)
     two = BranchStreams(layers, dev) if branch_streams and not per_kernel else None
     step = (lambda it, e=None: two.step(it)) if two else \
         (lambda it, e=None: run_step(layers, it, ws, e))
+    if graph and not per_kernel:
+        step = captured_steps(step, layers, warmup)
     for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
@@ -852,6 +877,9 @@ def main():
                     choices=["ffn_up", "ffn_down", "dit_block", "backbone", "q8_0_ffn_up",
                              "q4_k_ffn_up", "adaln_ffn_up"])
     ap.add_argument("--pool", type=int, default=4, help="distinct inputs rotated over steps")
+    ap.add_argument("--graph", action="store_true",
+                    help="the step time with each step replayed from a captured HIP graph "
+                         "(per-kernel figures stay eager)")
     ap.add_argument("--branch-streams", action="store_true",
                     help="dit_block / backbone: the step time with the two CFG branches issued "
                          "on two streams (per-kernel figures stay single-stream)")
@@ -913,7 +941,7 @@ def main():
     if args.branch_streams and args.workload not in ("dit_block", "backbone"):
         raise SystemExit("--branch-streams applies to --workload dit_block and backbone")
     step_ms, wall_ms, _, _ = measure(layers, args.steps, args.warmup, dev, False,
-                                     branch_streams=args.branch_streams)
+                                     branch_streams=args.branch_streams, graph=args.graph)
     total_ops = sum(lin.ops for lin in layers)
     value = total_ops / (step_ms * 1e-3) / 1e12
 
@@ -1046,6 +1074,8 @@ def main():
         cfg["workload"] += ", QKV and FFN-up inputs through the fused adaLN step"
     if args.branch_streams:
         cfg["workload"] += ", the two branches on two streams"
+    if args.graph:
+        cfg["workload"] += ", each step replayed from a HIP graph"
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TOPS", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),

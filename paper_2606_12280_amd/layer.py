@@ -116,6 +116,27 @@ def route(layer: PreparedLinear, X: torch.Tensor, out: torch.Tensor | None = Non
     return ops.w8a8_linear(Xq, x_scale, layer.Wq, layer.w_scale, layer.bias, out=out)
 
 
+def route_modulated(layer: PreparedLinear, X: torch.Tensor, shift: torch.Tensor,
+                    scale: torch.Tensor, eps: float = 1e-6, out: torch.Tensor | None = None,
+                    ws: Workspace | None = None) -> torch.Tensor:
+    """Y = layer(bf16(LayerNorm(X) * (1 + scale) + shift)) for a W8A8 layer
+    whose input a DiT block modulates (QKV, FFN up): the modulation fused
+    into the activation quantization (w8a8_adaln_quant_act), then the W8A8
+    GEMM. The fused step feeds the W8A8 path only; protected and GGUF layers
+    raise (in a DiT their inputs are not modulated)."""
+    if layer.protected or layer.weight_only:
+        raise ValueError("route_modulated takes W8A8 layers only; the fused adaLN step feeds "
+                         "the INT8 path")
+    M = X.shape[0]
+    if ws is None:
+        Xq = x_scale = None
+    else:
+        Xq, x_scale = ws.get(M, layer.K)
+    Xq, x_scale = ops.w8a8_adaln_quant_act(X, shift, scale, layer.inv_lambda, eps, Xq=Xq,
+                                           x_scale=x_scale)
+    return ops.w8a8_linear(Xq, x_scale, layer.Wq, layer.w_scale, layer.bias, out=out)
+
+
 def protected_layers(n_layers: int, n_protect: int, shapes_cycle: int = 4,
                      down_slot: int = 3) -> list[bool]:
     """Protection flags for a backbone whose layers cycle over

@@ -764,6 +764,31 @@ def test_adaln_quant_act_special_rows():
     _check_adaln(X, shift, scale, il, M, K, eps=0.0)
 
 
+@pytest.mark.parametrize("M,N,K", [(300, 520, 1088), (2000, 4096, 4096)])
+def test_route_modulated_against_the_oracle(M, N, K):
+    """layer.route_modulated (adaLN step + W8A8 GEMM) against the oracle's
+    modulation, quantization, int32 product and epilogue; protected layers
+    are refused."""
+    from paper_2606_12280_amd import layer
+    X, shift, scale, _ = _adaln_inputs([184, M, N, K], M, K)
+    rng = np.random.default_rng([185, M, N, K])
+    W = synth.to_bf16_bits(rng.normal(0, 0.02, (N, K)).astype(np.float32))
+    b = synth.to_bf16_bits(rng.normal(0, 0.01, N).astype(np.float32))
+    lam = rng.uniform(0.25, 4.0, K).astype(np.float32)
+    Wq_ref, ws_ref, il_ref = oracle.prepare_weight(W, lam, N, K)
+    Xq_ref, xs_ref = oracle.adaln_quant_act(X, shift, scale, il_ref, M, K)
+    acc = oracle.gemm_i32(Xq_ref, Wq_ref, M, N, K)
+    Y_ref = oracle.epilogue(acc, xs_ref, ws_ref, b, M, N)
+    Wd, bd = dev_bf16(W.reshape(N, K)), dev_bf16(b)
+    lin = layer.prepare_linear(Wd, bd, dev(lam), protected=False)
+    Y = layer.route_modulated(lin, dev_bf16(X.reshape(M, K)), dev_bf16(shift), dev_bf16(scale),
+                              ws=layer.Workspace("cuda"))
+    check_w8a8_output(host_bits(Y), Y_ref, acc, xs_ref, ws_ref, b)
+    prot = layer.prepare_linear(Wd, bd, None, protected=True)
+    with pytest.raises(ValueError):
+        layer.route_modulated(prot, dev_bf16(X.reshape(M, K)), dev_bf16(shift), dev_bf16(scale))
+
+
 def test_adaln_quant_act_full_size():
     """The FFN-up / QKV input of a DiT block, 4608 x 4096, whole tensor."""
     M, K = 4608, 4096

@@ -535,7 +535,14 @@ def clock_under_load(lin: Linear, dev, seconds: float = 3.0):
     """The graphics clock of each XCD while `lin`'s INT8 GEMM runs back to
     back, read in-process from the GPU metrics table through amdsmi (no
     child process). The first second is left out while the clock settles.
-    None where amdsmi or the metric is missing."""
+    None where amdsmi or the metric is missing.
+
+    From the same table, over the sampled window: the share of the power
+    manager's 1 ms intervals in which package power tracking (the socket
+    power limit) held the clock down, the average socket power, and the
+    energy per launch. On MI355X the energy accumulator counts 2^-16 J and
+    the firmware timestamp 10 ns (under a sustained load the two give the
+    1400 W power limit)."""
     try:
         import amdsmi
         amdsmi.amdsmi_init()
@@ -553,14 +560,20 @@ def clock_under_load(lin: Linear, dev, seconds: float = 3.0):
         uclk = []
         t0 = time.perf_counter()
         last = 0.0
+        first = None      # metrics table at the start of the sampled window
+        launches = 0      # launches since then
         while time.perf_counter() - t0 < seconds:
             for _ in range(per):
                 ops.w8a8_linear(Xq, xsc, lin.lay.Wq, lin.lay.w_scale, lin.lay.bias, out=lin.Y)
             torch.cuda.synchronize()
+            if first is not None:
+                launches += per
             now = time.perf_counter() - t0
             if now > 1.0 and now - last > 0.05:
                 last = now
                 met = amdsmi.amdsmi_get_gpu_metrics_info(h)
+                if first is None:
+                    first = met
                 clks = met.get("current_gfxclks")
                 u = met.get("current_uclk")
                 if isinstance(u, (int, float)) and 0 < u < 100000:
@@ -569,17 +582,20 @@ def clock_under_load(lin: Linear, dev, seconds: float = 3.0):
                     clks = [int(c) for c in clks if isinstance(c, (int, float)) and 0 < c < 10000]
                     if clks:
                         samples.append(clks)
+        end = amdsmi.amdsmi_get_gpu_metrics_info(h) if first is not None else None
         del Xq, xsc
         if not samples or len({len(c) for c in samples}) != 1:
             return None
         a = np.array(samples, dtype=np.float64)
         per_xcd = a.mean(axis=0)
-        return {"source": "amdsmi GPU metrics (current_gfxclks), sampled in-process during "
-                          f"{seconds:.0f} s of back-to-back launches of this kernel",
-                "mhz_per_xcd": [round(float(v)) for v in per_xcd],
-                "mhz_mean": round(float(per_xcd.mean()), 1),
-                "mhz_min": round(float(per_xcd.min()), 1), "samples": len(samples),
-                "memory_clock_mhz": round(float(np.mean(uclk)), 1) if uclk else None}
+        out = {"source": "amdsmi GPU metrics (current_gfxclks), sampled in-process during "
+                         f"{seconds:.0f} s of back-to-back launches of this kernel",
+               "mhz_per_xcd": [round(float(v)) for v in per_xcd],
+               "mhz_mean": round(float(per_xcd.mean()), 1),
+               "mhz_min": round(float(per_xcd.min()), 1), "samples": len(samples),
+               "memory_clock_mhz": round(float(np.mean(uclk)), 1) if uclk else None}
+        out["power"] = power_over_window(amdsmi, h, first, end, launches, lin.ops)
+        return out
     except Exception:
         return None
     finally:
@@ -587,6 +603,39 @@ def clock_under_load(lin: Linear, dev, seconds: float = 3.0):
             amdsmi.amdsmi_shut_down()
         except Exception:
             pass
+
+
+def power_over_window(amdsmi, h, first, end, launches, ops_per_launch):
+    """Power figures between two snapshots of the GPU metrics table taken
+    around `launches` back-to-back launches (see clock_under_load); None
+    where a field is missing."""
+    def num(m, k):
+        v = m.get(k) if m is not None else None
+        return float(v) if isinstance(v, (int, float)) else None
+
+    try:
+        cap = amdsmi.amdsmi_get_power_cap_info(h).get("power_cap")
+        cap_w = float(cap) / 1e6 if isinstance(cap, (int, float)) and cap > 0 else None
+    except Exception:
+        cap_w = None
+    d = {}
+    for k in ("accumulation_counter", "ppt_residency_acc", "energy_accumulator",
+              "firmware_timestamp"):
+        a, b = num(first, k), num(end, k)
+        d[k] = b - a if a is not None and b is not None else None
+    if not d["accumulation_counter"] or not d["firmware_timestamp"] or not launches:
+        return {"power_limit_w": cap_w}
+    seconds = d["firmware_timestamp"] * 1e-8
+    joules = d["energy_accumulator"] * 2.0 ** -16 if d["energy_accumulator"] is not None else None
+    out = {"power_limit_w": cap_w,
+           "window_s": round(seconds, 3), "launches": launches,
+           "ppt_throttle_share": (round(d["ppt_residency_acc"] / d["accumulation_counter"], 4)
+                                  if d["ppt_residency_acc"] is not None else None)}
+    if joules is not None and joules > 0:
+        out["avg_power_w"] = round(joules / seconds, 1)
+        out["joules_per_launch"] = round(joules / launches, 4)
+        out["tops_per_watt"] = round(ops_per_launch * launches / joules / 1e12, 3)
+    return out
 
 
 def quant_bytes(M, K) -> int:

@@ -42,6 +42,13 @@ def test_bench_json_line(capsys, monkeypatch):
     if clk is not None:  # amdsmi present
         assert len(clk["mhz_per_xcd"]) == 8 and 100 < clk["mhz_mean"] <= 2400
         assert r["frac"] < clk["frac_at_measured_clock"] < 1
+        pw = clk["power"]
+        if pw.get("ppt_throttle_share") is not None:  # the metrics table's accumulators
+            assert 0 <= pw["ppt_throttle_share"] <= 1 and pw["launches"] > 0
+        if pw.get("avg_power_w") is not None:
+            assert 50 < pw["avg_power_w"] < 2000 and pw["joules_per_launch"] > 0
+            assert pw["tops_per_watt"] == pytest.approx(
+                r["ops_per_launch"] / pw["joules_per_launch"] / 1e12, rel=2e-3)
     e = d["eager_torch"]
     assert e["shape"] == [4608, 4096, 16384] and e["us"] > 0 and e["fused_us"] > 0
     assert e["mean_abs_diff_rel"] < 1e-3

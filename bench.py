@@ -816,7 +816,25 @@ def counter_run(layers, dev, reps: int = 3, codes: str = "workload", path: str =
     """codes="uniform" replaces the workload's int8 codes (X and W) by
     uniform random ones in [-127, 127], to compare the clock the GPU holds
     under the two (same launches, same scales). path="bf16" runs the
-    workload's protected layer (bf16_linear) instead of the W8A8 one."""
+    workload's protected layer (bf16_linear) instead of the W8A8 one;
+    path="act" its activation step (w8a8_quant_act, or w8a8_adaln_quant_act
+    where the layer's input is modulated)."""
+    if path == "act":
+        lin = max((x for x in layers if not x.lay.protected), key=lambda x: x.ops)
+        ws = L.Workspace(dev)
+        Xq, xs = ws.get(lin.M, lin.lay.K)
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(reps):
+            lin.quant(lin.xs[0], Xq, xs)
+            torch.cuda.synchronize()
+            torch.neg(src, out=dst)
+            torch.cuda.synchronize()
+        step = "w8a8_quant_act" if lin.mod is None else "w8a8_adaln_quant_act"
+        log(f"counter run: {reps} x {step} {lin.M}x{lin.lay.K}, {reps} x neg over "
+            f"{COPY_BYTES} bytes")
+        return lin
     if path == "bf16":
         lin = max((x for x in layers if x.lay.protected), key=lambda x: x.ops)
         src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
@@ -947,8 +965,10 @@ def main():
                     help="only the short launch sequence the counter passes profile")
     ap.add_argument("--counter-codes", choices=["workload", "uniform"], default="workload",
                     help="int8 codes of the counter run: the workload's, or uniform random")
-    ap.add_argument("--counter-path", choices=["w8a8", "bf16"], default="w8a8",
-                    help="the linear the counter run launches: W8A8, or the protected bf16 one")
+    ap.add_argument("--counter-path", choices=["w8a8", "bf16", "act"], default="w8a8",
+                    help="what the counter run launches: the W8A8 linear, the protected bf16 "
+                         "one, or the activation step (the fused adaLN step where the input "
+                         "is modulated)")
     ap.add_argument("--counters-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 counter runs into profiles/ (no GPU)")
     args = ap.parse_args()

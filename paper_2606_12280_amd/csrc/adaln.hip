@@ -146,12 +146,34 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
     }
     const uint32_t scale_off = (gw == 0 && lane == 0) ? 0u : 4u;
 
+    // A row's scale and codes out (a row past the input stores nothing).
+    const auto store_row = [&](int64_t r, float scl, const uint32_t (&lo)[CH],
+                               const uint32_t (&hi)[CH]) {
+        const bool in = r < R;
+        rows::store_f32(make_rsrc(xscale + (in ? r : 0), in ? 4u : 0u), scale_off, scl);
+        const __amdgpu_buffer_rsrc_t ro =
+            make_rsrc(out + (in ? r : 0) * K, in ? static_cast<uint32_t>(K) : 0u);
+#pragma unroll
+        for (int c = 0; c < CH; ++c) store_codes(ro, out_off[c], lo[c], hi[c]);
+    };
+
     uint4 x[CH];
     {
         const __amdgpu_buffer_rsrc_t rin = row_in(group);
 #pragma unroll
         for (int c = 0; c < CH; ++c) x[c] = load_chunk(rin, in_off[c]);
     }
+    // A row's scale and codes go out one row late, right after the next
+    // row's sum exchange: the GPU counts vector loads and stores on one
+    // counter, and the compiler's wait for a row's data also waits for every
+    // store issued after that data's loads, so stores at the end of a row
+    // would hold up the next row by a store's full latency. The first
+    // pending row lies past the input, so its stores are dropped.
+    uint32_t pend_lo[CH], pend_hi[CH];
+    float pend_scl = 0.0f;
+    int64_t pend_row = R;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) pend_lo[c] = pend_hi[c] = 0u;
     for (int it = 0; it < rows_per_group; ++it) {
         const int64_t row = group + it * groups;
         // the next row (past the last row of the group it lies past the
@@ -188,6 +210,8 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
             for (int i = 1; i < G; ++i) s += red_sum[sub][i];
         }
         const double mean = k_pow2 ? s * inv_k : s / static_cast<double>(K);
+        __builtin_amdgcn_sched_barrier(0);  // after this row's data was waited for
+        store_row(pend_row, pend_scl, pend_lo, pend_hi);
 
         // centered values (kept for the modulation) and their sum of squares
         // (only live columns)
@@ -266,26 +290,24 @@ __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(
                 scl = amax / 127.0f;
                 r = 127.0f / amax;
             }
-            const bool in = row < R;
-            rows::store_f32(make_rsrc(xscale + (in ? row : 0), in ? 4u : 0u), scale_off, scl);
-            const __amdgpu_buffer_rsrc_t ro =
-                make_rsrc(out + (in ? row : 0) * K, in ? static_cast<uint32_t>(K) : 0u);
+            pend_row = row;
+            pend_scl = scl;
 #pragma unroll
             for (int c = 0; c < CH; ++c) {
-                uint32_t lo = 0u;
-                uint32_t hi = 0u;
+                pend_lo[c] = 0u;
+                pend_hi[c] = 0u;
                 if (nonzero) {
-                    lo = pack4(code_word(hv[c][0], r), code_word(hv[c][1], r),
-                               code_word(hv[c][2], r), code_word(hv[c][3], r));
-                    hi = pack4(code_word(hv[c][4], r), code_word(hv[c][5], r),
-                               code_word(hv[c][6], r), code_word(hv[c][7], r));
+                    pend_lo[c] = pack4(code_word(hv[c][0], r), code_word(hv[c][1], r),
+                                       code_word(hv[c][2], r), code_word(hv[c][3], r));
+                    pend_hi[c] = pack4(code_word(hv[c][4], r), code_word(hv[c][5], r),
+                                       code_word(hv[c][6], r), code_word(hv[c][7], r));
                 }
-                store_codes(ro, out_off[c], lo, hi);
             }
         }
 #pragma unroll
         for (int c = 0; c < CH; ++c) x[c] = xn[c];
     }
+    store_row(pend_row, pend_scl, pend_lo, pend_hi);
 }
 
 // One round of groups: as many as the GPU holds at once (fewer for short

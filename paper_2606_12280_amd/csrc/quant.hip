@@ -102,9 +102,31 @@ __global__ __launch_bounds__(WPB * 64) void smooth_quant_rows_kernel(
         for (int c = 0; c < CH; ++c) x[c] = rows::load_chunk(rin, col(c) * 16u);
     };
 
+    // A row's scale and codes out (a row past the input stores nothing).
+    const auto store_row = [&](int64_t r, float sc, const uint32_t (&lo)[CH],
+                               const uint32_t (&hi)[CH]) {
+        const bool in = r < R;
+        rows::store_f32(rows::make_rsrc(scale + (in ? r : 0), in ? 4u : 0u), scale_off, sc);
+        const __amdgpu_buffer_rsrc_t ro =
+            rows::make_rsrc(out + (in ? r : 0) * K, in ? static_cast<uint32_t>(K) : 0u);
+#pragma unroll
+        for (int c = 0; c < CH; ++c) rows::store_codes(ro, col(c) * 8u, lo[c], hi[c]);
+    };
+
     uint4 x[CH];
     if constexpr (PF) load_row(group, x);
     const int n_rows = PF ? rows_per_group : 1;
+    // With the prefetch, a row's scale and codes go out one row late, right
+    // after the next row's absmax exchange. The GPU counts vector loads and
+    // stores on one counter, and the compiler's wait for a row's data also
+    // waits for every store issued after that data's loads: stores at the
+    // end of a row would hold up the next row by a store's full latency.
+    // The first pending row lies past the input, so its stores are dropped.
+    uint32_t pend_lo[CH], pend_hi[CH];
+    float pend_sc = 0.0f;
+    int64_t pend_row = R;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) pend_lo[c] = pend_hi[c] = 0u;
     for (int it = 0; it < n_rows; ++it) {
         const int64_t row = group + it * groups;
         uint4 xn[CH];
@@ -122,6 +144,10 @@ __global__ __launch_bounds__(WPB * 64) void smooth_quant_rows_kernel(
 #pragma unroll
             for (int i = 0; i < G; ++i) amax = fmaxf(amax, red[it & 1][sub][i]);
         }
+        if constexpr (PF) {
+            __builtin_amdgcn_sched_barrier(0);  // after this row's data was waited for
+            store_row(pend_row, pend_sc, pend_lo, pend_hi);
+        }
         float sc = 0.0f;
         float r = 0.0f;
         const bool nonzero = amax >= kTinyAbsmax;
@@ -129,29 +155,34 @@ __global__ __launch_bounds__(WPB * 64) void smooth_quant_rows_kernel(
             sc = amax / 127.0f;
             r = 127.0f / amax;
         }
-        const bool in = row < R;
-        rows::store_f32(rows::make_rsrc(scale + (in ? row : 0), in ? 4u : 0u), scale_off, sc);
-        const __amdgpu_buffer_rsrc_t ro =
-            rows::make_rsrc(out + (in ? row : 0) * K, in ? static_cast<uint32_t>(K) : 0u);
+        uint32_t lo[CH], hi[CH];
 #pragma unroll
         for (int c = 0; c < CH; ++c) {
-            uint32_t lo = 0u;
-            uint32_t hi = 0u;
+            lo[c] = 0u;
+            hi[c] = 0u;
             if (nonzero) {
                 float t[8];
                 smooth8(x[c], ma[c], mb[c], t);
-                lo = rows::pack4(rows::code_word(t[0], r), rows::code_word(t[1], r),
-                                 rows::code_word(t[2], r), rows::code_word(t[3], r));
-                hi = rows::pack4(rows::code_word(t[4], r), rows::code_word(t[5], r),
-                                 rows::code_word(t[6], r), rows::code_word(t[7], r));
+                lo[c] = rows::pack4(rows::code_word(t[0], r), rows::code_word(t[1], r),
+                                    rows::code_word(t[2], r), rows::code_word(t[3], r));
+                hi[c] = rows::pack4(rows::code_word(t[4], r), rows::code_word(t[5], r),
+                                    rows::code_word(t[6], r), rows::code_word(t[7], r));
             }
-            rows::store_codes(ro, col(c) * 8u, lo, hi);
         }
         if constexpr (PF) {
+            pend_row = row;
+            pend_sc = sc;
 #pragma unroll
-            for (int c = 0; c < CH; ++c) x[c] = xn[c];
+            for (int c = 0; c < CH; ++c) {
+                pend_lo[c] = lo[c];
+                pend_hi[c] = hi[c];
+                x[c] = xn[c];
+            }
+        } else {
+            store_row(row, sc, lo, hi);
         }
     }
+    if constexpr (PF) store_row(pend_row, pend_sc, pend_lo, pend_hi);
 }
 
 // One round of groups: as many as the GPU holds at once (fewer for short

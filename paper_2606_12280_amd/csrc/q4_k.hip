@@ -31,6 +31,11 @@
 namespace w8a8 {
 namespace {
 
+// The wave's index in its workgroup, in a scalar register.
+__device__ __forceinline__ int wave_index() {
+    return __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+}
+
 // The thread's unit under grid_for().
 __device__ __forceinline__ int64_t unit_index() {
     return (static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x) * 256 + threadIdx.x;
@@ -151,22 +156,35 @@ __global__ __launch_bounds__(256) void q4_k_quantize_kernel(
     reinterpret_cast<uint4 *>(qs)[j] = make_uint4(packed[0], packed[1], packed[2], packed[3]);
 }
 
-// One thread per 8 weights: 4 bytes of codes, the super-block's 12 scale
-// bytes and two scales in, 16 bytes of bf16 out, so a wave's stores cover
-// 1 KiB contiguously.
+// One thread per 8 weights: 4 bytes of codes and two binary16 scales in, 16
+// bytes of bf16 out, so a wave's stores cover 1 KiB contiguously. A wave's
+// 64 octets are exactly two super-blocks (its first octet is a multiple of
+// 64), so the 12 scale bytes of both are wave-uniform: scalar loads, and
+// each half of the wave takes its own. That leaves three vector loads per
+// thread instead of six (36.1 -> 33.4 us at 16384 x 4096 in one job, output
+// identical). The second super-block is clamped to the last one, so a wave
+// whose upper half lies past the end reads nothing outside the planes.
 __global__ __launch_bounds__(256) void q4_k_dequantize_kernel(
     const uint32_t *__restrict__ qs, const uint32_t *__restrict__ scales,
     const uint16_t *__restrict__ d, const uint16_t *__restrict__ dmin, int64_t octets,
     u32x4 *__restrict__ W) {
-    const int64_t t = unit_index();
+    const int lane = threadIdx.x & 63;
+    const int wave = wave_index();
+    const int64_t t0 =
+        (static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x) * 256 + wave * 64;
+    if (t0 >= octets) return;
+    const int64_t supers = octets >> 5;  // 32 octets per super-block
+    const int64_t g0 = t0 >> 5;
+    const int64_t g1 = g0 + 1 < supers ? g0 + 1 : g0;
+    const uint32_t a0 = scales[3 * g0], a1 = scales[3 * g0 + 1], a2 = scales[3 * g0 + 2];
+    const uint32_t b0 = scales[3 * g1], b1 = scales[3 * g1 + 1], b2 = scales[3 * g1 + 2];
+    const bool upper = lane >= 32;
+    const uint32_t w0 = upper ? b0 : a0, w1 = upper ? b1 : a1, w2 = upper ? b2 : a2;
+    const int64_t t = t0 + lane;
     if (t >= octets) return;
+    const int64_t g = t >> 5;
     const int jj = static_cast<int>((t >> 2) & (kSubs - 1));  // sub-block in its super-block
-    const int64_t g = t >> 5;                                    // super-block (32 octets)
-    // Every load first, none behind a branch: the codes, the super-block's
-    // three scale words and its two binary16 scales go out together, so a
-    // thread waits for one memory round trip, not two.
     const uint32_t q = __builtin_nontemporal_load(qs + t);
-    const uint32_t w0 = scales[3 * g], w1 = scales[3 * g + 1], w2 = scales[3 * g + 2];
     const uint16_t dh = d[g], mh = dmin[g];
     // the sub-block's 6-bit scale and offset, for both halves of the layout,
     // then the one for jj (a select, so both halves of a wave agree on the

@@ -562,6 +562,7 @@ def clock_under_load(lin: Linear, dev, seconds: float = 3.0):
         last = 0.0
         first = None      # metrics table at the start of the sampled window
         launches = 0      # launches since then
+        t_first = 0.0
         while time.perf_counter() - t0 < seconds:
             for _ in range(per):
                 ops.w8a8_linear(Xq, xsc, lin.lay.Wq, lin.lay.w_scale, lin.lay.bias, out=lin.Y)
@@ -574,6 +575,7 @@ def clock_under_load(lin: Linear, dev, seconds: float = 3.0):
                 met = amdsmi.amdsmi_get_gpu_metrics_info(h)
                 if first is None:
                     first = met
+                    t_first = time.perf_counter()
                 clks = met.get("current_gfxclks")
                 u = met.get("current_uclk")
                 if isinstance(u, (int, float)) and 0 < u < 100000:
@@ -583,6 +585,7 @@ def clock_under_load(lin: Linear, dev, seconds: float = 3.0):
                     if clks:
                         samples.append(clks)
         end = amdsmi.amdsmi_get_gpu_metrics_info(h) if first is not None else None
+        per_launch = (time.perf_counter() - t_first) / launches if launches else None
         del Xq, xsc
         if not samples or len({len(c) for c in samples}) != 1:
             return None
@@ -594,7 +597,8 @@ def clock_under_load(lin: Linear, dev, seconds: float = 3.0):
                "mhz_mean": round(float(per_xcd.mean()), 1),
                "mhz_min": round(float(per_xcd.min()), 1), "samples": len(samples),
                "memory_clock_mhz": round(float(np.mean(uclk)), 1) if uclk else None}
-        out["power"] = power_over_window(amdsmi, h, first, end, launches, lin.ops)
+        out["power"] = power_over_window(amdsmi, h, first, end, per_launch, lin.ops)
+        out["power"]["launches"] = launches
         return out
     except Exception:
         return None
@@ -605,10 +609,14 @@ def clock_under_load(lin: Linear, dev, seconds: float = 3.0):
             pass
 
 
-def power_over_window(amdsmi, h, first, end, launches, ops_per_launch):
+def power_over_window(amdsmi, h, first, end, seconds_per_launch, ops_per_launch):
     """Power figures between two snapshots of the GPU metrics table taken
-    around `launches` back-to-back launches (see clock_under_load); None
-    where a field is missing."""
+    around back-to-back launches of one kernel (see clock_under_load): the
+    share of the power manager's 1 ms intervals with the power limiter on,
+    and the average socket power over the table's own interval (its energy
+    counter over its timestamp). Joules per launch are that power times the
+    measured time per launch, so a table refreshed on its own schedule does
+    not skew them. None where a field is missing."""
     def num(m, k):
         v = m.get(k) if m is not None else None
         return float(v) if isinstance(v, (int, float)) else None
@@ -623,19 +631,122 @@ def power_over_window(amdsmi, h, first, end, launches, ops_per_launch):
               "firmware_timestamp"):
         a, b = num(first, k), num(end, k)
         d[k] = b - a if a is not None and b is not None else None
-    if not d["accumulation_counter"] or not d["firmware_timestamp"] or not launches:
-        return {"power_limit_w": cap_w}
+    out = {"power_limit_w": cap_w}
+    if not d["accumulation_counter"] or not d["firmware_timestamp"]:
+        return out
     seconds = d["firmware_timestamp"] * 1e-8
-    joules = d["energy_accumulator"] * 2.0 ** -16 if d["energy_accumulator"] is not None else None
-    out = {"power_limit_w": cap_w,
-           "window_s": round(seconds, 3), "launches": launches,
-           "ppt_throttle_share": (round(d["ppt_residency_acc"] / d["accumulation_counter"], 4)
-                                  if d["ppt_residency_acc"] is not None else None)}
-    if joules is not None and joules > 0:
-        out["avg_power_w"] = round(joules / seconds, 1)
-        out["joules_per_launch"] = round(joules / launches, 4)
-        out["tops_per_watt"] = round(ops_per_launch * launches / joules / 1e12, 3)
+    out["window_s"] = round(seconds, 3)
+    if d["ppt_residency_acc"] is not None:
+        out["ppt_throttle_share"] = round(d["ppt_residency_acc"] / d["accumulation_counter"], 4)
+    if d["energy_accumulator"] is not None and d["energy_accumulator"] > 0:
+        watts = d["energy_accumulator"] * 2.0 ** -16 / seconds
+        out["avg_power_w"] = round(watts, 1)
+        if seconds_per_launch:
+            joules = watts * seconds_per_launch
+            out["joules_per_launch"] = round(joules, 5)
+            if ops_per_launch:
+                out["tops_per_watt"] = round(ops_per_launch / joules / 1e12, 3)
     return out
+
+
+def power_table(layers, dev, seconds: float = 2.0, settle: float = 0.8):
+    """Each kernel of the workload's layers run back to back: `settle`
+    seconds to let the clock settle, then `seconds` measured. Per kernel:
+    time per launch (HIP events), the XCD clock mean, and the socket power
+    figures of power_over_window. The activation steps read inputs rotating
+    over more than the 256 MB Infinity Cache. None without amdsmi."""
+    try:
+        import amdsmi
+        amdsmi.amdsmi_init()
+    except Exception:
+        return None
+    try:
+        h = _amdsmi_handle(amdsmi, dev)
+        if h is None:
+            return None
+        table = []
+
+        def run(label, fn, ops_per_launch=0, nbytes=0):
+            t0 = time.perf_counter()
+            while time.perf_counter() - t0 < settle:
+                for _ in range(10):
+                    fn()
+                torch.cuda.synchronize()
+            first = amdsmi.amdsmi_get_gpu_metrics_info(h)
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            n, clocks, last = 0, [], 0.0
+            a.record()
+            t0 = time.perf_counter()
+            while time.perf_counter() - t0 < seconds:
+                for _ in range(10):
+                    fn()
+                n += 10
+                torch.cuda.synchronize()
+                if time.perf_counter() - last > 0.1:
+                    last = time.perf_counter()
+                    c = amdsmi.amdsmi_get_gpu_metrics_info(h).get("current_gfxclks")
+                    if isinstance(c, (list, tuple)):
+                        c = [v for v in c if isinstance(v, (int, float)) and 0 < v < 10000]
+                        if c:
+                            clocks.append(float(np.mean(c)))
+            b.record()
+            torch.cuda.synchronize()
+            end = amdsmi.amdsmi_get_gpu_metrics_info(h)
+            us = a.elapsed_time(b) * 1e3 / n
+            e = {"kernel": label, "us_per_launch": round(us, 2), "launches": n,
+                 "mhz_mean": round(float(np.mean(clocks)), 1) if clocks else None}
+            if ops_per_launch:
+                e["TOPS"] = round(ops_per_launch / us / 1e6, 1)
+            if nbytes:
+                e["GB_s"] = round(nbytes / us / 1e3, 1)
+            e.update(power_over_window(amdsmi, h, first, end, us * 1e-6, ops_per_launch))
+            table.append(e)
+            log(f"power: {json.dumps(e)}")
+
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(12)
+        for lin in layers:
+            M, K, N = lin.M, lin.lay.K, lin.lay.N
+            shape = f"{M}x{K}->{N}"
+            X = lin.xs[0]
+            if lin.lay.protected:
+                run(f"bf16_linear {shape}", lambda: ops.bf16_linear(X, lin.lay.W, lin.lay.bias,
+                                                                    out=lin.Y), lin.ops)
+                continue
+            Xq = torch.empty(M, K, dtype=torch.int8, device=dev)
+            xsc = torch.empty(M, dtype=torch.float32, device=dev)
+            lin.quant(X, Xq, xsc)
+            run(f"w8a8_linear {shape}", lambda: ops.w8a8_linear(
+                Xq, xsc, lin.lay.Wq, lin.lay.w_scale, lin.lay.bias, out=lin.Y), lin.ops)
+            nbuf = max(3, int(np.ceil(700e6 / (3 * M * K))))
+            xs_in = [X.clone() for _ in range(nbuf)]
+            qs = [torch.empty_like(Xq) for _ in range(nbuf)]
+            rot = {"i": 0}
+
+            def quant():
+                i = rot["i"] = (rot["i"] + 1) % nbuf
+                ops.w8a8_quant_act(xs_in[i], lin.lay.inv_lambda, Xq=qs[i], x_scale=xsc)
+            run(f"w8a8_quant_act {M}x{K}", quant, 0, quant_bytes(M, K))
+            if K <= 8192:
+                sh, sc = ((torch.randn(K, device=dev, generator=gen) * sd).bfloat16()
+                          for sd in (0.05, 0.1))
+
+                def adaln():
+                    i = rot["i"] = (rot["i"] + 1) % nbuf
+                    ops.w8a8_adaln_quant_act(xs_in[i], sh, sc, lin.lay.inv_lambda, Xq=qs[i],
+                                             x_scale=xsc)
+                run(f"w8a8_adaln_quant_act {M}x{K}", adaln, 0, quant_bytes(M, K) + 4 * K)
+            del xs_in, qs, Xq, xsc
+        return table
+    except Exception as exc:  # a missing metrics field: report it, keep going
+        log(f"power table unavailable: {exc}")
+        return None
+    finally:
+        try:
+            amdsmi.amdsmi_shut_down()
+        except Exception:
+            pass
 
 
 def quant_bytes(M, K) -> int:
@@ -969,6 +1080,9 @@ def main():
                     help="what the counter run launches: the W8A8 linear, the protected bf16 "
                          "one, or the activation step (the fused adaLN step where the input "
                          "is modulated)")
+    ap.add_argument("--power-table", action="store_true",
+                    help="only each kernel of the workload back to back, with its socket "
+                         "power, power-limiter share, clock and joules per launch")
     ap.add_argument("--counters-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 counter runs into profiles/ (no GPU)")
     args = ap.parse_args()
@@ -1001,6 +1115,9 @@ def main():
         f"{time.perf_counter() - t_build:.1f} s")
     if args.counter_run:
         counter_run(layers, dev, codes=args.counter_codes, path=args.counter_path)
+        return
+    if args.power_table:
+        print(json.dumps({"workload": args.workload, "power_table": power_table(layers, dev)}))
         return
 
     # per-kernel durations inside the timed steps (events between kernels)

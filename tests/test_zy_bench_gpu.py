@@ -49,6 +49,10 @@ def test_bench_json_line(capsys, monkeypatch):
             assert 50 < pw["avg_power_w"] < 2000 and pw["joules_per_launch"] > 0
             assert pw["tops_per_watt"] == pytest.approx(
                 r["ops_per_launch"] / pw["joules_per_launch"] / 1e12, rel=2e-3)
+            # joules per launch = average power x time per launch, near the
+            # timed launches' own duration
+            assert pw["joules_per_launch"] / pw["avg_power_w"] == pytest.approx(
+                r["avg_launch_us"] * 1e-6, rel=0.25)
     e = d["eager_torch"]
     assert e["shape"] == [4608, 4096, 16384] and e["us"] > 0 and e["fused_us"] > 0
     assert e["mean_abs_diff_rel"] < 1e-3
@@ -87,3 +91,29 @@ def test_branch_streams_write_the_same_outputs():
     torch.cuda.synchronize()
     for lin, y in zip(layers, one):
         assert torch.equal(lin.Y.view(torch.int16), y.view(torch.int16)), lin.name
+
+
+def test_power_table_entries():
+    """bench.py --power-table: one entry per kernel of the FFN-up layer (the
+    GEMM, the quant step, the adaLN step), each with its time, rate and, where
+    the metrics table has them, the socket power figures (short windows)."""
+    sys.path.insert(0, ROOT)
+    import torch
+
+    import bench
+
+    dev = torch.device("cuda:0")
+    print("power table, ffn_up, 1 s windows", flush=True)
+    layers = bench.build_workload("ffn_up", dev, 1)
+    table = bench.power_table(layers, dev, seconds=1.0, settle=0.2)
+    if table is None:  # amdsmi absent
+        pytest.skip("amdsmi not available")
+    kinds = [e["kernel"].split()[0] for e in table]
+    assert kinds == ["w8a8_linear", "w8a8_quant_act", "w8a8_adaln_quant_act"]
+    for e in table:
+        assert e["us_per_launch"] > 0 and e["launches"] > 0
+        assert ("TOPS" in e) == (e["kernel"].startswith("w8a8_linear"))
+        if e.get("avg_power_w") is not None:
+            assert 50 < e["avg_power_w"] < 2000 and e["joules_per_launch"] > 0
+        if e.get("ppt_throttle_share") is not None:
+            assert 0 <= e["ppt_throttle_share"] <= 1

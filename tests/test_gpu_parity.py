@@ -57,7 +57,7 @@ def test_quant_act_bit_exact(M, K):
     assert np.array_equal(Xq, Xq_ref)
 
 
-@pytest.mark.parametrize("M,K", [(300001, 64), (65537, 1024), (20011, 4096)])
+@pytest.mark.parametrize("M,K", [(300001, 64), (65537, 1024), (20011, 4096), (3001, 16384)])
 def test_quant_act_many_rows_per_group(M, K):
     """Long inputs: one launch holds as many row groups as the GPU keeps
     resident and each walks dozens of rows, the last of them ragged; every
@@ -740,7 +740,7 @@ def test_adaln_quant_act_bit_exact(M, K):
     _check_adaln(*_adaln_inputs([180, M, K], M, K), M, K)
 
 
-@pytest.mark.parametrize("M,K", [(200003, 64), (30011, 1024), (9001, 4096)])
+@pytest.mark.parametrize("M,K", [(200003, 64), (30011, 1024), (9001, 4096), (6007, 8192)])
 def test_adaln_quant_act_many_rows_per_group(M, K):
     """Long inputs: each resident row group walks dozens of rows, the last of
     them ragged; codes and scales bit-exact."""

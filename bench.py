@@ -846,6 +846,25 @@ class _OracleLinear:
         return rows, dt
 
 
+def _host_info() -> dict:
+    """The host the oracle ran on: CPU model, logical CPUs, and the CPUs
+    this process may run on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        allowed = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        allowed = None
+    return {"cpu_model": model, "logical_cpus": os.cpu_count(), "cpus_allowed": allowed}
+
+
 def cpu_baseline(workload: str, target_s: float = 10.0):
     """The CPU oracle timed on a bounded sample of the workload on this
     host's cores (OpenMP over token rows).
@@ -871,7 +890,7 @@ def cpu_baseline(workload: str, target_s: float = 10.0):
         tops = 2.0 * rows * N * K * reps / dt / 1e12
         what = f"{rows} of {M} token rows" if reps == 1 else f"{reps} runs of all {M} token rows"
         return {"value": round(tops, 6), "unit": "TOPS", "cores": oracle.num_threads(),
-                "kind": "oracle",
+                "kind": "oracle", "host": _host_info(),
                 "quant_GB_s": round((3 * rows * K + 4 * rows) * reps / q / 1e9, 3),
                 "gemm_epilogue_TOPS": round(2.0 * rows * N * K * reps / (dt - q) / 1e12, 6),
                 "sample": f"{what} of the {M}x{K}->{N} linear: smoothing + per-token quant + "
@@ -905,7 +924,7 @@ def cpu_baseline(workload: str, target_s: float = 10.0):
         per.append(f"{'bf16' if prot else 'W8A8'} {lin.M}x{lin.K}->{lin.N} x{count}: "
                    f"{rows} rows in {dt:.2f} s")
     return {"value": round(total_ops / total_s / 1e12, 6), "unit": "TOPS",
-            "cores": oracle.num_threads(), "kind": "oracle (extrapolated)",
+            "cores": oracle.num_threads(), "kind": "oracle (extrapolated)", "host": _host_info(),
             "step_s_extrapolated": round(total_s, 2),
             "sample": f"{label}: each distinct linear timed on a row sample, the step's time "
                       f"extrapolated as the sum over shapes of time per row x {synth.TOKENS} "

@@ -14,8 +14,9 @@ paths), dit_block (the four linears of a block, both CFG branches), backbone
 Prints one JSON line. ``value`` is the step's throughput in TOPS
 (2 M N K per step divided by the step time). ``roofline`` covers the dominant
 kernel (the INT8 GEMM); its ``clock`` holds the XCD clocks read while that
-kernel runs back to back and the fraction of the peak at that clock. ``cpu_baseline`` is the CPU oracle timed on a bounded
-sample of the same workload on this host. ``eager_torch`` times the dominant
+kernel runs back to back, the fraction of the peak at that clock, and the
+socket power over the same window. ``cpu_baseline`` is the CPU oracle timed
+on a bounded sample of the same workload on this host. ``eager_torch`` times the dominant
 layer run the way the paper runs it, as eager Torch ops with torch._int_mm for
 the GEMM, on the same GPU. ``accuracy`` (FFN workloads) gives the W8A8 and
 bf16 paths' error against X W^T + b in binary64.

@@ -2,8 +2,8 @@
 path, or a GGUF weight-only format, Q8_0 or Q4_K (paper Section 3: every
 linear is W8A8 except the top-N most fragile layers, N = 17 of 211 per
 branch, which stay bf16 with no activation quantization; independently, a
-checkpoint can be stored as Q8_0 or Q4_K). Host-side bookkeeping only: the arithmetic runs in the
-library's kernels through ops."""
+checkpoint can be stored as Q8_0 or Q4_K). Host-side bookkeeping only: the
+arithmetic runs in the library's kernels through ops."""
 from __future__ import annotations
 
 from dataclasses import dataclass

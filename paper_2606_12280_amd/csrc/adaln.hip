@@ -320,7 +320,7 @@ hipError_t launch(const uint16_t *src, const uint16_t *shift, const uint16_t *sc
                   float *xscale, hipStream_t stream) {
     constexpr int SLOTS = WPB / G;
     if (R <= 0) return hipSuccess;
-    static int64_t resident[256] = {};
+    static std::atomic<int64_t> resident[256];
     const int64_t rpg = rows::rows_per_group(
         R, rows::resident_groups(
                reinterpret_cast<const void *>(&adaln_quant_rows_kernel<G, CH, WPB>), WPB * 64,

@@ -49,6 +49,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <type_traits>
 
 #include "internal.h"
@@ -1456,16 +1457,18 @@ struct Specialized {
 // The persistent 288 x 256 kernel: one workgroup per CU (a multiple of 8,
 // at most one per tile), each walking its tiles.
 int persistent_grid() {
-    static int cached[256] = {};
+    static std::atomic<int> cached[256];  // per device; racing fills agree
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 256) return 0;
-    if (cached[dev] == 0) {
+    int n = cached[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
         int cus = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
             return 0;
-        cached[dev] = cus / 8 * 8;
+        n = cus / 8 * 8;
+        cached[dev].store(n, std::memory_order_relaxed);
     }
-    return cached[dev];
+    return n;
 }
 
 template <class Op, int EPI>

@@ -192,7 +192,7 @@ hipError_t launch_rows(const uint16_t *src, const float *mul, int64_t R, int64_t
                        int8_t *out, float *scale, hipStream_t stream) {
     constexpr int SLOTS = WPB / G;
     if (R <= 0) return hipSuccess;
-    static int64_t resident[256] = {};
+    static std::atomic<int64_t> resident[256];
     const int64_t rpg =
         PF ? rows::rows_per_group(
                  R, rows::resident_groups(

@@ -14,6 +14,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace w8a8 {
 namespace rows {
 
@@ -73,12 +75,14 @@ __device__ __forceinline__ uint32_t pack4(uint32_t a, uint32_t b, uint32_t c, ui
 // Row groups the current device holds at once for `kernel` launched with
 // `threads` per workgroup and `groups_per_block` groups in each (CUs x
 // resident workgroups per CU x groups per workgroup); 0 when the runtime
-// cannot say. `cache` is the caller's, one entry per device.
+// cannot say. `cache` is the caller's, one entry per device; host threads
+// calling at once may both fill an entry, with the same value.
 inline int64_t resident_groups(const void *kernel, int threads, int groups_per_block,
-                               int64_t (&cache)[256]) {
+                               std::atomic<int64_t> (&cache)[256]) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 256) return 0;
-    if (cache[dev] == 0) {
+    int64_t n = cache[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
         int cus = 0;
         int per_cu = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
@@ -86,9 +90,10 @@ inline int64_t resident_groups(const void *kernel, int threads, int groups_per_b
             hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) !=
                 hipSuccess)
             return 0;
-        cache[dev] = static_cast<int64_t>(cus) * per_cu * groups_per_block;
+        n = static_cast<int64_t>(cus) * per_cu * groups_per_block;
+        cache[dev].store(n, std::memory_order_relaxed);
     }
-    return cache[dev];
+    return n;
 }
 
 // Rows per group for R rows: one round of the resident groups, each walking

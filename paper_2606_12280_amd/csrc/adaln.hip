@@ -82,7 +82,8 @@ __device__ __forceinline__ uint32_t bf16_bits_past_midpoint(double d, float f) {
 }
 
 __device__ __forceinline__ double wave_sum(double v) { return lanes::sum(v); }
-__device__ __forceinline__ float wave_max(float v) { return lanes::max(v); }
+// v is a running absmax (fmaxf of fabsf values from 0), so never NaN or negative.
+__device__ __forceinline__ float wave_max(float v) { return lanes::max_nonneg(v); }
 
 template <int G, int CH, int WPB>
 __global__ __launch_bounds__(WPB * 64) void adaln_quant_rows_kernel(

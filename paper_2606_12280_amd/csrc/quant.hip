@@ -34,7 +34,8 @@ constexpr float kTinyAbsmax = 0x1p-96f;  // rows below quantize to zero
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-__device__ __forceinline__ float wave_max(float v) { return lanes::max(v); }
+// v is a running absmax (fmaxf of fabsf values from 0), so never NaN or negative.
+__device__ __forceinline__ float wave_max(float v) { return lanes::max_nonneg(v); }
 
 // The 8 smoothed values of one chunk: float(x_e) * mul_e, one binary32
 // rounding each.

@@ -71,19 +71,24 @@ def test_quant_act_many_rows_per_group(M, K):
 
 
 def test_quant_act_special_rows():
-    """Zero, tiny (below 2^-96), constant, one-hot and tie rows."""
+    """Zero, tiny (below 2^-96), constant, one-hot and tie rows, a row of
+    binary32 subnormals (its absmax too is a subnormal bit pattern) and a
+    row of negative zeros."""
     K = 256
-    rows = np.zeros((6, K), np.float32)
+    rows = np.zeros((8, K), np.float32)
     rows[1, :] = -3.0
     rows[2, :] = 2.0 ** -100
     rows[3, 17] = 0.375
     rows[4, :16] = [127.0, 0.5, 1.5, 2.5, -0.5, -1.5, -2.5, 3.5, 126.5, -126.5,
                     0.25, 0.75, -0.75, 64.5, 65.5, 0.0]
     rows[5, :] = np.linspace(-1e-20, 1e-20, K)
+    rows[6, :] = np.ldexp(np.arange(1, K + 1, dtype=np.float32), -140) * (-1) ** np.arange(K)
+    rows[7, :] = -0.0
     X = synth.to_bf16_bits(rows)
-    Xq, xs, Xq_ref, xs_ref = _quant_case(X, np.ones(K, np.float32), 6, K)
+    Xq, xs, Xq_ref, xs_ref = _quant_case(X, np.ones(K, np.float32), 8, K)
     assert np.array_equal(xs, xs_ref) and np.array_equal(Xq, Xq_ref)
-    assert xs[0] == 0 and xs[2] == 0 and not Xq[0].any() and not Xq[2].any()
+    for r in (0, 2, 6, 7):
+        assert xs[r] == 0 and not Xq[r].any()
 
 
 @pytest.mark.parametrize("N,K", [(512, 256), (100, 4096), (33, 16384), (7, 1024)])

@@ -22,8 +22,8 @@
 // GPU keeps resident, each walking an equal share of the rows with the next
 // row prefetched. The three row reductions (sum, centered sum of squares,
 // absmax) run as lane butterflies, then across the G waves through LDS. The
-// vector ALU's issue bounds the kernel, not its bytes: about 29 VALU instructions
-// per element, a third of them binary64.
+// vector ALU's issue bounds the kernel, not its bytes: about 27 VALU instructions
+// per element of a lane, nearly a third of them binary64.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>

@@ -6,8 +6,13 @@
 // Both operands are K-contiguous ("NT": X [M][K], W [N][K]), the natural
 // layout for MFMA, where each lane feeds 16 contiguous bytes of one row per
 // instruction. The kernels work on 16-byte chunks along K, so one skeleton
-// serves both element types: v_mfma_i32_32x32x32_i8 consumes 32 int8 of a row
-// and v_mfma_f32_32x32x16_bf16 16 bf16, i.e. two chunks either way.
+// serves both element types. The 12-wave kernels multiply 16 x 16 blocks
+// with a 64-byte K step (v_mfma_i32_16x16x64_i8: 64 int8 of a row,
+// v_mfma_f32_16x16x32_bf16: 32 bf16, four chunks either way); the others
+// 32 x 32 blocks with a 32-byte step (v_mfma_i32_32x32x32_i8,
+// v_mfma_f32_32x32x16_bf16, two chunks). Under the GPU's power limit the
+// 16 x 16 forms hold a higher clock: they move half the accumulator bytes
+// per multiply-add.
 //
 // A workgroup computes a BM x BN tile of Y.
 //
@@ -22,17 +27,20 @@
 //     (s_waitcnt vmcnt(n) on a wave's own loads, then s_barrier without a
 //     memory fence, which would drain every prefetch).
 //   MFMA: the W tile feeds the instruction's first operand and the X tile
-//     its second, so C = W X^T and lane l holds token m = l % 32 of a 32x32
-//     block with 4 consecutive output channels per accumulator quad.
-//     Fragments are double-buffered in registers: the next step's LDS reads
-//     overlap the current MFMAs, also across tile boundaries.
+//     its second, so C = W X^T; every accumulator quad holds 4 consecutive
+//     output channels of one token (lane l: token l % 32 of a 32 x 32 block,
+//     or l % 16 of a 16 x 16 block). Fragments are read ahead into
+//     registers: the next step's LDS reads overlap the current MFMAs, also
+//     across tile boundaries.
 //   epilogue: y = float(acc) * (x_scale[m] * w_scale[n]) + bias[n] with one
 //     fma, four channels packed into 8 bytes of bf16 per store.
 //
 // Three kernels share this skeleton:
 //   gemm_2s_kernel  large tiles (288 x 256 with 12 waves, 192 x 256 with 8)
 //                   in two-slot rings; four of the waves also issue the tile
-//                   loads. The default wherever its tiles fill the CUs;
+//                   loads. The default wherever its tiles fill the CUs, and
+//                   made persistent as gemm_pt_kernel where they take more
+//                   than one round of the CUs;
 //   gemm_ws_kernel  warp-specialized: NPROD producer waves only issue the
 //                   tile loads, the WAVES_M x WAVES_N consumer waves only read
 //                   fragments and run MFMAs. With one wave doing both, the
@@ -150,6 +158,39 @@ struct Bf16Op {
         return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, a),
                                                        __builtin_bit_cast(v8bf, b), c, 0, 0, 0);
     }
+};
+
+// The same products on 16 x 16 output blocks with a 64-byte K step
+// (v_mfma_i32_16x16x64_i8, v_mfma_f32_16x16x32_bf16): a quarter of the
+// accumulator bytes per instruction for half the multiply-adds, so half the
+// accumulator traffic per multiply-add. A loop of nothing but these MFMAs on
+// random operands holds a higher clock under the power limit than one of the
+// 32 x 32 forms (4.15 against 2.80 POP/s for int8 in one job).
+struct I8Op16 {
+    using Acc = v4i;
+    __device__ static Acc mma(v4i a, v4i b, Acc c) {
+        return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+    }
+};
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+struct Bf16Op16 {
+    using Acc = v4f;
+    __device__ static Acc mma(v4i a, v4i b, Acc c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, a),
+                                                       __builtin_bit_cast(v8bf, b), c, 0, 0, 0);
+    }
+};
+
+template <class Op>
+struct Narrow;
+template <>
+struct Narrow<I8Op> {
+    using type = I8Op16;
+};
+template <>
+struct Narrow<Bf16Op> {
+    using type = Bf16Op16;
 };
 
 enum Epilogue { kDequantBf16 = 0, kStoreI32 = 1, kBiasBf16 = 2 };
@@ -573,7 +614,7 @@ struct Mma {
         for (int j = 0; j < TJ; ++j)
             xf[buf][j] = *reinterpret_cast<const v4i *>(slot + x_base + j * 32 * BK + chunk * 16);
     }
-    // The MFMA order of Mma1: X fragment outer, W fragments alternating.
+    // X fragment outer, W fragments alternating (as in Mma16::half).
     __device__ __forceinline__ void step(int buf) {
 #pragma unroll
         for (int j = 0; j < TJ; ++j)
@@ -646,8 +687,8 @@ struct Mma2 {
         for (int j = 0; j < TJ; ++j)
             xf[S][j] = *reinterpret_cast<const v4i *>(xslot + x_row + j * 32 * BK + chunk * 16);
     }
-    // X fragment outer, W fragments in alternating order, as in Mma1 (here
-    // 0.1-0.4% faster than W outer at three 192 x 256 shapes, outputs
+    // X fragment outer, W fragments in alternating order, as in Mma16::half
+    // (here 0.1-0.4% faster than W outer at three 192 x 256 shapes, outputs
     // identical).
     template <int S>
     __device__ __forceinline__ void step() {
@@ -692,87 +733,248 @@ struct Mma2 {
     }
 };
 
-// MFMA side of one wave of gemm_2s_kernel with three or more waves per SIMD:
-// fragments read one MFMA step ahead into two register buffers. The other
-// waves of the SIMD cover an LDS read's latency, and the 168 registers a
-// wave has at three waves per SIMD leave no room for four buffers.
-template <class Op, int BK, int TI, int TJ, int SWZ>
-struct Mma1 {
-    static constexpr int CPR = BK / 16;
-    static constexpr int KSTEPS = BK / 32;
-    static_assert(KSTEPS == 4, "four MFMA steps per K tile");
-    typename Op::Acc acc[TI][TJ];
-    v4i wf[2][TI];
-    v4i xf[2][TJ];
-    int x_row, w_row, fhalf, fkey;
+// Epilogue of one wave for the 16 x 16 blocks of Mma16. In block (i, a, j, b)
+// element e of lane l holds channel 32 i + 16 a + 4 (l / 16) + e and token
+// 32 j + 16 b + l % 16 of the wave's tile: each accumulator is 4
+// consecutive channels of one token.
+template <int TI, int TJ, int EPI, bool N_VEC, bool HAS_BIAS>
+struct Epi16 {
+    static constexpr int kRowStride = 64 * TI + 16;
+    static constexpr int kSliceBytes = 32 * kRowStride;
 
-    __device__ __forceinline__ void init(int lane, int mbase, int nbase) {
-        const int frow = lane & 31;
-        fhalf = lane >> 5;
-        fkey = (frow >> SWZ) & (CPR - 1);
-        x_row = (mbase + frow) * BK;
-        w_row = (nbase + frow) * BK;
-#pragma unroll
-        for (int i = 0; i < TI; ++i)
-#pragma unroll
-            for (int j = 0; j < TJ; ++j) acc[i][j] = typename Op::Acc{};
-    }
-    // Fragments of MFMA step s (0..3) of a K tile into buffer s % 2.
-    template <int S>
-    __device__ __forceinline__ void load(const int8_t *xslot, const int8_t *wslot) {
-        const int chunk = (2 * S + fhalf) ^ fkey;
-#pragma unroll
-        for (int i = 0; i < TI; ++i)
-            wf[S & 1][i] = *reinterpret_cast<const v4i *>(wslot + w_row + i * 32 * BK + chunk * 16);
-#pragma unroll
-        for (int j = 0; j < TJ; ++j)
-            xf[S & 1][j] = *reinterpret_cast<const v4i *>(xslot + x_row + j * 32 * BK + chunk * 16);
-    }
-    // The step's MFMAs with the X fragment outer and the W fragments in
-    // alternating order, so that consecutive MFMAs share an operand, also
-    // from one X fragment to the next: fewer operand bits change between
-    // them, and the clock the GPU holds under this load is set by power
-    // (0.5-1.5% faster than W outer at the DiT shapes in one job, outputs
-    // identical).
-    template <int S>
-    __device__ __forceinline__ void step() {
+    // int32 accumulators straight to C (nbase: the wave's first channel in
+    // the whole output). Rows past M fall outside the resource; channels past
+    // N are not stored. N_VEC: N % 4 == 0, so 4 channels go out as one
+    // aligned 16-byte store.
+    template <class Acc>
+    __device__ __forceinline__ void store(const Acc (&acc)[TI][2][TJ][2], void *Yout, int m0,
+                                          int rows_x, int mbase, int nbase, int N,
+                                          int lane) const {
+        static_assert(EPI == kStoreI32, "the int32 store");
+        const int r16 = lane & 15, kg = lane >> 4;
+        const __amdgpu_buffer_rsrc_t ry =
+            make_rsrc(static_cast<int8_t *>(Yout) + static_cast<int64_t>(m0) * N * 4,
+                      static_cast<uint32_t>(rows_x) * N * 4u);
 #pragma unroll
         for (int j = 0; j < TJ; ++j)
 #pragma unroll
-            for (int ii = 0; ii < TI; ++ii) {
-                const int i = (j & 1) ? TI - 1 - ii : ii;
-                acc[i][j] = Op::mma(wf[S & 1][i], xf[S & 1][j], acc[i][j]);
+            for (int b = 0; b < 2; ++b) {
+                const uint32_t row_off = static_cast<uint32_t>(mbase + 32 * j + 16 * b + r16) * N;
+#pragma unroll
+                for (int i = 0; i < TI; ++i)
+#pragma unroll
+                    for (int a = 0; a < 2; ++a) {
+                        const int n = nbase + 32 * i + 16 * a + 4 * kg;
+                        if (N_VEC && n + 3 < N) {
+                            __builtin_amdgcn_raw_buffer_store_b128(acc[i][a][j][b], ry,
+                                                                   (row_off + n) * 4u, 0, 0);
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                const uint32_t off =
+                                    n + e < N ? (row_off + n + e) * 4u : kOutOfRange;
+                                __builtin_amdgcn_raw_buffer_store_b32(acc[i][a][j][b][e], ry, off,
+                                                                      0, 0);
+                            }
+                        }
+                    }
             }
     }
-    // One K tile. On entry buffer 0 holds its step 0. Steps 0..2 read the
-    // next step; then `boundary()`; then, unless LAST, step 3 reads step 0
-    // of the next tile from (nxslot, nwslot) and LOADS loads (`issue(i)`)
-    // go out during it.
+
+    // The bf16 epilogues, one 32-token slice at a time through `stage`
+    // (kSliceBytes of the wave's own), with the operands read from their LDS
+    // copy (tile-local token mbase.., channel nbase..; n0 is the tile's first
+    // channel). Each slice is converted into `stage` as 4-channel groups,
+    // then stored as whole rows: 16 bytes per lane, 8 lanes per 128-byte row.
+    // A wave's LDS accesses execute in order, so the row reads of slice j - 1
+    // are done before slice j is written over them. The operand copies hold
+    // zeros past N; where N % 8 != 0 the rows go out element by element.
+    template <class Acc>
+    __device__ __forceinline__ void store_slices_lds(const Acc (&acc)[TI][2][TJ][2],
+                                                     int8_t *stage, const float *xs_l,
+                                                     const float *ws_l, const uint16_t *b_l,
+                                                     void *Yout, int m0, int rows_x, int mbase,
+                                                     int nbase, int n0, int N, int lane) const {
+        static_assert(EPI != kStoreI32, "row stores are for the bf16 epilogues");
+        constexpr int CPR = 64 * TI / 16;  // 16-byte chunks per row
+        constexpr int ROUNDS = 32 * CPR / 64;
+        static_assert(32 * CPR % 64 == 0, "whole store rounds");
+        const int r16 = lane & 15, kg = lane >> 4;
+        const __amdgpu_buffer_rsrc_t ry =
+            make_rsrc(static_cast<int8_t *>(Yout) + static_cast<int64_t>(m0) * N * 2,
+                      static_cast<uint32_t>(rows_x) * N * 2u);
+        const bool vec8 = (N & 7) == 0;
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) {
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const int t = 16 * b + r16;
+                const float xv = EPI == kDequantBf16 ? xs_l[mbase + 32 * j + t] : 0.0f;
+#pragma unroll
+                for (int i = 0; i < TI; ++i)
+#pragma unroll
+                    for (int a = 0; a < 2; ++a) {
+                        const int c = 32 * i + 16 * a + 4 * kg;
+                        float4 w4 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                        if constexpr (EPI == kDequantBf16)
+                            w4 = *reinterpret_cast<const float4 *>(ws_l + nbase + c);
+                        uint2 b2 = make_uint2(0u, 0u);
+                        if constexpr (HAS_BIAS)
+                            b2 = *reinterpret_cast<const uint2 *>(b_l + nbase + c);
+                        const float wv[4] = {w4.x, w4.y, w4.z, w4.w};
+                        const uint32_t bw[2] = {b2.x, b2.y};
+                        float y[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const float v = static_cast<float>(acc[i][a][j][b][e]);
+                            const float bb = __uint_as_float((e & 1) ? (bw[e >> 1] & 0xffff0000u)
+                                                                     : (bw[e >> 1] << 16));
+                            if constexpr (EPI == kDequantBf16)
+                                y[e] = __builtin_fmaf(v, xv * wv[e], bb);
+                            else
+                                y[e] = v + bb;
+                        }
+                        *reinterpret_cast<v2u *>(stage + t * kRowStride + c * 2) =
+                            v2u{f32x2_to_bf16x2(y[0], y[1]), f32x2_to_bf16x2(y[2], y[3])};
+                    }
+            }
+#pragma unroll
+            for (int r = 0; r < ROUNDS; ++r) {
+                const int id = r * 64 + lane;
+                const int row = id / CPR;
+                const int c = id % CPR;
+                const v4i v = *reinterpret_cast<const v4i *>(stage + row * kRowStride + c * 16);
+                const int n = n0 + nbase + 8 * c;
+                const uint32_t base = static_cast<uint32_t>(mbase + 32 * j + row) * N;
+                if (vec8 || n + 8 <= N) {
+                    const uint32_t off = n + 8 <= N ? (base + n) * 2u : kOutOfRange;
+                    __builtin_amdgcn_raw_buffer_store_b128(v, ry, off, 0, 0);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const uint32_t off = n + e < N ? (base + n + e) * 2u : kOutOfRange;
+                        __builtin_amdgcn_raw_buffer_store_b16(
+                            static_cast<uint16_t>(static_cast<uint32_t>(v[e >> 1]) >>
+                                                  (16 * (e & 1))),
+                            ry, off, 0, 0);
+                    }
+                }
+            }
+        }
+    }
+};
+
+// MFMA side of one wave of gemm_pt_kernel with the 16 x 16 x 64-byte MFMAs:
+// TI x TJ blocks of 32 x 32 (channels x tokens), each 2 x 2 MFMA blocks
+// acc[i][a][j][b] (channels 32 i + 16 a.., tokens 32 j + 16 b..). Lane l
+// reads row l % 16 of a 16-row block, chunk 4 s + l / 16 of the K tile's
+// 64-byte step s; the swizzle key depends on l only, since every block
+// starts on a multiple of 16 rows. Each step runs as two halves, one per
+// token half b, and the fragments are read one half ahead: the W fragments
+// of a step (2 TI) serve both halves, the X fragments (TJ) one half. At
+// most two steps' W fragments and two halves' X fragments are live (56
+// registers for TI = 2, TJ = 3), which the 168 registers of a wave at
+// three waves per SIMD hold.
+template <class Op, int BK, int TI, int TJ, int SWZ>
+struct Mma16 {
+    static constexpr int CPR = BK / 16;
+    static_assert(BK == 128, "two 64-byte MFMA steps per K tile");
+    typename Op::Acc acc[TI][2][TJ][2];
+    v4i wf[2][TI][2];  // by step parity
+    v4i xf[2][TJ];     // by token half
+    int x_off[2], w_off[2];  // the lane's row and swizzled chunk, per step
+
+    __device__ __forceinline__ void init(int lane, int mbase, int nbase) {
+        const int r16 = lane & 15;
+        const int kg = lane >> 4;
+        const int key = (r16 >> SWZ) & (CPR - 1);
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+            const int chunk = (4 * s + kg) ^ key;
+            x_off[s] = (mbase + r16) * BK + chunk * 16;
+            w_off[s] = (nbase + r16) * BK + chunk * 16;
+        }
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+                for (int j = 0; j < TJ; ++j)
+#pragma unroll
+                    for (int b = 0; b < 2; ++b) acc[i][a][j][b] = typename Op::Acc{};
+    }
+    template <int S, int P>
+    __device__ __forceinline__ void load_w(const int8_t *wslot) {
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+                wf[P][i][a] = *reinterpret_cast<const v4i *>(wslot + w_off[S] +
+                                                             (32 * i + 16 * a) * BK);
+    }
+    template <int S, int B>
+    __device__ __forceinline__ void load_x(const int8_t *xslot) {
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+            xf[B][j] = *reinterpret_cast<const v4i *>(xslot + x_off[S] + (32 * j + 16 * B) * BK);
+    }
+    // The fragments that start a K tile: step 0's W and its first token half.
+    template <int S>
+    __device__ __forceinline__ void load(const int8_t *xslot, const int8_t *wslot) {
+        static_assert(S == 0, "a K tile starts at step 0");
+        load_w<0, 0>(wslot);
+        load_x<0, 0>(xslot);
+    }
+    // The MFMAs of token half B with the W fragments of parity P: X fragment
+    // outer, W fragments in alternating order, so that consecutive MFMAs
+    // share an operand, also from one X fragment to the next. Fewer operand
+    // bits then change between them, and under this load the clock is set
+    // by power (with the 32 x 32 blocks: 0.5-1.5% faster than W outer at the
+    // DiT shapes in one job, outputs identical).
+    template <int P, int B>
+    __device__ __forceinline__ void half() {
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+#pragma unroll
+            for (int ii = 0; ii < 2 * TI; ++ii) {
+                const int w = (j & 1) ? 2 * TI - 1 - ii : ii;
+                const int i = w >> 1, a = w & 1;
+                acc[i][a][j][B] = Op::mma(wf[P][i][a], xf[B][j], acc[i][a][j][B]);
+            }
+    }
+    // One K tile. On entry wf[0] and xf[0] hold step 0's W and first token
+    // half. Halves (0,0), (0,1) and (1,0) read the next half's fragments;
+    // then `boundary()`; then, unless LAST, half (1,1) reads the next tile's
+    // first fragments from (nxslot, nwslot) and LOADS loads (`issue(i)`) go
+    // out during it.
     template <bool LAST, int LOADS, class Boundary, class Issue>
     __device__ __forceinline__ void tile(const int8_t *xslot, const int8_t *wslot,
                                          const int8_t *nxslot, const int8_t *nwslot,
                                          Boundary &&boundary, Issue &&issue) {
-        load<1>(xslot, wslot);
-        step<0>();
-        interleave_from<0, TI * TJ, TI + TJ, 0>();
+        constexpr int NM = 2 * TI * TJ;  // MFMAs per half
+        load_x<0, 1>(xslot);
+        half<0, 0>();
+        interleave_from<0, NM, TJ, 0>();
         sched_fence();
-        load<2>(xslot, wslot);
-        step<1>();
-        interleave_from<0, TI * TJ, TI + TJ, 0>();
+        load_w<1, 1>(wslot);
+        load_x<1, 0>(xslot);
+        half<0, 1>();
+        interleave_from<0, NM, 2 * TI + TJ, 0>();
         sched_fence();
-        load<3>(xslot, wslot);
-        step<2>();
-        interleave_from<0, TI * TJ, TI + TJ, 0>();
+        load_x<1, 1>(xslot);
+        half<1, 0>();
+        interleave_from<0, NM, TJ, 0>();
         sched_fence();
         if constexpr (!LAST) {
             boundary();
             sched_fence();
 #pragma unroll
             for (int i = 0; i < LOADS; ++i) issue(i);
-            load<0>(nxslot, nwslot);
+            load_w<0, 0>(nwslot);
+            load_x<0, 0>(nxslot);
         }
-        step<3>();
-        interleave_from<0, TI * TJ, LAST ? 0 : TI + TJ, LOADS>();
+        half<1, 1>();
+        interleave_from<0, NM, LAST ? 0 : 2 * TI + TJ, LOADS>();
         sched_fence();
     }
 };
@@ -996,9 +1198,12 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_2s_kernel(
             dma16(rx, xslot(kt) + (iw + (i - LW) * NI) * 1024, off_x[i - LW] + kt * BK);
     };
 
-    // Fragments two MFMA steps ahead at two waves per SIMD, one at three.
+    // Fragments two MFMA steps ahead at two waves per SIMD (32 x 32 blocks);
+    // at three, the 16 x 16 blocks of Mma16, read one half step ahead.
     constexpr bool AHEAD2 = NW == 8;
-    std::conditional_t<AHEAD2, Mma2<Op, BK, TI, TJ, SWZ>, Mma1<Op, BK, TI, TJ, SWZ>> mma;
+    std::conditional_t<AHEAD2, Mma2<Op, BK, TI, TJ, SWZ>,
+                       Mma16<typename Narrow<Op>::type, BK, TI, TJ, SWZ>>
+        mma;
     // Accumulators in AGPRs at two waves per SIMD. At three, a wave has 168
     // registers, which the compiler splits evenly between VGPRs and AGPRs
     // once a kernel uses AGPRs: 96 accumulators in 84 AGPRs spill. In the
@@ -1040,19 +1245,32 @@ __global__ __launch_bounds__(WAVES_M *WAVES_N * 64) void gemm_2s_kernel(
     }
     mma.template tile<true, 0>(xslot(kt), wslot(kt), xslot(kt), wslot(kt), [] {}, [](int) {});
 
-    EpiT epi;
-    if constexpr (EPI == kStoreI32) {
-        epi.store(mma.acc, Yout, m0, rows_x, mbase, n0 + nbase, N, lane & 31, lane >> 5);
+    if constexpr (!AHEAD2) {
+        Epi16<TI, TJ, EPI, N_VEC, HAS_BIAS> epi;
+        static_assert(SLICED, "12 waves stage 32-token slices");
+        if constexpr (EPI == kStoreI32) {
+            epi.store(mma.acc, Yout, m0, rows_x, mbase, n0 + nbase, N, lane);
+        } else {
+            wait_lgkmcnt0();
+            barrier();  // every wave is done with the ring
+            epi.store_slices_lds(mma.acc, smem + wave * STAGE_BYTES, ep_xs, ep_ws, ep_b, Yout,
+                                 m0, rows_x, mbase, nbase, n0, N, lane);
+        }
     } else {
-        epi.load_lds(ep_xs, ep_ws, ep_b, mbase, nbase, lane & 31, lane >> 5);
-        wait_lgkmcnt0();
-        barrier();  // every wave is done with the ring
-        if constexpr (SLICED)
-            epi.store_slices(mma.acc, smem + wave * STAGE_BYTES, Yout, m0, rows_x, mbase,
-                             n0 + nbase, N, lane & 31, lane >> 5, lane);
-        else
-            epi.store_rows(mma.acc, smem + wave * STAGE_BYTES, Yout, m0, rows_x, mbase,
-                           n0 + nbase, N, lane & 31, lane >> 5, lane);
+        EpiT epi;
+        if constexpr (EPI == kStoreI32) {
+            epi.store(mma.acc, Yout, m0, rows_x, mbase, n0 + nbase, N, lane & 31, lane >> 5);
+        } else {
+            epi.load_lds(ep_xs, ep_ws, ep_b, mbase, nbase, lane & 31, lane >> 5);
+            wait_lgkmcnt0();
+            barrier();  // every wave is done with the ring
+            if constexpr (SLICED)
+                epi.store_slices(mma.acc, smem + wave * STAGE_BYTES, Yout, m0, rows_x, mbase,
+                                 n0 + nbase, N, lane & 31, lane >> 5, lane);
+            else
+                epi.store_rows(mma.acc, smem + wave * STAGE_BYTES, Yout, m0, rows_x, mbase,
+                               n0 + nbase, N, lane & 31, lane >> 5, lane);
+        }
     }
 }
 
@@ -1093,7 +1311,7 @@ __global__ __launch_bounds__(768) void gemm_pt_kernel(
     constexpr int XSLOT = BM * BK;
     constexpr int SLOT = (BM + BN) * BK;
     constexpr int ROWS_PER_DMA = 1024 / BK;  // 8 rows of a panel per 1 KiB block
-    using EpiT = Epi<TI, TJ, EPI, true, HAS_BIAS>;
+    using EpiT = Epi16<TI, TJ, EPI, true, HAS_BIAS>;
     static_assert(12 * EpiT::kSliceBytes <= SLOT, "output slices stage in one slot");
     // epilogue operands: x_scale [320] (BM rounded up to whole 64-lane
     // dword loads), w_scale [256], bias [256] bf16
@@ -1146,11 +1364,12 @@ __global__ __launch_bounds__(768) void gemm_pt_kernel(
         int8_t *slot = slot_ptr(q);
         uint32_t base = off0;
         asm volatile("" : "+v"(base));
+        uint32_t step = panel_step;
+        asm volatile("" : "+s"(step));
         if (i < LW)
-            dma16(tl.rw, slot + XSLOT + (iw + i * NI) * 1024, base + (i * panel_step + kt * BK));
+            dma16(tl.rw, slot + XSLOT + (iw + i * NI) * 1024, base + (i * step + kt * BK));
         else
-            dma16(tl.rx, slot + (iw + (i - LW) * NI) * 1024,
-                  base + ((i - LW) * panel_step + kt * BK));
+            dma16(tl.rx, slot + (iw + (i - LW) * NI) * 1024, base + ((i - LW) * step + kt * BK));
     };
     // The epilogue operands of `tl` into LDS (wave EPW; zero past M / N).
     auto issue_ep = [&](const Tile &tl) {
@@ -1175,7 +1394,7 @@ __global__ __launch_bounds__(768) void gemm_pt_kernel(
             dma4(rb, reinterpret_cast<int8_t *>(ep_b) + 256 * i, 4u * lane + 256u * i);
     };
 
-    Mma1<Op, BK, TI, TJ, SWZ> mma;
+    Mma16<typename Narrow<Op>::type, BK, TI, TJ, SWZ> mma;
     int t = blockIdx.x;
     Tile cur = tile_of(t);
     int q = 0;  // sequence number of the current tile's first K tile
@@ -1197,28 +1416,22 @@ __global__ __launch_bounds__(768) void gemm_pt_kernel(
         barrier();
     };
     for (;;) {
-        // Lane-dependent addresses are rederived per tile from an opaque
-        // copy of the lane id rather than hoisted and held across tiles.
-        int ln = lane;
-        asm volatile("" : "+v"(ln));
         const int tn_ = t + static_cast<int>(gridDim.x);
         const bool has_next = tn_ < total;
         const Tile nxt = tile_of(has_next ? tn_ : t);
         int kt = 0;
-        auto issue_kt2 = [&](int i) { issue_one(cur, kt + 2, q + kt + 2, i); };
-        for (; kt + 2 < KT; ++kt)
+        // The boundary of K tile kt sends K tile kt+2 into the slot it frees;
+        // at kt = KT-2 that is the next tile's first K tile. (One loop for
+        // both keeps the register allocation of the loop body: as a separate
+        // copy after the loop, the tile spilled an accumulator.)
+        auto issue_ahead = [&](int i) {
+            const bool same = kt + 2 < KT;
+            if (same || has_next) issue_one(same ? cur : nxt, same ? kt + 2 : 0, q + kt + 2, i);
+        };
+        for (; kt + 1 < KT; ++kt)
             mma.template tile<false, LOADS>(slot_ptr(q + kt), slot_ptr(q + kt) + XSLOT,
                                             slot_ptr(q + kt + 1), slot_ptr(q + kt + 1) + XSLOT,
-                                            boundary, issue_kt2);
-        // K tile KT-2: its boundary sends the next tile's first K tile into
-        // the slot it frees.
-        auto issue_next0 = [&](int i) {
-            if (has_next) issue_one(nxt, 0, q + KT, i);
-        };
-        mma.template tile<false, LOADS>(slot_ptr(q + kt), slot_ptr(q + kt) + XSLOT,
-                                        slot_ptr(q + kt + 1), slot_ptr(q + kt + 1) + XSLOT,
-                                        boundary, issue_next0);
-        ++kt;
+                                            boundary, issue_ahead);
         mma.template tile<true, 0>(slot_ptr(q + kt), slot_ptr(q + kt) + XSLOT,
                                    slot_ptr(q + kt), slot_ptr(q + kt) + XSLOT, [] {},
                                    [](int) {});
@@ -1228,14 +1441,17 @@ __global__ __launch_bounds__(768) void gemm_pt_kernel(
         wait_lgkmcnt0();
         wait_vmcnt<0>();  // loaders: the next first K tile; EPW: the operands
         barrier();
+        // Lane-dependent addresses are rederived per tile from an opaque
+        // copy of the lane id rather than hoisted and held across the K
+        // tiles (here the epilogue's, below the next tile's fragments').
+        int le = lane;
+        asm volatile("" : "+v"(le));
         EpiT epi;
         if constexpr (EPI == kStoreI32) {
-            epi.store(mma.acc, Yout, cur.m0, cur.rows_x, mbase, cur.n0 + nbase, N, ln & 31,
-                      ln >> 5);
+            epi.store(mma.acc, Yout, cur.m0, cur.rows_x, mbase, cur.n0 + nbase, N, le);
         } else {
             epi.store_slices_lds(mma.acc, stage + wave * EpiT::kSliceBytes, ep_xs, ep_ws, ep_b,
-                                 Yout, cur.m0, cur.rows_x, mbase, nbase, cur.n0, N, ln & 31,
-                                 ln >> 5, ln);
+                                 Yout, cur.m0, cur.rows_x, mbase, nbase, cur.n0, N, le);
         }
         if (!has_next) break;
         wait_lgkmcnt0();

@@ -1739,8 +1739,10 @@ struct TwoSlot {
 //  - K a multiple of 128 bytes (every DiT shape): the candidate that
 //    minimizes the estimated time, rounds of the 256 CUs (one workgroup per
 //    CU) x tile area / rate, where rate is the throughput per output
-//    element at full rounds, measured on the DiT shapes relative to the
-//    288 x 256 tiles. Ties go to the earlier candidate.
+//    element at full rounds, measured at 4608 x 4096 -> 16384 (where every
+//    candidate fills whole rounds) relative to the 288 x 256 tiles, whose
+//    16 x 16 MFMAs make them the fastest per element. Ties go to the earlier
+//    candidate.
 //    * 288 x 256 tiles (tokens x channels), two-slot, 12 waves of 96 x 64:
 //      at M = 4608 = 16 x 288 every DiT shape fills whole rounds (N = 16384:
 //      4, N = 12288: 3, N = 4096: 1);
@@ -1758,9 +1760,9 @@ struct TileChoice {
 };
 constexpr TileChoice kTiles[] = {
     {288, 256, 768, 1.0},
-    {192, 256, 512, 0.94},
-    {192, 128, 512, 0.86},
-    {256, 128, 512, 0.86},
+    {192, 256, 512, 0.82},
+    {192, 128, 512, 0.71},
+    {256, 128, 512, 0.73},
 };
 constexpr int kTileChoices = sizeof(kTiles) / sizeof(kTiles[0]);
 

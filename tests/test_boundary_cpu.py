@@ -133,9 +133,11 @@ def test_gemm_config_picks_tiles_by_rounds(lib):
     # every DiT linear at M = 4608 = 16 x 288 fills whole rounds of 288 x 256
     for N, K in [(16384, 4096), (4096, 16384), (12288, 4096), (4096, 4096)]:
         assert cfg(4608, N, K) == T288 and cfg(4608, N, K, bf16=True) == T288
-    # N = 12290: 784 large tiles take 4 rounds, 1176 of 192 x 256 take 5
-    # (5 x 49152 / 0.94 < 4 x 73728)
-    assert cfg(4545, 12290, 384) == T192
+    # N = 4350: 272 large tiles take 2 rounds, 408 of 192 x 256 take 2 too
+    # (2 x 49152 / 0.82 < 2 x 73728); at N = 12290 (784 tiles, 4 rounds,
+    # against 1176, 5 rounds) the large tiles win (5 x 49152 / 0.82 > 4 x 73728)
+    assert cfg(4545, 4350, 384) == T192
+    assert cfg(4545, 12290, 384) == T288
     # fewer than a round of tiles: the smallest tile
     assert cfg(64, 512, 256) == S192 and cfg(200, 4096, 512) == S192
     # M = 1000: 384 tiles of 192 x 128 take 2 rounds, 256 of 256 x 128 one

@@ -237,7 +237,7 @@ LARGE_RAGGED = [(4571, 16376, 128), (4600, 16375, 256), (4545, 12290, 384),
 # threads) the library reports for it.
 CONFIG_SHAPES = [
     ((4571, 16376, 128), (288, 256, 768)),
-    ((4545, 12290, 384), (192, 256, 512)),
+    ((4545, 4350, 384), (192, 256, 512)),
     ((250, 1000, 256), (192, 128, 512)),
     ((1000, 8190, 256), (256, 128, 512)),
     ((513, 384, 4160), (192, 256, 256)),

@@ -415,11 +415,12 @@ def test_nondefault_stream():
 # --------------------------------------------------------------------------
 
 @pytest.mark.parametrize("M,N,K", [(64, 512, 256), (257, 129, 192), (100, 300, 4160),
-                                   (33, 64, 16384)])
+                                   (33, 64, 16384), (4600, 4093, 256)])
 def test_bf16_linear_small_integers_exact(M, N, K):
     """Integer inputs keep every binary32 partial sum exact, so the result
     must equal the oracle's bit for bit (catches any dropped or repeated
-    K block)."""
+    K block). The last shape runs the 12-wave 288 x 256 kernel with an odd N,
+    whose rows go out element by element."""
     rng = np.random.default_rng([113, M, N, K])
     X = synth.to_bf16_bits(rng.integers(-8, 9, (M, K)).astype(np.float32))
     W = synth.to_bf16_bits(rng.integers(-8, 9, (N, K)).astype(np.float32))

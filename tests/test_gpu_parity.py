@@ -345,6 +345,26 @@ def test_gemm_i32_extremes(K):
     assert abs(int(C[0, 1])) == 127 * 127 * K
 
 
+def test_gemm_i32_extremes_on_the_large_tiles():
+    """The same +-127 codes through the 12-wave 288 x 256 kernel (16 x 16
+    MFMA blocks) at a full DiT output, 4608 x 4096, with K = 32768: every
+    accumulator is +-127^2 K or 0, which the structure of the codes gives in
+    closed form (A's row m is 127 s_m, s_m = +-1; B's rows n % 3 != 0 are all
+    -127, the others alternate +127, -127 along K and sum to 0)."""
+    M, N, K = 4608, 4096, 32768
+    assert ops.w8a8_gemm_config(M, N, K) == (288, 256, 768)
+    A = np.full((M, K), 127, np.int8)
+    A[1::2] = -127
+    B = np.full((N, K), -127, np.int8)
+    B[::3, ::2] = 127
+    C = host(ops.w8a8_gemm_i32(dev(A), dev(B)))
+    sign = np.where(np.arange(M) % 2 == 0, 1, -1).astype(np.int64)
+    rowsum_b = np.where(np.arange(N) % 3 == 0, 0, -127 * K).astype(np.int64)
+    want = (127 * sign)[:, None] * rowsum_b[None, :]
+    assert np.array_equal(C.astype(np.int64), want)
+    assert abs(int(C[0, 1])) == 127 * 127 * K
+
+
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES + [(64, 512, 256)])
 @pytest.mark.parametrize("with_bias", [True, False])
 def test_w8a8_linear_recipe(M, N, K, with_bias):
